@@ -1,0 +1,127 @@
+"""Workload descriptions (shapes, seeds, thresholds) for the five synthetic configs.
+
+Shapes follow the paper's setting: a Llama-2-7B backbone (Sec. V-A), 224x224
+frames cut into 14x14 patches so N = 256 (Sec. III-A), and the OFT variant with
+8-step action chunks of 7 dimensions decoded in parallel (Sec. V-A).
+"""
+from dataclasses import dataclass, field, replace
+from typing import List, Tuple
+
+
+@dataclass
+class VLAConfig:
+    name: str
+    batch: int = 1
+    n_layers: int = 32
+    d_model: int = 4096
+    n_heads: int = 32
+    ffn: int = 11008
+    vocab: int = 32000
+    n_bins: int = 256
+    img: int = 224
+    patch: int = 14
+    n_views: int = 1
+    n_text: int = 20
+    n_proprio: int = 0
+    n_action_q: int = 0
+    n_decode: int = 7           # D action tokens per control step
+    parallel_decode: bool = False   # OFT-style: D head rows from one pass
+    reduce_min: bool = False    # gate on min over positions instead of mean
+    tau: Tuple[int, int] = (249, 250)   # cosine threshold as num/den
+    theta: float = 0.1          # margin threshold
+    reuse_permille: List[int] = field(default_factory=list)  # per layer, empty = 1000 everywhere
+    rms_eps: float = 1e-5
+    rope_theta: float = 10000.0
+    seed: int = 2
+    wscale_log2: int = -5       # linear / embedding weights U[-2^-5, 2^-5)
+    bin_scale_log2: int = -2    # LM-head rows of the action bins
+    norm_full_vocab: bool = True    # softmax normaliser over the full vocabulary
+
+    @property
+    def head_dim(self) -> int:
+        return self.d_model // self.n_heads
+
+    @property
+    def patches_per_side(self) -> int:
+        return self.img // self.patch
+
+    @property
+    def n_patches(self) -> int:
+        return self.n_views * self.patches_per_side ** 2
+
+    @property
+    def patch_dim(self) -> int:
+        return self.patch * self.patch * 3
+
+    @property
+    def n_extra(self) -> int:
+        return self.n_proprio + self.n_action_q
+
+    @property
+    def prompt_len(self) -> int:
+        return self.n_patches + self.n_text + self.n_extra
+
+    @property
+    def bin_lo(self) -> int:
+        return self.vocab - self.n_bins
+
+    @property
+    def n_head_rows(self) -> int:
+        """Rows whose logits the prompt pass produces: the last prompt row, or the
+        action-query rows when the action chunk is decoded in parallel."""
+        return self.n_action_q if self.parallel_decode else 1
+
+    @property
+    def kv_len(self) -> int:
+        """Key slots per layer: the prompt plus the D-1 fed-back action tokens."""
+        if self.parallel_decode:
+            return self.prompt_len
+        return self.prompt_len + self.n_decode - 1
+
+    def permille(self) -> List[int]:
+        if self.reuse_permille:
+            assert len(self.reuse_permille) == self.n_layers
+            return list(self.reuse_permille)
+        return [1000] * self.n_layers
+
+    def with_(self, **kw) -> "VLAConfig":
+        return replace(self, **kw)
+
+
+def config_c1() -> VLAConfig:
+    """Tiny decoder: 2 layers, d=256, 4 heads, FFN 688, vocab 1024 (last 256 are
+    action bins), 112x112 frame -> 64 patches, 8 text tokens, 7 action tokens,
+    tau = 0.99, theta = 0.1."""
+    return VLAConfig(name="C1", n_layers=2, d_model=256, n_heads=4, ffn=688, vocab=1024,
+                     img=112, n_text=8, tau=(99, 100), theta=0.1, seed=1,
+                     wscale_log2=-4, bin_scale_log2=0)
+
+
+def config_c2() -> VLAConfig:
+    """Llama-2-7B shape, 256 visual + 20 text tokens, one step at 50% reuse,
+    then 7-token autoregressive action decode."""
+    return VLAConfig(name="C2", seed=2)
+
+
+def config_c3() -> VLAConfig:
+    """7B shape over a 50-frame moving-rectangle episode; per-layer reuse decays
+    linearly 80% -> 20%; tau = 0.996 (the paper's default); theta = 0.1."""
+    L = 32
+    q = [800 - (600 * l) // (L - 1) for l in range(L)]
+    return VLAConfig(name="C3", seed=3, reuse_permille=q, tau=(249, 250), theta=0.1)
+
+
+def config_c4() -> VLAConfig:
+    """7B shape with a parallel-decoded action chunk: two views (512 visual
+    tokens), 1 proprio row, 20 text tokens, 56 action-query rows (8 steps x 7
+    dims) decoded in one pass; gate on the minimum margin."""
+    return VLAConfig(name="C4", seed=4, n_views=2, n_proprio=1, n_action_q=56,
+                     n_decode=56, parallel_decode=True, reduce_min=True)
+
+
+def config_c5() -> VLAConfig:
+    """7B shape, 256 visual tokens, 16 independent episodes batched per step."""
+    return VLAConfig(name="C5", seed=5, batch=16)
+
+
+ALL_CONFIGS = {"C1": config_c1, "C2": config_c2, "C3": config_c3, "C4": config_c4, "C5": config_c5}
