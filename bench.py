@@ -1,0 +1,208 @@
+#!/usr/bin/env python3
+"""Control steps/s of the Gated VLA-Cache hot path on one MI355X.
+
+One control step (Alg. 1) on a Llama-2-7B-shaped VLA decoder with random
+bf16 weights and seeded synthetic frames:
+  margin gate on the previous step's margins  ->  Stage 1 static-patch
+  selection  ->  prompt pass over the recomputed rows only  ->  7-token
+  autoregressive action decode.
+The workload keeps the cache at every step (the gate is evaluated and its
+decision reported, but not applied), so every timed step reuses exactly the
+128 static patches of 256 (50%).
+
+Prints one JSON line.  --gpus N with N > 1 is refused: the path runs on one GPU.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
+BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    return ap.parse_args()
+
+
+def layer_weight_bytes(cfg):
+    d, F = cfg.d_model, cfg.ffn
+    return (4 * d * d + 3 * d * F) * 2
+
+
+def cpu_baseline(cfg, w_cpu, si, n_static):
+    """The oracle on a one-layer slice of the same step, scaled to 32 layers."""
+    import numpy as np
+    from oracle.vla import OracleVLA
+    from oracle.llama import head_row
+    cfg1 = cfg.with_(n_layers=1)
+    o = OracleVLA(cfg1, w_cpu)
+    ft, fp = si["frame_t"].numpy(), si["frame_prev"].numpy()
+    ids = si["text_ids"].numpy()
+    t0 = time.perf_counter()
+    masks, ns = o.select_static(ft, fp)
+    t_sel = time.perf_counter() - t0
+    o.valid[:] = True
+    t0 = time.perf_counter()
+    o.step_prefill(ft, ids, None, masks)
+    o.decode_actions()
+    t_slice = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    for _ in range(cfg.n_decode):
+        head_row(o.H[1, 0, cfg.prompt_len - 1], o.w["final_norm"], o.w["lm_head"], cfg.rms_eps)
+    t_head = time.perf_counter() - t0
+    t_step = t_sel + cfg.n_layers * (t_slice - t_head) + t_head
+    cores = len(os.sched_getaffinity(0))
+    omp = os.environ.get("OMP_NUM_THREADS")
+    if omp and omp.isdigit():
+        cores = min(cores, int(omp))
+    return {"value": 1.0 / t_step, "unit": "control steps/s", "cores": cores, "kind": "oracle",
+            "sample": "float64 oracle on 1 of the 32 decoder layers (prompt pass over the %d recomputed rows and "
+                      "the 6 single-token decode passes), plus Stage 1 and the 7 LM-head rows; per-layer time "
+                      "scaled to 32 layers; measured %.1f s" % (int(o.recomputed[0, 0]), t_sel + t_slice + t_head),
+            "seconds_per_step": t_step}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print("bench.py runs the hot path on one GPU; --gpus %d is not supported (multi-GPU sharding is "
+              "described in DESIGN.md, not built)" % args.gpus, file=sys.stderr)
+        return 2
+    import torch
+    import synth
+    from paper_2608_10824_amd import gvc
+    from paper_2608_10824_amd.session import Session
+
+    cfg = synth.config_c2()
+    n_static = 128
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    w = synth.model_weights(cfg, device=dev)
+    si = synth.step_inputs(cfg, n_static)
+    w_cpu = None
+    if not args.no_cpu_baseline:
+        w_cpu = {k: v.cpu() for k, v in w.items() if k != "layers"}
+        w_cpu["layers"] = [{k: v.cpu() for k, v in w["layers"][0].items()}]
+    s = Session(cfg, w, device=dev)
+    torch.cuda.synchronize()
+    del w
+    torch.cuda.empty_cache()
+
+    fp, ft = si["frame_prev"].to(dev), si["frame_t"].to(dev)
+    ids = si["text_ids"].to(dev)
+    stream = s.stream
+
+    # first step: no cache yet, full pass
+    s.step_prefill(fp, ids)
+    s.decode_actions()
+
+    fired = []
+
+    def control_step(ev=None):
+        m, fire = s.margin_gate(force=[0])      # Alg. 1 test on step t-1; the workload keeps the cache
+        fired.append(bool(fire[0]))
+        mask, _ = s.select_static(ft, fp)
+        if ev:
+            ev[0].record(stream)
+        s.step_prefill(ft, ids, None, mask)
+        if ev:
+            ev[1].record(stream)
+        s.decode_actions()
+        if ev:
+            ev[2].record(stream)
+
+    for _ in range(args.warmup):
+        control_step()
+    torch.cuda.synchronize()
+
+    # timed region: the steps/s value
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        control_step()
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    ms_step = dt * 1e3 / args.steps
+    rows = s.read(gvc.STATE_ROWS).cpu().tolist()
+
+    # second region, same steps: phase events and the dominant kernel's launches
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    launches_per_step = (cfg.n_decode - 1) * cfg.n_layers
+    gvc.profile_begin(s.ctx, gvc.K_DECODE_GU, launches_per_step * args.steps + 8)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        control_step(evs[i])
+    torch.cuda.synchronize()
+    dt2 = time.perf_counter() - t0
+    gu_ms, gu_n = gvc.profile_end(s.ctx)
+    prefill_ms = sum(e[0].elapsed_time(e[1]) for e in evs) / args.steps
+    decode_ms = sum(e[1].elapsed_time(e[2]) for e in evs) / args.steps
+
+    d, F, V, L, P = cfg.d_model, cfg.ffn, cfg.vocab, cfg.n_layers, cfg.prompt_len
+    # dominant kernel: decode gate/up GEMM, one launch per layer per decode pass
+    gu_bytes = 2 * F * d * 2 + d * 2 + F * 2
+    gu_avg_s = gu_ms / 1e3 / max(gu_n, 1)
+    gu_gbs = gu_bytes / gu_avg_s / 1e9
+    # prompt pass algorithmic work: the recomputed rows of every layer, their
+    # attention over the keys up to each row's position, and the head row
+    mask = s.mask[0].cpu().numpy().astype(bool)              # [L][N]
+    M = rows[0]
+    prefill_flops = 2 * V * d
+    for l in range(L):
+        qpos = [p for p in range(P) if not (1 <= p <= cfg.n_patches and mask[l][p - 1])]
+        prefill_flops += 2 * len(qpos) * (4 * d * d + 3 * d * F) + 2 * sum(2 * (p + 1) * d for p in qpos)
+    prefill_bytes = L * layer_weight_bytes(cfg) + V * d * 2
+    decode_bytes = (cfg.n_decode - 1) * (L * layer_weight_bytes(cfg) + V * d * 2
+                                         + L * 2 * 2 * d * (P + cfg.n_decode))
+    out = {
+        "metric": "control steps/s at 7B, 256 visual tokens, 50% reuse; prefill MFMA util %",
+        "value": args.steps / dt,
+        "unit": "control steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "Llama-2-7B-shaped VLA decoder (32 layers, d=4096, 32 heads, FFN 11008, vocab "
+                               "32000, 256 action bins), random bf16 weights; 224x224 frame = 256 visual + 20 text "
+                               "tokens; 128 static patches reused (50%); 7-token autoregressive action decode",
+                   "batch": 1, "prompt_len": P, "recomputed_rows_per_layer": M, "decode_tokens": cfg.n_decode},
+        "prefill_ms": prefill_ms,
+        "prefill_tflops": prefill_flops / (prefill_ms / 1e3) / 1e12,
+        "prefill_mfma_util_pct": 100.0 * prefill_flops / (prefill_ms / 1e3) / 1e12 / BF16_PEAK_TFLOPS,
+        "prefill_hbm_gbs": prefill_bytes / (prefill_ms / 1e3) / 1e9,
+        "decode_ms": decode_ms,
+        "decode_gbs": decode_bytes / (decode_ms / 1e3) / 1e9,
+        "decode_hbm_frac": decode_bytes / (decode_ms / 1e3) / 1e9 / HBM_PEAK_GBS,
+        "gate_fired_steps": sum(fired),
+        "roofline": {"bound": "hbm", "achieved": gu_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": gu_gbs / HBM_PEAK_GBS, "traffic": None,
+                     "kernel": "k_gemm<1,8,EPI_SILU> (decode gate/up projection, M=1)",
+                     "bytes_per_launch": gu_bytes, "avg_launch_us": gu_avg_s * 1e6, "launches": gu_n,
+                     "region_ms_per_step": dt2 * 1e3 / args.steps},
+    }
+    if not args.no_cpu_baseline:
+        cb = cpu_baseline(cfg, w_cpu, si, n_static)
+        out["cpu_baseline"] = cb
+    s.close()
+    print(json.dumps(out))
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,237 @@
+/*
+ * gvc.h - C ABI of the Gated VLA-Cache control-step library for MI355X (gfx950).
+ *
+ * One control step of a Llama-2-shaped vision-language-action decoder in which
+ * visually static image-patch tokens reuse the K/V they had at the previous
+ * frame, and a logit-margin gate forces a full recompute when the model's
+ * action confidence was low (arxiv 2608.10824, Alg. 1).  A step is:
+ *
+ *   gvc_margin_gate      Eq. 1 margin of the previous step, compared with theta
+ *                        (Alg. 1, first test); invalidates fired episodes.
+ *   gvc_select_static    Stage 1 patch cosine similarity of I_t vs I_{t-1}
+ *                        (Sec. III-B) with a per-layer reuse proportion (Stage 3).
+ *   gvc_step_prefill     the prompt pass over the non-reused tokens only, with
+ *                        fresh K/V scattered into the persistent cache
+ *                        (Alg. 1, partial or full forward pass).
+ *   gvc_decode_actions   autoregressive decode of the D action tokens (Sec. III-A,
+ *                        Alg. 1 last step), recording each token's margin.
+ *
+ * Conventions shared by every call:
+ *  - Every function returns GVC_OK (0) or a GVC_E* code; gvc_last_error() gives
+ *    a thread-local message for the last failure.  No C++ exception crosses
+ *    this boundary.
+ *  - "dev" pointers are device memory of the GPU current when gvc_init_cache
+ *    ran; "host" pointers are ordinary host memory.  The caller owns all
+ *    device memory (weights, arenas, inputs, outputs); the library owns only
+ *    the host-side context.  Device pointers must be 256-byte aligned.
+ *  - Work is enqueued on the HIP stream given to gvc_init_cache, in call
+ *    order.  Calls return before the GPU finishes except gvc_margin_gate,
+ *    gvc_step_prefill (it waits for the per-layer row counts, a few bytes,
+ *    before enqueuing the layers) and gvc_read_state.
+ *  - No call allocates device memory; gvc_init_cache allocates only the
+ *    host context.
+ *  - A context is not thread-safe; calls on one context must not overlap.
+ *
+ * Key slots per layer: kv_len = P + D - 1 (autoregressive) or P (parallel),
+ * padded to kv_pad = kv_len rounded up to a multiple of 32.
+ *
+ * Data layout of the model (all row-major, bf16 = IEEE bfloat16 bits):
+ *  Token order of one episode's prompt of P = N + n_text + n_proprio + n_action_q
+ *  rows, row index = position: [text 0] [N visual tokens, view-major, raster]
+ *  [text 1..n_text-1] [proprio rows] [action-query rows].  Only visual tokens
+ *  can be reused.
+ */
+#ifndef GVC_H
+#define GVC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum gvc_status {
+  GVC_OK = 0,
+  GVC_EINVAL = 1,   /* null pointer, bad shape or threshold, NaN theta */
+  GVC_ESTATE = 2,   /* call out of order (e.g. decode before any prefill) */
+  GVC_ENOMEM = 3,   /* an arena is smaller than gvc_sizes reported */
+  GVC_EDEVICE = 4   /* a HIP call failed; see gvc_last_error() */
+};
+
+enum gvc_reduce { GVC_REDUCE_MEAN = 0, GVC_REDUCE_MIN = 1 };
+
+enum gvc_state_item {
+  GVC_STATE_H = 0,       /* fp32 [B][P][d]  hidden state entering layer `layer` (0..L) */
+  GVC_STATE_K = 1,       /* bf16 [B][n_heads][kv_pad][head_dim] keys of layer `layer` (after RoPE) */
+  GVC_STATE_V = 2,       /* bf16 [B][n_heads][head_dim][kv_pad] values of layer `layer` (dim-major) */
+  GVC_STATE_HEAD_LOGITS = 3, /* fp32 [B][n_head_rows][V] logits of the last prompt pass */
+  GVC_STATE_VALID = 4,   /* int32 [B] cache-valid flags */
+  GVC_STATE_ROWS = 5,    /* int32 [L]: rows recomputed per layer by the last prompt pass */
+  GVC_STATE_MARGINS = 6  /* fp32 [B][D] per-position margins of the last decode */
+};
+
+/* Model and workload shape.  Llama-2 block (Sec. V-A backbone): pre-norm
+ * RMSNorm, rotary embedding pairing dim i with i + head_dim/2, multi-head
+ * attention, SwiGLU; no biases. */
+typedef struct gvc_desc {
+  int32_t batch;          /* B independent episodes stepped together */
+  int32_t n_layers;       /* L */
+  int32_t d_model;        /* d, a multiple of 64 */
+  int32_t n_heads;        /* head_dim = d / n_heads must be 64 or 128 */
+  int32_t ffn;            /* SwiGLU hidden width F */
+  int32_t vocab;          /* V; the last n_bins ids are the action bins */
+  int32_t n_bins;         /* 2 <= n_bins <= vocab; vocab a multiple of 16 */
+  int32_t img;            /* frame side in pixels (square frames) */
+  int32_t patch;          /* patch side p; img % p == 0; N = n_views (img/p)^2 */
+  int32_t n_views;        /* camera views per frame */
+  int32_t n_text;         /* language tokens, >= 1 */
+  int32_t n_proprio;      /* proprio rows (given embeddings) */
+  int32_t n_action_q;     /* action-query rows (given embeddings) */
+  int32_t n_decode;       /* D action tokens per step */
+  int32_t parallel_decode;/* 0: D-1 single-token passes follow the prompt pass;
+                             1: the D action-query rows give the D positions */
+  int32_t norm_full_vocab;/* 1: softmax normaliser over all V ids; 0: over the bins */
+  float rms_eps;          /* RMSNorm epsilon (1e-5 for Llama-2) */
+  float rope_theta;       /* rotary base (10000 for Llama-2) */
+} gvc_desc;
+
+/* bf16 weights of one decoder layer, canonical [out_features][in_features]. */
+typedef struct gvc_layer_weights {
+  const void* wq;         /* dev bf16 [d][d] */
+  const void* wk;         /* dev bf16 [d][d] */
+  const void* wv;         /* dev bf16 [d][d] */
+  const void* wo;         /* dev bf16 [d][d] */
+  const void* wg;         /* dev bf16 [F][d]  SwiGLU gate */
+  const void* wu;         /* dev bf16 [F][d]  SwiGLU up */
+  const void* wd;         /* dev bf16 [d][F]  SwiGLU down */
+  const void* attn_norm;  /* dev bf16 [d] RMSNorm gain before attention */
+  const void* ffn_norm;   /* dev bf16 [d] RMSNorm gain before the FFN */
+} gvc_layer_weights;
+
+typedef struct gvc_weights {
+  const void* embed;       /* dev bf16 [V][d] token embedding table */
+  const void* patch_proj;  /* dev bf16 [d][p*p*3]: visual row = (pixels/255) . W^T (Sec. III-A) */
+  const void* lm_head;     /* dev bf16 [V][d] */
+  const void* final_norm;  /* dev bf16 [d] */
+  const gvc_layer_weights* layers; /* host array of L entries */
+} gvc_weights;
+
+typedef struct gvc_ctx gvc_ctx;
+
+/* Device bytes the caller must provide.  weight_bytes: packed weights (written
+ * once by gvc_init_cache); state_bytes: the persistent cache (H, K, V, flags,
+ * margins); workspace_bytes: per-step scratch.  Any may be NULL.
+ * Errors: GVC_EINVAL for a shape the kernels do not support. */
+int32_t gvc_sizes(const gvc_desc* desc, size_t* weight_bytes, size_t* state_bytes,
+                  size_t* workspace_bytes);
+
+/* Binds a context to the current GPU and to `stream` (a hipStream_t, NULL =
+ * the null stream).  Packs the canonical weights into `weight_arena` (the
+ * canonical tensors are not referenced afterwards and may be freed once the
+ * stream has run the packing), zeroes the state so every episode starts with
+ * an invalid cache (the first step is a full pass, Alg. 1) and zeroes the
+ * workspace.  *out receives the context.  Errors: GVC_EINVAL (null pointer,
+ * unsupported shape), GVC_ENOMEM (an arena too small), GVC_EDEVICE. */
+int32_t gvc_init_cache(const gvc_desc* desc, const gvc_weights* weights,
+                       void* weight_arena, size_t weight_bytes,
+                       void* state, size_t state_bytes,
+                       void* workspace, size_t workspace_bytes,
+                       void* stream, gvc_ctx** out);
+
+/* Stage 1 + applied Stage 3 (Sec. III-B).  frame_t, frame_prev: dev uint8
+ * [B][n_views][img][img][3].  A patch (p x p x 3 values, H,W,C order) is static
+ * iff its cosine with the same patch of frame_prev exceeds tau_num/tau_den,
+ * decided exactly in integer arithmetic (both patches all-zero: static;
+ * exactly one all-zero: not static).  Static patches are ranked by cosine,
+ * highest first, ties to the lower index; layer l reuses the first
+ * floor(reuse_permille[l] * |S| / 1000) of them.
+ * reuse_permille: host int32 [L] in [0, 1000], or NULL for 1000 everywhere.
+ * reuse_mask: dev uint8 [B][L][N] out (1 = reuse at that layer).
+ * n_static: dev int32 [B] out (|S|), or NULL.
+ * Errors: GVC_EINVAL (null frame/mask, 0 < tau_num <= tau_den violated,
+ * permille out of range). */
+int32_t gvc_select_static(gvc_ctx* ctx, const uint8_t* frame_t, const uint8_t* frame_prev,
+                          int32_t tau_num, int32_t tau_den, const int32_t* reuse_permille,
+                          uint8_t* reuse_mask, int32_t* n_static);
+
+/* The prompt pass (Alg. 1, full or partial forward).  frame_t: dev uint8
+ * [B][n_views][img][img][3]; text_ids: dev int32 [B][n_text] (ids < V);
+ * extra_rows: dev fp32 [B][n_proprio + n_action_q][d] given embeddings, or
+ * NULL when there are none; reuse_mask: dev uint8 [B][L][N] from
+ * gvc_select_static, or NULL for a full pass.  Episodes whose cache is
+ * invalid run full whatever the mask says.  A visual token reused at layer l
+ * keeps its K/V and its layer-l output from the last pass that computed them;
+ * every other row is recomputed and its K/V overwrite the cache.  Afterwards
+ * every episode's cache is valid and the head logits are ready for
+ * gvc_decode_actions.  Blocks until the per-layer row counts are known.
+ * Errors: GVC_EINVAL (null frame or ids, missing extra rows), GVC_EDEVICE. */
+int32_t gvc_step_prefill(gvc_ctx* ctx, const uint8_t* frame_t, const int32_t* text_ids,
+                         const float* extra_rows, const uint8_t* reuse_mask);
+
+/* Action decode (Sec. III-A; Eq. 1 inputs).  For each of the D positions:
+ * greedy token = the highest action-bin logit (ties to the lower id) and
+ * margin = p1 - p2 of the two highest bin probabilities under the softmax
+ * over the whole vocabulary (over the bins if norm_full_vocab == 0).
+ * Autoregressive mode runs D-1 single-token passes feeding back each token
+ * (or forced_tokens[b][j] when given); parallel mode reads the action-query
+ * rows of the prompt pass.  tokens_out: dev int32 [B][D]; margins_out: dev
+ * fp32 [B][D]; logits_out: dev fp32 [B][D][V] or NULL; forced_tokens: dev
+ * int32 [B][D] or NULL.  The margins are also kept in the state for
+ * gvc_margin_gate.  Errors: GVC_ESTATE if no prompt pass ran since the last
+ * decode, GVC_EINVAL, GVC_EDEVICE. */
+int32_t gvc_decode_actions(gvc_ctx* ctx, int32_t* tokens_out, float* margins_out,
+                           float* logits_out, const int32_t* forced_tokens);
+
+/* The gate of Alg. 1: m_b = mean (Eq. 1) or min over the last decode's D
+ * margins of episode b; fire_b = !(m_b >= theta) (strict <, NaN fires);
+ * a fired episode's cache becomes invalid so its next prompt pass is full.
+ * force: host int8 [B] (-1: decide, 0: keep, 1: fire) or NULL.
+ * margin_out: host fp32 [B]; fire_out: host uint8 [B] (either may be NULL).
+ * Synchronizes the stream.  Errors: GVC_ESTATE before any decode, GVC_EINVAL
+ * (NaN theta, bad reduce), GVC_EDEVICE. */
+int32_t gvc_margin_gate(gvc_ctx* ctx, float theta, int32_t reduce, float* margin_out,
+                        uint8_t* fire_out, const int8_t* force);
+
+/* Invalidates episode b's cache (b = -1: all episodes). Errors: GVC_EINVAL. */
+int32_t gvc_invalidate(gvc_ctx* ctx, int32_t b);
+
+/* Copies one state item (enum gvc_state_item) of layer `layer` into dst (dev),
+ * then synchronizes the stream.  dst_bytes must hold the item.
+ * Errors: GVC_EINVAL (bad item/layer, short dst), GVC_EDEVICE. */
+int32_t gvc_read_state(gvc_ctx* ctx, int32_t item, int32_t layer, void* dst, size_t dst_bytes);
+
+/* Size in bytes of a state item (see gvc_read_state). */
+size_t gvc_state_item_bytes(const gvc_ctx* ctx, int32_t item);
+
+/* Kernel classes for gvc_profile_begin: the launches of one class are
+ * bracketed by HIP events on the context's stream. */
+enum gvc_kernel_class {
+  GVC_K_DECODE_QKV = 0, GVC_K_DECODE_ATTN = 1, GVC_K_DECODE_O = 2, GVC_K_DECODE_GU = 3,
+  GVC_K_DECODE_DOWN = 4, GVC_K_DECODE_HEAD = 5,
+  GVC_K_PREFILL_QKV = 6, GVC_K_PREFILL_ATTN = 7, GVC_K_PREFILL_O = 8, GVC_K_PREFILL_GU = 9,
+  GVC_K_PREFILL_DOWN = 10, GVC_K_PREFILL_HEAD = 11, GVC_K_EMBED = 12, GVC_K_NORM = 13,
+  GVC_K_SELECT = 14, GVC_K_COUNT = 15
+};
+
+/* Starts timing every launch of kernel class `cls` (enum gvc_kernel_class):
+ * a start and a stop event are recorded on the context's stream around each
+ * such launch, for at most `max_launches` launches.  Creates the events (host
+ * call; do not use inside a captured region).  Errors: GVC_EINVAL, GVC_EDEVICE. */
+int32_t gvc_profile_begin(gvc_ctx* ctx, int32_t cls, int32_t max_launches);
+
+/* Stops timing, synchronizes the stream and returns the summed elapsed time
+ * of the recorded launches (milliseconds) and their count.  Errors:
+ * GVC_ESTATE if no profile is running, GVC_EDEVICE. */
+int32_t gvc_profile_end(gvc_ctx* ctx, double* total_ms, int32_t* launches);
+
+/* Frees the host context.  Device memory stays with the caller. */
+int32_t gvc_destroy(gvc_ctx* ctx);
+
+/* Thread-local text of the last error ("" if none). */
+const char* gvc_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* GVC_H */

@@ -1,0 +1,684 @@
+// Host side of libgvc: shape validation, arena planning, weight packing and
+// the per-call launch sequences of the C ABI declared in include/gvc.h.
+#include "gvc.h"
+#include "gvc_kernels.h"
+
+#include <algorithm>
+#include <cmath>
+#include <cstdlib>
+#include <cstring>
+#include <string>
+#include <vector>
+
+using namespace gvc;
+
+namespace {
+
+thread_local std::string g_err;
+
+int32_t fail(int32_t code, const std::string& msg) {
+  g_err = msg;
+  return code;
+}
+
+#define HIP_TRY(x)                                                                      \
+  do {                                                                                  \
+    hipError_t e_ = (x);                                                                \
+    if (e_ != hipSuccess) return fail(GVC_EDEVICE, std::string(#x) + ": " + hipGetErrorString(e_)); \
+  } while (0)
+
+constexpr size_t kAlign = 256;
+constexpr size_t kPartialBytes = size_t(64) << 20;   // split-K partial tiles
+constexpr int kTickets = 1 << 16;
+constexpr int kTargetWgs = 1024;
+
+struct Bump {
+  size_t off = 0;
+  size_t take(size_t bytes) {
+    const size_t o = off;
+    off += (bytes + kAlign - 1) / kAlign * kAlign;
+    return o;
+  }
+};
+
+struct Packed {
+  size_t off = 0;
+  int N = 0, K = 0, Nblk = 0, KB = 0;
+};
+
+struct Plan {
+  gvc_desc d{};
+  int B, L, D, H, dh, F, V, N, P, kv_len, kv_pad, head_rows, patch_dim, n_extra, bin_lo;
+  int KBd, KBf, KBp, KBx;
+  int Mmax, Mp;
+  // weight arena
+  std::vector<Packed> wq, wk, wv, wo, wg, wu, wd;
+  Packed patch, lm;
+  size_t embed_off, gains_off, final_gain_off, weight_bytes;
+  // state
+  size_t H_off, K_off, V_off, valid_off, margins_off, head_logits_off, rowcount_off, state_bytes;
+  size_t layer_kv_elems;
+  // workspace
+  size_t rows_off, counts_off, epc_off, epo_off, stats_off, x_off, q_off, o_off, r_off, act_off, xdec_off,
+      logits_off, part_off, tickets_off, rope_off, decrows_off, headrows_off, tokens_off, gate_m_off, gate_f_off,
+      ws_bytes;
+};
+
+Packed plan_packed(Bump& a, int N, int K) {
+  Packed p;
+  p.N = N; p.K = K;
+  p.Nblk = (N + 15) / 16;
+  p.KB = (K + 31) / 32;
+  p.off = a.take((size_t)p.Nblk * 16 * p.KB * 32 * 2);
+  return p;
+}
+
+int32_t make_plan(const gvc_desc* dsc, Plan& p) {
+  if (!dsc) return fail(GVC_EINVAL, "null desc");
+  const gvc_desc& d = *dsc;
+  p.d = d;
+  if (d.batch < 1 || d.batch > 64) return fail(GVC_EINVAL, "batch must be in [1, 64]");
+  if (d.n_layers < 1 || d.n_layers > 128) return fail(GVC_EINVAL, "n_layers must be in [1, 128]");
+  if (d.d_model < 64 || d.d_model % 64) return fail(GVC_EINVAL, "d_model must be a positive multiple of 64");
+  if (d.n_heads < 1 || d.d_model % d.n_heads) return fail(GVC_EINVAL, "n_heads must divide d_model");
+  const int dh = d.d_model / d.n_heads;
+  if (dh != 64 && dh != 128) return fail(GVC_EINVAL, "head_dim must be 64 or 128");
+  if (d.ffn < 16 || d.ffn % 16) return fail(GVC_EINVAL, "ffn must be a positive multiple of 16");
+  if (d.n_bins < 2 || d.n_bins > d.vocab || d.vocab % 16) return fail(GVC_EINVAL, "bad vocab / n_bins");
+  if (d.patch < 1 || d.img < d.patch || d.img % d.patch) return fail(GVC_EINVAL, "img must be a multiple of patch");
+  if (d.n_views < 1) return fail(GVC_EINVAL, "n_views must be >= 1");
+  if (d.n_text < 1 || d.n_proprio < 0 || d.n_action_q < 0) return fail(GVC_EINVAL, "bad token counts");
+  if (d.n_decode < 1) return fail(GVC_EINVAL, "n_decode must be >= 1");
+  if (d.parallel_decode && d.n_action_q != d.n_decode)
+    return fail(GVC_EINVAL, "parallel decode needs n_action_q == n_decode");
+  if (!(d.rms_eps >= 0.f) || !(d.rope_theta > 0.f)) return fail(GVC_EINVAL, "bad rms_eps / rope_theta");
+  p.B = d.batch; p.L = d.n_layers; p.D = d.n_decode; p.H = d.n_heads; p.dh = dh; p.F = d.ffn; p.V = d.vocab;
+  const int side = d.img / d.patch;
+  p.N = d.n_views * side * side;
+  if (p.N > 1024) return fail(GVC_EINVAL, "at most 1024 patches per frame");
+  p.n_extra = d.n_proprio + d.n_action_q;
+  p.P = p.N + d.n_text + p.n_extra;
+  p.kv_len = d.parallel_decode ? p.P : p.P + p.D - 1;
+  p.kv_pad = (p.kv_len + 31) / 32 * 32;
+  if (p.kv_pad > 8192) return fail(GVC_EINVAL, "sequence too long");
+  p.head_rows = d.parallel_decode ? d.n_action_q : 1;
+  p.patch_dim = d.patch * d.patch * 3;
+  p.bin_lo = d.vocab - d.n_bins;
+  p.KBd = d.d_model / 32;
+  p.KBf = (d.ffn + 31) / 32;
+  p.KBp = (p.patch_dim + 31) / 32;
+  p.KBx = std::max(p.KBd, p.KBp);
+  p.Mmax = std::max(p.B * p.P, p.B);
+  p.Mp = (p.Mmax + 15) / 16 * 16;
+
+  Bump w;
+  for (int l = 0; l < p.L; ++l) {
+    p.wq.push_back(plan_packed(w, d.d_model, d.d_model));
+    p.wk.push_back(plan_packed(w, d.d_model, d.d_model));
+    p.wv.push_back(plan_packed(w, d.d_model, d.d_model));
+    p.wo.push_back(plan_packed(w, d.d_model, d.d_model));
+    p.wg.push_back(plan_packed(w, d.ffn, d.d_model));
+    p.wu.push_back(plan_packed(w, d.ffn, d.d_model));
+    p.wd.push_back(plan_packed(w, d.d_model, d.ffn));
+  }
+  p.patch = plan_packed(w, d.d_model, p.patch_dim);
+  p.lm = plan_packed(w, d.vocab, d.d_model);
+  p.embed_off = w.take((size_t)d.vocab * d.d_model * 2);
+  p.gains_off = w.take((size_t)p.L * 2 * d.d_model * 4);
+  p.final_gain_off = w.take((size_t)d.d_model * 4);
+  p.weight_bytes = w.off;
+
+  Bump s;
+  p.layer_kv_elems = (size_t)p.B * p.H * p.kv_pad * dh;
+  p.H_off = s.take((size_t)(p.L + 1) * p.B * p.P * d.d_model * 4);
+  p.K_off = s.take(p.layer_kv_elems * p.L * 2);
+  p.V_off = s.take(p.layer_kv_elems * p.L * 2);
+  p.valid_off = s.take((size_t)p.B * 4);
+  p.margins_off = s.take((size_t)p.B * p.D * 4);
+  p.head_logits_off = s.take((size_t)p.B * p.head_rows * p.V * 4);
+  p.rowcount_off = s.take((size_t)p.L * 4);
+  p.state_bytes = s.off;
+
+  Bump k;
+  const size_t tot = (size_t)p.B * p.P;
+  p.rows_off = k.take((size_t)p.L * 3 * tot * 4);
+  p.counts_off = k.take((size_t)p.L * 4);
+  p.epc_off = k.take((size_t)p.L * p.B * 4);
+  p.epo_off = k.take((size_t)p.L * p.B * 4);
+  p.stats_off = k.take((size_t)p.B * p.N * 3 * 4);
+  p.x_off = k.take((size_t)p.Mp * p.KBx * 32 * 2);
+  p.q_off = k.take((size_t)p.Mp * d.d_model * 2);
+  p.o_off = k.take((size_t)p.Mp * p.KBd * 32 * 2);
+  p.r_off = k.take((size_t)p.Mp * d.d_model * 4);
+  p.act_off = k.take((size_t)p.Mp * p.KBf * 32 * 2);
+  p.xdec_off = k.take((size_t)p.B * d.d_model * 4);
+  p.logits_off = k.take((size_t)p.B * p.V * 4);
+  p.part_off = k.take(kPartialBytes);
+  p.tickets_off = k.take((size_t)kTickets * 4);
+  p.rope_off = k.take((size_t)p.kv_pad * (dh / 2) * 8);
+  p.decrows_off = k.take((size_t)p.D * 3 * p.B * 4);
+  p.headrows_off = k.take((size_t)3 * p.B * p.head_rows * 4);
+  p.tokens_off = k.take((size_t)p.B * p.D * 4);
+  p.gate_m_off = k.take((size_t)p.B * 4);
+  p.gate_f_off = k.take((size_t)p.B * 4);
+  p.ws_bytes = k.off;
+  return GVC_OK;
+}
+
+}  // namespace
+
+struct gvc_ctx {
+  Plan p;
+  hipStream_t stream = nullptr;
+  int device = 0;
+  char* w = nullptr;
+  char* st = nullptr;
+  char* ws = nullptr;
+  bool prefill_done = false;
+  bool decode_done = false;
+  int force_splits = 0;   // GVC_FORCE_SPLITS: split every GEMM's k range this many ways (testing)
+  // launch timing of one kernel class (gvc_profile_begin / _end)
+  int prof_cls = -1;
+  std::vector<hipEvent_t> prof_ev;
+  int prof_n = 0;
+  std::vector<int> counts;
+
+  template <class T> T* W(size_t off) const { return reinterpret_cast<T*>(w + off); }
+  template <class T> T* S(size_t off) const { return reinterpret_cast<T*>(st + off); }
+  template <class T> T* K(size_t off) const { return reinterpret_cast<T*>(ws + off); }
+  const bf16x8* packed(const Packed& m) const { return reinterpret_cast<const bf16x8*>(w + m.off); }
+  float* H(int l) const { return S<float>(p.H_off) + (size_t)l * p.B * p.P * p.d.d_model; }
+  bf16* Kc(int l) const { return S<bf16>(p.K_off) + (size_t)l * p.layer_kv_elems; }
+  bf16* Vc(int l) const { return S<bf16>(p.V_off) + (size_t)l * p.layer_kv_elems; }
+  RowMap rows(int l) const {
+    const int tot = p.B * p.P;
+    const int* base = K<int>(p.rows_off) + (size_t)l * 3 * tot;
+    return RowMap{base, base + tot, base + 2 * tot};
+  }
+  RowMap dec_rows(int j) const {
+    const int* base = K<int>(p.decrows_off) + (size_t)j * 3 * p.B;
+    return RowMap{base, base + p.B, base + 2 * p.B};
+  }
+  RowMap head_rows() const {
+    const int n = p.B * p.head_rows;
+    const int* base = K<int>(p.headrows_off);
+    return RowMap{base, base + n, base + 2 * n};
+  }
+};
+
+namespace {
+
+// Split-K and token tiling of one GEMM launch.
+void tile_gemm(GemmArgs& a, int M, int force_splits) {
+  a.M = M;
+  a.mblocks = (M + 15) / 16;
+  a.mtiles = (a.mblocks + 15) / 16;
+  const int NT = (a.mblocks + a.mtiles - 1) / a.mtiles;
+  const int tiles = (a.n_pairs + 3) / 4;
+  const int base = tiles * a.mtiles;
+  int S = 1;
+  if (base < kTargetWgs) S = (kTargetWgs + base - 1) / base;
+  S = std::min(S, std::max(1, a.KB / 8));          // at least 8 k-steps per split
+  // Partial tiles are written and read once each; keep that traffic under a
+  // quarter of the weight bytes the launch streams.
+  const size_t per_split = (size_t)base * 4 * 2 * NT * 64 * sizeof(floatx4);
+  const size_t weight_bytes = (size_t)a.n_pairs * 2 * 16 * a.KB * 32 * 2;
+  if (force_splits > 0) S = std::min(force_splits, a.KB);
+  else
+    while (S > 1 && 2 * per_split * S > weight_bytes / 4) --S;
+  while (S > 1 && (per_split * S > kPartialBytes || base > kTickets)) --S;
+  a.kb_per_split = (a.KB + S - 1) / S;
+  a.splits = (a.KB + a.kb_per_split - 1) / a.kb_per_split;
+}
+
+int nt_of(const GemmArgs& a) { return (a.mblocks + a.mtiles - 1) / a.mtiles; }
+
+// Start / stop events around a launch of class `cls` when it is profiled.
+struct ProfScope {
+  gvc_ctx* c;
+  bool on;
+  ProfScope(gvc_ctx* ctx, int cls) : c(ctx), on(ctx->prof_cls == cls && 2 * ctx->prof_n + 1 < (int)ctx->prof_ev.size()) {
+    if (on) (void)hipEventRecord(c->prof_ev[2 * c->prof_n], c->stream);
+  }
+  ~ProfScope() {
+    if (on) {
+      (void)hipEventRecord(c->prof_ev[2 * c->prof_n + 1], c->stream);
+      ++c->prof_n;
+    }
+  }
+};
+
+GemmArgs base_args(const gvc_ctx* c) {
+  GemmArgs a;
+  memset(&a, 0, sizeof(a));
+  a.part = c->K<floatx4>(c->p.part_off);
+  a.tickets = c->K<int>(c->p.tickets_off);
+  a.e.d = c->p.d.d_model;
+  a.e.head_dim = c->p.dh;
+  a.e.n_heads = c->p.H;
+  a.e.kv_pad = c->p.kv_pad;
+  a.e.rope = c->K<float2>(c->p.rope_off);
+  return a;
+}
+
+int32_t run_gemm(gvc_ctx* c, GemmArgs& a, int epi, int M, int cls) {
+  if (M <= 0) return GVC_OK;
+  tile_gemm(a, M, c->force_splits);
+  ProfScope ps(c, cls);
+  HIP_TRY(launch_gemm(a, epi, nt_of(a), c->stream));
+  return GVC_OK;
+}
+
+// One decoder layer over M rows: `src` holds the layer input rows (mapped by
+// rows.idx when src_mapped), `dst` receives the outputs (same mapping rule).
+int32_t run_layer(gvc_ctx* c, int l, const RowMap& rows, int M, float* src, float* dst, bool mapped,
+                  bool decode, int n_keys, int max_tiles, const int* epc, const int* epo) {
+  const Plan& p = c->p;
+  const float* gains = c->W<float>(p.gains_off) + (size_t)l * 2 * p.d.d_model;
+  bf16* X = c->K<bf16>(p.x_off);
+  bf16* Q = c->K<bf16>(p.q_off);
+  bf16* O = c->K<bf16>(p.o_off);
+  float* R = c->K<float>(p.r_off);
+  bf16* A = c->K<bf16>(p.act_off);
+  const int k0 = decode ? GVC_K_DECODE_QKV : GVC_K_PREFILL_QKV;   // class of this layer's QKV launch
+  {
+    ProfScope ps(c, GVC_K_NORM);
+    HIP_TRY(launch_rmsnorm(src, mapped ? rows.idx : nullptr, M, p.d.d_model, gains, p.d.rms_eps, X, p.KBd, c->stream));
+  }
+  {
+    GemmArgs a = base_args(c);
+    a.w[0] = c->packed(p.wq[l]); a.w[1] = c->packed(p.wk[l]); a.w[2] = c->packed(p.wv[l]);
+    a.wblk[0] = a.wblk[1] = a.wblk[2] = p.wq[l].Nblk;
+    a.map = MAP_QKV; a.n_pairs = 3 * p.wq[l].Nblk / 2; a.n_out = p.d.d_model; a.KB = p.KBd;
+    a.x = reinterpret_cast<const bf16x8*>(X);
+    a.e.rows = rows; a.e.q = Q; a.e.kc = c->Kc(l); a.e.vc = c->Vc(l);
+    int32_t r = run_gemm(c, a, EPI_QKV, M, k0);
+    if (r) return r;
+  }
+  {
+    ProfScope ps(c, k0 + 1);
+    if (decode)
+      HIP_TRY(launch_attn_decode(Q, c->Kc(l), c->Vc(l), p.B, p.H, p.dh, p.kv_pad, n_keys, O, p.KBd, c->stream));
+    else
+      HIP_TRY(launch_attn_prefill(Q, c->Kc(l), c->Vc(l), rows.pos, epc, epo, p.B, p.H, p.dh, p.kv_pad, max_tiles, O,
+                                  p.KBd, c->stream));
+  }
+  {
+    GemmArgs a = base_args(c);
+    a.w[0] = c->packed(p.wo[l]); a.wblk[0] = p.wo[l].Nblk;
+    a.map = MAP_PLAIN; a.n_pairs = (p.wo[l].Nblk + 1) / 2; a.n_out = p.d.d_model; a.KB = p.KBd;
+    a.x = reinterpret_cast<const bf16x8*>(O);
+    a.e.rows = rows; a.e.resid = src; a.e.resid_mapped = mapped; a.e.out = R; a.e.out_mapped = 0;
+    int32_t r = run_gemm(c, a, EPI_RESID, M, k0 + 2);
+    if (r) return r;
+  }
+  {
+    ProfScope ps(c, GVC_K_NORM);
+    HIP_TRY(launch_rmsnorm(R, nullptr, M, p.d.d_model, gains + p.d.d_model, p.d.rms_eps, X, p.KBd, c->stream));
+  }
+  {
+    GemmArgs a = base_args(c);
+    a.w[0] = c->packed(p.wg[l]); a.w[1] = c->packed(p.wu[l]);
+    a.wblk[0] = a.wblk[1] = p.wg[l].Nblk;
+    a.map = MAP_GU; a.n_pairs = p.wg[l].Nblk; a.n_out = p.F; a.KB = p.KBd;
+    a.x = reinterpret_cast<const bf16x8*>(X);
+    a.e.rows = rows; a.e.act = A; a.e.kb_act = p.KBf; a.e.n_feat = p.F;
+    int32_t r = run_gemm(c, a, EPI_SILU, M, k0 + 3);
+    if (r) return r;
+  }
+  {
+    GemmArgs a = base_args(c);
+    a.w[0] = c->packed(p.wd[l]); a.wblk[0] = p.wd[l].Nblk;
+    a.map = MAP_PLAIN; a.n_pairs = (p.wd[l].Nblk + 1) / 2; a.n_out = p.d.d_model; a.KB = p.KBf;
+    a.x = reinterpret_cast<const bf16x8*>(A);
+    a.e.rows = rows; a.e.resid = R; a.e.resid_mapped = 0; a.e.out = dst; a.e.out_mapped = mapped;
+    int32_t r = run_gemm(c, a, EPI_RESID, M, k0 + 4);
+    if (r) return r;
+  }
+  return GVC_OK;
+}
+
+// Final RMSNorm + LM head over M rows of `src` (mapped through rows.idx when given).
+int32_t run_head(gvc_ctx* c, const RowMap& rows, const float* src, int M, float* logits, int cls) {
+  const Plan& p = c->p;
+  bf16* X = c->K<bf16>(p.x_off);
+  {
+    ProfScope ps(c, GVC_K_NORM);
+    HIP_TRY(launch_rmsnorm(src, rows.idx, M, p.d.d_model, c->W<float>(p.final_gain_off), p.d.rms_eps, X, p.KBd,
+                           c->stream));
+  }
+  GemmArgs a = base_args(c);
+  a.w[0] = c->packed(p.lm); a.wblk[0] = p.lm.Nblk;
+  a.map = MAP_PLAIN; a.n_pairs = (p.lm.Nblk + 1) / 2; a.n_out = p.V; a.KB = p.KBd;
+  a.x = reinterpret_cast<const bf16x8*>(X);
+  a.e.rows = rows; a.e.store = logits; a.e.ld_store = p.V;
+  return run_gemm(c, a, EPI_STORE, M, cls);
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* gvc_last_error(void) { return g_err.c_str(); }
+
+int32_t gvc_sizes(const gvc_desc* desc, size_t* weight_bytes, size_t* state_bytes, size_t* workspace_bytes) {
+  Plan p;
+  int32_t r = make_plan(desc, p);
+  if (r) return r;
+  if (weight_bytes) *weight_bytes = p.weight_bytes;
+  if (state_bytes) *state_bytes = p.state_bytes;
+  if (workspace_bytes) *workspace_bytes = p.ws_bytes;
+  return GVC_OK;
+}
+
+int32_t gvc_init_cache(const gvc_desc* desc, const gvc_weights* wt, void* weight_arena, size_t weight_bytes,
+                       void* state, size_t state_bytes, void* workspace, size_t workspace_bytes, void* stream,
+                       gvc_ctx** out) {
+  if (!out) return fail(GVC_EINVAL, "null out");
+  *out = nullptr;
+  Plan p;
+  int32_t r = make_plan(desc, p);
+  if (r) return r;
+  if (!wt || !wt->embed || !wt->patch_proj || !wt->lm_head || !wt->final_norm || !wt->layers)
+    return fail(GVC_EINVAL, "null weight pointer");
+  for (int l = 0; l < p.L; ++l) {
+    const gvc_layer_weights& lw = wt->layers[l];
+    if (!lw.wq || !lw.wk || !lw.wv || !lw.wo || !lw.wg || !lw.wu || !lw.wd || !lw.attn_norm || !lw.ffn_norm)
+      return fail(GVC_EINVAL, "null layer weight pointer at layer " + std::to_string(l));
+  }
+  if (!weight_arena || !state || !workspace) return fail(GVC_EINVAL, "null arena");
+  if (((uintptr_t)weight_arena | (uintptr_t)state | (uintptr_t)workspace) % kAlign)
+    return fail(GVC_EINVAL, "arenas must be 256-byte aligned");
+  if (weight_bytes < p.weight_bytes || state_bytes < p.state_bytes || workspace_bytes < p.ws_bytes)
+    return fail(GVC_ENOMEM, "arena smaller than gvc_sizes reported");
+
+  gvc_ctx* c = new gvc_ctx();
+  c->p = p;
+  c->stream = reinterpret_cast<hipStream_t>(stream);
+  c->w = static_cast<char*>(weight_arena);
+  c->st = static_cast<char*>(state);
+  c->ws = static_cast<char*>(workspace);
+  c->counts.assign(p.L, 0);
+  auto bail = [&](int32_t code) { delete c; return code; };
+  hipStream_t s = c->stream;
+  const int dm = p.d.d_model;
+
+#define INIT_TRY(x)                                                                                   \
+  do {                                                                                                \
+    hipError_t e_ = (x);                                                                              \
+    if (e_ != hipSuccess) return bail(fail(GVC_EDEVICE, std::string(#x) + ": " + hipGetErrorString(e_))); \
+  } while (0)
+
+  INIT_TRY(hipGetDevice(&c->device));
+  if (const char* fs = getenv("GVC_FORCE_SPLITS")) c->force_splits = atoi(fs);
+  INIT_TRY(launch_fill_u32(reinterpret_cast<uint32_t*>(c->st), 0u, p.state_bytes / 4, s));
+  INIT_TRY(launch_fill_u32(reinterpret_cast<uint32_t*>(c->ws), 0u, p.ws_bytes / 4, s));
+  for (int l = 0; l < p.L; ++l) {
+    const gvc_layer_weights& lw = wt->layers[l];
+    const Packed* mats[7] = {&p.wq[l], &p.wk[l], &p.wv[l], &p.wo[l], &p.wg[l], &p.wu[l], &p.wd[l]};
+    const void* srcs[7] = {lw.wq, lw.wk, lw.wv, lw.wo, lw.wg, lw.wu, lw.wd};
+    for (int i = 0; i < 7; ++i)
+      INIT_TRY(launch_pack(static_cast<const bf16*>(srcs[i]), mats[i]->N, mats[i]->K, c->W<bf16>(mats[i]->off),
+                           mats[i]->Nblk, mats[i]->KB, s));
+    float* g = c->W<float>(p.gains_off) + (size_t)l * 2 * dm;
+    INIT_TRY(launch_convert_gain(static_cast<const bf16*>(lw.attn_norm), g, dm, s));
+    INIT_TRY(launch_convert_gain(static_cast<const bf16*>(lw.ffn_norm), g + dm, dm, s));
+  }
+  INIT_TRY(launch_pack(static_cast<const bf16*>(wt->patch_proj), p.patch.N, p.patch.K, c->W<bf16>(p.patch.off),
+                       p.patch.Nblk, p.patch.KB, s));
+  INIT_TRY(launch_pack(static_cast<const bf16*>(wt->lm_head), p.lm.N, p.lm.K, c->W<bf16>(p.lm.off), p.lm.Nblk,
+                       p.lm.KB, s));
+  INIT_TRY(hipMemcpyAsync(c->W<char>(p.embed_off), wt->embed, (size_t)p.V * dm * 2, hipMemcpyDeviceToDevice, s));
+  INIT_TRY(launch_convert_gain(static_cast<const bf16*>(wt->final_norm), c->W<float>(p.final_gain_off), dm, s));
+  INIT_TRY(launch_rope_table(c->K<float2>(p.rope_off), p.kv_pad, p.dh, p.d.rope_theta, s));
+
+  // static row maps: decode pass j (token at position P + j - 1) and the head rows
+  std::vector<int> dec((size_t)p.D * 3 * p.B), head((size_t)3 * p.B * p.head_rows);
+  for (int j = 0; j < p.D; ++j)
+    for (int b = 0; b < p.B; ++b) {
+      dec[((size_t)j * 3 + 0) * p.B + b] = b;
+      dec[((size_t)j * 3 + 1) * p.B + b] = b;
+      dec[((size_t)j * 3 + 2) * p.B + b] = p.P + j - 1;
+    }
+  const int nh = p.B * p.head_rows;
+  for (int b = 0; b < p.B; ++b)
+    for (int i = 0; i < p.head_rows; ++i) {
+      const int pos = p.d.parallel_decode ? p.N + p.d.n_text + p.d.n_proprio + i : p.P - 1;
+      const int r = b * p.head_rows + i;
+      head[r] = b * p.P + pos;
+      head[nh + r] = b;
+      head[2 * nh + r] = pos;
+    }
+  INIT_TRY(hipMemcpyAsync(c->K<int>(p.decrows_off), dec.data(), dec.size() * 4, hipMemcpyHostToDevice, s));
+  INIT_TRY(hipMemcpyAsync(c->K<int>(p.headrows_off), head.data(), head.size() * 4, hipMemcpyHostToDevice, s));
+  INIT_TRY(hipStreamSynchronize(s));
+#undef INIT_TRY
+  *out = c;
+  return GVC_OK;
+}
+
+int32_t gvc_select_static(gvc_ctx* c, const uint8_t* frame_t, const uint8_t* frame_prev, int32_t tau_num,
+                          int32_t tau_den, const int32_t* reuse_permille, uint8_t* reuse_mask, int32_t* n_static) {
+  if (!c || !frame_t || !frame_prev || !reuse_mask) return fail(GVC_EINVAL, "null argument");
+  if (!(tau_num > 0 && tau_num <= tau_den && tau_den <= (1 << 20)))
+    return fail(GVC_EINVAL, "tau must satisfy 0 < num <= den <= 2^20");
+  const Plan& p = c->p;
+  std::vector<int> q(p.L, 1000);
+  if (reuse_permille)
+    for (int l = 0; l < p.L; ++l) {
+      if (reuse_permille[l] < 0 || reuse_permille[l] > 1000) return fail(GVC_EINVAL, "permille out of [0, 1000]");
+      q[l] = reuse_permille[l];
+    }
+  int* stats = c->K<int>(p.stats_off);
+  ProfScope ps(c, GVC_K_SELECT);
+  HIP_TRY(launch_patch_stats(frame_t, frame_prev, p.B, p.d.n_views, p.d.img, p.d.patch, stats, c->stream));
+  HIP_TRY(launch_rank_mask(stats, p.B, p.N, p.L, tau_num, tau_den, q.data(), reuse_mask, n_static, c->stream));
+  return GVC_OK;
+}
+
+int32_t gvc_step_prefill(gvc_ctx* c, const uint8_t* frame_t, const int32_t* text_ids, const float* extra_rows,
+                         const uint8_t* reuse_mask) {
+  if (!c || !frame_t || !text_ids) return fail(GVC_EINVAL, "null argument");
+  const Plan& p = c->p;
+  if (p.n_extra > 0 && !extra_rows) return fail(GVC_EINVAL, "extra_rows required");
+  hipStream_t s = c->stream;
+  int* counts = c->K<int>(p.counts_off);
+  int* epc = c->K<int>(p.epc_off);
+  int* epo = c->K<int>(p.epo_off);
+  HIP_TRY(launch_build_rows(reuse_mask, c->S<int>(p.valid_off), p.B, p.L, p.N, p.P, c->K<int>(p.rows_off), counts, epc,
+                            epo, s));
+  HIP_TRY(hipMemcpyAsync(c->S<int>(p.rowcount_off), counts, (size_t)p.L * 4, hipMemcpyDeviceToDevice, s));
+  HIP_TRY(hipMemcpyAsync(c->counts.data(), counts, (size_t)p.L * 4, hipMemcpyDeviceToHost, s));
+  HIP_TRY(hipStreamSynchronize(s));
+  for (int l = 0; l < p.L; ++l)
+    if (c->counts[l] < 1 || c->counts[l] > p.B * p.P) return fail(GVC_EDEVICE, "corrupt row count");
+
+  // layer-0 embeddings of the rows recomputed at layer 0
+  {
+    const RowMap r0 = c->rows(0);
+    bf16* X = c->K<bf16>(p.x_off);
+    HIP_TRY(launch_im2row(frame_t, p.d.n_views, p.d.img, p.d.patch, r0.idx, r0.pos, c->counts[0], p.P, p.KBp, X, s));
+    GemmArgs a = base_args(c);
+    a.w[0] = c->packed(p.patch); a.wblk[0] = p.patch.Nblk;
+    a.map = MAP_PLAIN; a.n_pairs = (p.patch.Nblk + 1) / 2; a.n_out = p.d.d_model; a.KB = p.KBp;
+    a.x = reinterpret_cast<const bf16x8*>(X);
+    a.e.rows = r0; a.e.h0 = c->H(0); a.e.embed = c->W<bf16>(p.embed_off); a.e.text_ids = text_ids;
+    a.e.extra = extra_rows; a.e.n_patches = p.N; a.e.n_text = p.d.n_text; a.e.n_extra = p.n_extra;
+    int32_t r = run_gemm(c, a, EPI_EMBED, c->counts[0], GVC_K_EMBED);
+    if (r) return r;
+  }
+  const int max_tiles = (p.P + 15) / 16;
+  for (int l = 0; l < p.L; ++l) {
+    int32_t r = run_layer(c, l, c->rows(l), c->counts[l], c->H(l), c->H(l + 1), true, false, 0, max_tiles,
+                          epc + l * p.B, epo + l * p.B);
+    if (r) return r;
+  }
+  int32_t r = run_head(c, c->head_rows(), c->H(p.L), p.B * p.head_rows, c->S<float>(p.head_logits_off),
+                       GVC_K_PREFILL_HEAD);
+  if (r) return r;
+  HIP_TRY(launch_fill_u32(reinterpret_cast<uint32_t*>(c->S<int>(p.valid_off)), 1u, p.B, s));
+  c->prefill_done = true;
+  return GVC_OK;
+}
+
+int32_t gvc_decode_actions(gvc_ctx* c, int32_t* tokens_out, float* margins_out, float* logits_out,
+                           const int32_t* forced_tokens) {
+  if (!c || !tokens_out || !margins_out) return fail(GVC_EINVAL, "null argument");
+  if (!c->prefill_done) return fail(GVC_ESTATE, "decode_actions needs a prompt pass first");
+  const Plan& p = c->p;
+  hipStream_t s = c->stream;
+  int* tok = c->K<int>(p.tokens_off);
+  float* mg = c->S<float>(p.margins_off);
+  const float* hl = c->S<float>(p.head_logits_off);
+  const int full = p.d.norm_full_vocab ? 1 : 0;
+  if (p.d.parallel_decode) {
+    HIP_TRY(launch_logits_reduce(hl, p.B * p.head_rows, p.V, p.bin_lo, full, tok, mg, p.D, 0, p.head_rows, s));
+    if (logits_out)
+      HIP_TRY(hipMemcpyAsync(logits_out, hl, (size_t)p.B * p.D * p.V * 4, hipMemcpyDeviceToDevice, s));
+  } else {
+    HIP_TRY(launch_logits_reduce(hl, p.B, p.V, p.bin_lo, full, tok, mg, p.D, 0, 1, s));
+    if (logits_out)
+      HIP_TRY(hipMemcpy2DAsync(logits_out, (size_t)p.D * p.V * 4, hl, (size_t)p.V * 4, (size_t)p.V * 4, p.B,
+                               hipMemcpyDeviceToDevice, s));
+    float* xdec = c->K<float>(p.xdec_off);
+    float* lg = c->K<float>(p.logits_off);
+    for (int j = 1; j < p.D; ++j) {
+      const int* src = forced_tokens ? forced_tokens + (j - 1) : tok + (j - 1);
+      HIP_TRY(launch_embed_tokens(c->W<bf16>(p.embed_off), src, p.D, p.B, p.d.d_model, xdec, s));
+      const RowMap rows = c->dec_rows(j);
+      const int pos = p.P + j - 1;
+      for (int l = 0; l < p.L; ++l) {
+        int32_t r = run_layer(c, l, rows, p.B, xdec, xdec, false, true, pos + 1, 0, nullptr, nullptr);
+        if (r) return r;
+      }
+      RowMap hr{nullptr, rows.ep, rows.pos};
+      int32_t r = run_head(c, hr, xdec, p.B, lg, GVC_K_DECODE_HEAD);
+      if (r) return r;
+      HIP_TRY(launch_logits_reduce(lg, p.B, p.V, p.bin_lo, full, tok, mg, p.D, j, 1, s));
+      if (logits_out)
+        HIP_TRY(hipMemcpy2DAsync(logits_out + (size_t)j * p.V, (size_t)p.D * p.V * 4, lg, (size_t)p.V * 4,
+                                 (size_t)p.V * 4, p.B, hipMemcpyDeviceToDevice, s));
+    }
+  }
+  HIP_TRY(hipMemcpyAsync(tokens_out, tok, (size_t)p.B * p.D * 4, hipMemcpyDeviceToDevice, s));
+  HIP_TRY(hipMemcpyAsync(margins_out, mg, (size_t)p.B * p.D * 4, hipMemcpyDeviceToDevice, s));
+  c->prefill_done = false;
+  c->decode_done = true;
+  return GVC_OK;
+}
+
+int32_t gvc_margin_gate(gvc_ctx* c, float theta, int32_t reduce, float* margin_out, uint8_t* fire_out,
+                        const int8_t* force) {
+  if (!c) return fail(GVC_EINVAL, "null context");
+  if (theta != theta) return fail(GVC_EINVAL, "theta is NaN");
+  if (reduce != GVC_REDUCE_MEAN && reduce != GVC_REDUCE_MIN) return fail(GVC_EINVAL, "bad reduce");
+  if (!c->decode_done) return fail(GVC_ESTATE, "margin_gate needs a decode first");
+  const Plan& p = c->p;
+  float* m = c->K<float>(p.gate_m_off);
+  int* f = c->K<int>(p.gate_f_off);
+  HIP_TRY(launch_gate(c->S<float>(p.margins_off), p.B, p.D, theta, reduce == GVC_REDUCE_MIN, force,
+                      c->S<int>(p.valid_off), m, f, c->stream));
+  std::vector<float> hm(p.B);
+  std::vector<int> hf(p.B);
+  HIP_TRY(hipMemcpyAsync(hm.data(), m, (size_t)p.B * 4, hipMemcpyDeviceToHost, c->stream));
+  HIP_TRY(hipMemcpyAsync(hf.data(), f, (size_t)p.B * 4, hipMemcpyDeviceToHost, c->stream));
+  HIP_TRY(hipStreamSynchronize(c->stream));
+  for (int b = 0; b < p.B; ++b) {
+    if (margin_out) margin_out[b] = hm[b];
+    if (fire_out) fire_out[b] = (uint8_t)(hf[b] != 0);
+  }
+  return GVC_OK;
+}
+
+int32_t gvc_invalidate(gvc_ctx* c, int32_t b) {
+  if (!c) return fail(GVC_EINVAL, "null context");
+  const Plan& p = c->p;
+  if (b < -1 || b >= p.B) return fail(GVC_EINVAL, "episode out of range");
+  int* v = c->S<int>(p.valid_off);
+  if (b < 0)
+    HIP_TRY(launch_fill_u32(reinterpret_cast<uint32_t*>(v), 0u, p.B, c->stream));
+  else
+    HIP_TRY(launch_fill_u32(reinterpret_cast<uint32_t*>(v + b), 0u, 1, c->stream));
+  return GVC_OK;
+}
+
+size_t gvc_state_item_bytes(const gvc_ctx* c, int32_t item) {
+  if (!c) return 0;
+  const Plan& p = c->p;
+  switch (item) {
+    case GVC_STATE_H: return (size_t)p.B * p.P * p.d.d_model * 4;
+    case GVC_STATE_K:
+    case GVC_STATE_V: return p.layer_kv_elems * 2;
+    case GVC_STATE_HEAD_LOGITS: return (size_t)p.B * p.head_rows * p.V * 4;
+    case GVC_STATE_VALID: return (size_t)p.B * 4;
+    case GVC_STATE_ROWS: return (size_t)p.L * 4;
+    case GVC_STATE_MARGINS: return (size_t)p.B * p.D * 4;
+    default: return 0;
+  }
+}
+
+int32_t gvc_read_state(gvc_ctx* c, int32_t item, int32_t layer, void* dst, size_t dst_bytes) {
+  if (!c || !dst) return fail(GVC_EINVAL, "null argument");
+  const Plan& p = c->p;
+  const size_t n = gvc_state_item_bytes(c, item);
+  if (n == 0) return fail(GVC_EINVAL, "bad state item");
+  if (dst_bytes < n) return fail(GVC_EINVAL, "destination too small");
+  const void* src = nullptr;
+  switch (item) {
+    case GVC_STATE_H:
+      if (layer < 0 || layer > p.L) return fail(GVC_EINVAL, "layer out of range");
+      src = c->H(layer);
+      break;
+    case GVC_STATE_K:
+    case GVC_STATE_V:
+      if (layer < 0 || layer >= p.L) return fail(GVC_EINVAL, "layer out of range");
+      src = item == GVC_STATE_K ? (const void*)c->Kc(layer) : (const void*)c->Vc(layer);
+      break;
+    case GVC_STATE_HEAD_LOGITS: src = c->S<float>(p.head_logits_off); break;
+    case GVC_STATE_VALID: src = c->S<int>(p.valid_off); break;
+    case GVC_STATE_ROWS: src = c->S<int>(p.rowcount_off); break;
+    case GVC_STATE_MARGINS: src = c->S<float>(p.margins_off); break;
+  }
+  HIP_TRY(hipMemcpyAsync(dst, src, n, hipMemcpyDeviceToDevice, c->stream));
+  HIP_TRY(hipStreamSynchronize(c->stream));
+  return GVC_OK;
+}
+
+int32_t gvc_profile_begin(gvc_ctx* c, int32_t cls, int32_t max_launches) {
+  if (!c) return fail(GVC_EINVAL, "null context");
+  if (cls < 0 || cls >= GVC_K_COUNT || max_launches < 1) return fail(GVC_EINVAL, "bad kernel class or count");
+  for (hipEvent_t e : c->prof_ev) (void)hipEventDestroy(e);
+  c->prof_ev.assign((size_t)2 * max_launches, nullptr);
+  for (auto& e : c->prof_ev) HIP_TRY(hipEventCreate(&e));
+  c->prof_n = 0;
+  c->prof_cls = cls;
+  return GVC_OK;
+}
+
+int32_t gvc_profile_end(gvc_ctx* c, double* total_ms, int32_t* launches) {
+  if (!c) return fail(GVC_EINVAL, "null context");
+  if (c->prof_cls < 0) return fail(GVC_ESTATE, "no profile running");
+  HIP_TRY(hipStreamSynchronize(c->stream));
+  double tot = 0.0;
+  for (int i = 0; i < c->prof_n; ++i) {
+    float ms = 0.f;
+    HIP_TRY(hipEventElapsedTime(&ms, c->prof_ev[2 * i], c->prof_ev[2 * i + 1]));
+    tot += ms;
+  }
+  if (total_ms) *total_ms = tot;
+  if (launches) *launches = c->prof_n;
+  for (hipEvent_t e : c->prof_ev) (void)hipEventDestroy(e);
+  c->prof_ev.clear();
+  c->prof_cls = -1;
+  c->prof_n = 0;
+  return GVC_OK;
+}
+
+int32_t gvc_destroy(gvc_ctx* c) {
+  if (c)
+    for (hipEvent_t e : c->prof_ev) (void)hipEventDestroy(e);
+  delete c;
+  return GVC_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,125 @@
+// Internal declarations shared by the HIP kernels and the host side of libgvc.
+//
+// Data layouts used on the device:
+//  * packed weights: a [N][K] bf16 matrix is stored as 16-row blocks, each
+//    block as K/32 fragments of 64 lanes x 8 bf16 (1 KiB), in the operand
+//    order of the gfx950 MFMA v_mfma_f32_16x16x32_bf16: lane l of fragment
+//    (blk, kb) holds W[blk*16 + l%16][kb*32 + (l/16)*8 + 0..7].  A wave streams
+//    a block as contiguous 1 KiB loads.  Rows >= N and columns >= K are zero.
+//  * activations feeding a GEMM ("frag layout"): the same arrangement with
+//    token rows in place of weight rows: element (m, k) lives in fragment
+//    (m/16, k/32), lane ((k%32)/8)*16 + m%16, slot k%8.
+//  * K cache: bf16 [B][H][kv_pad][head_dim] per layer, after RoPE.
+//  * V cache: bf16 [B][H][head_dim][kv_pad] per layer (transposed, so a run of
+//    keys for one dimension is contiguous).
+//  * hidden state H: fp32 [L+1][B][P][d]; row index b*P + pos.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace gvc {
+
+typedef uint16_t bf16;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef uint16_t u16x4 __attribute__((ext_vector_type(4)));
+typedef uint16_t u16x8 __attribute__((ext_vector_type(8)));
+
+__device__ __forceinline__ float bf2f(bf16 h) { return __uint_as_float(((uint32_t)h) << 16); }
+
+// fp32 -> bf16, round to nearest even; NaN stays NaN.
+__device__ __forceinline__ bf16 f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (bf16)((u >> 16) | 0x40);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (bf16)(u >> 16);
+}
+
+__device__ __forceinline__ floatx4 mfma16(const bf16x8& a, const bf16x8& b, const floatx4& c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+// Offset (in bf16 elements) of element (m, k) in frag layout with KB k-fragments per row block.
+__device__ __forceinline__ size_t frag_off(int m, int k, int KB) {
+  return ((((size_t)(m >> 4) * KB + (k >> 5)) * 64 + ((k & 31) >> 3) * 16 + (m & 15)) << 3) + (k & 7);
+}
+
+// ------------------------------------------------------------------ GEMM
+enum { MAP_PLAIN = 0, MAP_QKV = 1, MAP_GU = 2 };
+enum { EPI_QKV = 0, EPI_RESID = 1, EPI_SILU = 2, EPI_STORE = 3, EPI_EMBED = 4 };
+
+struct RowMap {
+  const int* idx;   // row index into the residual / output arrays
+  const int* ep;    // episode b
+  const int* pos;   // absolute position
+};
+
+struct EpiArgs {
+  RowMap rows;
+  // EPI_QKV
+  bf16* q;            // [Mp][d] row-major, after RoPE
+  bf16* kc;           // this layer's K cache
+  bf16* vc;           // this layer's V cache (transposed)
+  const float2* rope; // [kv_pad][head_dim/2] (cos, sin)
+  int d, head_dim, n_heads, kv_pad;
+  // EPI_RESID: out[row] = resid[row] + acc, rows mapped through rows.idx when *_mapped
+  const float* resid; int resid_mapped;
+  float* out; int out_mapped;
+  // EPI_SILU: frag-layout bf16 activations with kb_act k-fragments per row block
+  bf16* act; int kb_act; int n_feat;
+  // EPI_STORE
+  float* store; int ld_store;
+  // EPI_EMBED
+  float* h0; const bf16* embed; const int* text_ids; const float* extra;
+  int n_patches, n_text, n_extra;
+};
+
+struct GemmArgs {
+  const bf16x8* w[3];   // packed matrices (fragment units)
+  int wblk[3];          // 16-row blocks per matrix
+  int map;
+  int n_pairs;          // pairs of 16-row blocks (one pair per wave)
+  int n_out;            // output features of the (first) matrix, for MAP_PLAIN
+  int KB;               // k-fragments (K padded / 32)
+  int splits, kb_per_split;
+  const bf16x8* x;      // frag-layout activations
+  int M, mblocks, mtiles;
+  floatx4* part;        // split-K partials
+  int* tickets;
+  EpiArgs e;
+};
+
+// ------------------------------------------------------------------ launchers
+// All launchers enqueue on `s` and return hipGetLastError().
+hipError_t launch_pack(const bf16* src, int N, int K, bf16* dst, int Nblk, int KB, hipStream_t s);
+hipError_t launch_convert_gain(const bf16* src, float* dst, int n, hipStream_t s);
+hipError_t launch_rope_table(float2* tab, int kv_pad, int head_dim, float theta, hipStream_t s);
+hipError_t launch_fill_u32(uint32_t* p, uint32_t v, size_t n, hipStream_t s);
+
+hipError_t launch_patch_stats(const uint8_t* ft, const uint8_t* fp, int B, int views, int img, int patch,
+                              int* stats, hipStream_t s);
+hipError_t launch_rank_mask(const int* stats, int B, int N, int L, long long tau_num, long long tau_den,
+                            const int* permille_dev, uint8_t* mask, int* n_static, hipStream_t s);
+
+hipError_t launch_build_rows(const uint8_t* mask, const int* valid, int B, int L, int N, int P,
+                             int* rows, int* counts, int* ep_counts, int* ep_offsets, hipStream_t s);
+hipError_t launch_im2row(const uint8_t* frame, int views, int img, int patch, const int* idx, const int* pos,
+                         int M, int P, int KB, bf16* x, hipStream_t s);
+hipError_t launch_rmsnorm(const float* src, const int* idx, int M, int d, const float* gain, float eps,
+                          bf16* x, int KB, hipStream_t s);
+hipError_t launch_gemm(const GemmArgs& a, int epi, int NT, hipStream_t s);
+hipError_t launch_attn_prefill(const bf16* q, const bf16* kc, const bf16* vc, const int* rows_pos,
+                               const int* ep_counts, const int* ep_offsets, int B, int H, int head_dim,
+                               int kv_pad, int max_tiles, bf16* o, int KB, hipStream_t s);
+hipError_t launch_attn_decode(const bf16* q, const bf16* kc, const bf16* vc, int B, int H, int head_dim,
+                              int kv_pad, int n_keys, bf16* o, int KB, hipStream_t s);
+hipError_t launch_embed_tokens(const bf16* embed, const int* tokens, int tok_stride, int B, int d,
+                               float* x, hipStream_t s);
+hipError_t launch_logits_reduce(const float* logits, int rows, int V, int bin_lo, int full_vocab,
+                                int* tok_out, float* margin_out, int out_stride, int out_col,
+                                int rows_per_ep, hipStream_t s);
+hipError_t launch_gate(const float* margins, int B, int D, float theta, int use_min, const int8_t* force,
+                       int* valid, float* m_out, int* fire_out, hipStream_t s);
+hipError_t launch_select_tokens(const int* src, int src_stride, int col, int B, int* dst, hipStream_t s);
+
+}  // namespace gvc

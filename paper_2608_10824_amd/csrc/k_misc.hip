@@ -1,0 +1,349 @@
+// Row bookkeeping, normalisation, embedding, logits reduction, the gate and
+// the one-time weight packing.
+#include "gvc_kernels.h"
+
+namespace gvc {
+
+// ------------------------------------------------------------------ packing
+// Canonical bf16 W[N][K] -> 16-row-block fragment layout (see gvc_kernels.h).
+__global__ void k_pack(const bf16* __restrict__ src, int N, int K, bf16* __restrict__ dst, int Nblk, int KB) {
+  const size_t total = (size_t)Nblk * KB * 64;
+  for (size_t e = (size_t)blockIdx.x * blockDim.x + threadIdx.x; e < total; e += (size_t)gridDim.x * blockDim.x) {
+    const int lane = (int)(e & 63);
+    const size_t fk = e >> 6;
+    const int kb = (int)(fk % KB);
+    const int blk = (int)(fk / KB);
+    const int n = blk * 16 + (lane & 15);
+    const int k = kb * 32 + (lane >> 4) * 8;
+    u16x8 v = {0, 0, 0, 0, 0, 0, 0, 0};
+    if (n < N) {
+      const bf16* row = src + (size_t)n * K;
+      if ((K & 7) == 0 && k + 8 <= K) {
+        v = *(const u16x8*)(row + k);
+      } else {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) v[i] = (k + i < K) ? row[k + i] : (bf16)0;
+      }
+    }
+    *(u16x8*)(dst + e * 8) = v;
+  }
+}
+
+__global__ void k_convert_gain(const bf16* __restrict__ src, float* __restrict__ dst, int n) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) dst[i] = bf2f(src[i]);
+}
+
+// (cos, sin) of pos * theta^(-2i/d_h), evaluated in double then rounded.
+__global__ void k_rope_table(float2* __restrict__ tab, int kv_pad, int head_dim, float theta) {
+  const int half = head_dim / 2;
+  const int e = blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= kv_pad * half) return;
+  const int pos = e / half, i = e % half;
+  const double ang = (double)pos * pow((double)theta, -2.0 * i / head_dim);
+  tab[e] = float2{(float)cos(ang), (float)sin(ang)};
+}
+
+__global__ void k_fill_u32(uint32_t* p, uint32_t v, size_t n) {
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) p[i] = v;
+}
+
+// ------------------------------------------------------------------ row lists
+// One workgroup per layer.  Row r = b*P + pos of the batched prompt is
+// recomputed at layer l unless episode b has a valid cache, a mask is given,
+// pos is a visual token (1..N) and mask[b][l][pos-1] is set.  Writes the
+// compacted rows in (b, pos) order as three int arrays (idx, ep, pos) of
+// stride B*P, the per-layer count, and per-episode counts and offsets.
+__global__ __launch_bounds__(1024) void k_build_rows(const uint8_t* __restrict__ mask, const int* __restrict__ valid,
+                                                     int B, int L, int N, int P, int* __restrict__ rows,
+                                                     int* __restrict__ counts, int* __restrict__ ep_counts,
+                                                     int* __restrict__ ep_offsets) {
+  __shared__ int warp_sums[16];
+  __shared__ int s_base;
+  const int l = blockIdx.x;
+  const int total = B * P;
+  int* r_idx = rows + (size_t)l * 3 * total;
+  int* r_ep = r_idx + total;
+  int* r_pos = r_ep + total;
+  if (threadIdx.x == 0) s_base = 0;
+  __syncthreads();
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  for (int c0 = 0; c0 < total; c0 += 1024) {
+    const int r = c0 + threadIdx.x;
+    int flag = 0, b = 0, pos = 0;
+    if (r < total) {
+      b = r / P; pos = r % P;
+      flag = 1;
+      if (mask && valid[b] && pos >= 1 && pos <= N && mask[((size_t)b * L + l) * N + pos - 1]) flag = 0;
+    }
+    // inclusive scan within the wave
+    int x = flag;
+    for (int o = 1; o < 64; o <<= 1) {
+      const int y = __shfl_up(x, o);
+      if (lane >= o) x += y;
+    }
+    if (lane == 63) warp_sums[wv] = x;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      int acc = 0;
+      for (int w = 0; w < 16; ++w) { const int t = warp_sums[w]; warp_sums[w] = acc; acc += t; }
+    }
+    __syncthreads();
+    const int excl = s_base + warp_sums[wv] + x - flag;
+    if (r < total) {
+      if (pos == 0) ep_offsets[l * B + b] = excl;
+      if (flag) { r_idx[excl] = r; r_ep[excl] = b; r_pos[excl] = pos; }
+    }
+    __syncthreads();
+    if (threadIdx.x == 1023) s_base = excl + flag;
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) counts[l] = s_base;
+  __syncthreads();
+  if (threadIdx.x < B) {
+    const int b = threadIdx.x;
+    const int next = (b + 1 < B) ? ep_offsets[l * B + b + 1] : s_base;
+    ep_counts[l * B + b] = next - ep_offsets[l * B + b];
+  }
+}
+
+// ------------------------------------------------------------------ embeddings
+// Pixel rows of the layer-0 recomputed rows, frag layout, exact integers in
+// bf16; non-visual rows and the padding columns are zero.
+__global__ void k_im2row(const uint8_t* __restrict__ frame, int views, int img, int patch,
+                         const int* __restrict__ idx, const int* __restrict__ pos_arr, int M, int P, int KB,
+                         bf16* __restrict__ x) {
+  const int chunks = KB * 4;   // 8-element chunks per row
+  const int e = blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= M * chunks) return;
+  const int m = e / chunks, k0 = (e % chunks) * 8;
+  const int pos = pos_arr[m];
+  const int N = views * (img / patch) * (img / patch);
+  const int pd = patch * patch * 3;
+  u16x8 v = {0, 0, 0, 0, 0, 0, 0, 0};
+  if (pos >= 1 && pos <= N) {
+    const int b = idx[m] / P;
+    const int n = pos - 1;
+    const int side = img / patch, per_view = side * side;
+    const int vw = n / per_view, rc = n % per_view, r = rc / side, c = rc % side;
+    const size_t base = (size_t)b * views * img * img * 3 +
+                        ((size_t)vw * img * img + (size_t)r * patch * img + (size_t)c * patch) * 3;
+    const int row_bytes = patch * 3;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int k = k0 + i;
+      if (k < pd) {
+        const int pr = k / row_bytes, pc = k % row_bytes;
+        v[i] = f2bf((float)frame[base + (size_t)pr * img * 3 + pc]);
+      }
+    }
+  }
+  *(u16x8*)(x + frag_off(m, k0, KB)) = v;
+}
+
+__global__ void k_embed_tokens(const bf16* __restrict__ embed, const int* __restrict__ tokens, int tok_stride, int d,
+                               float* __restrict__ x) {
+  const int b = blockIdx.y;
+  const int f = (blockIdx.x * blockDim.x + threadIdx.x) * 4;
+  if (f >= d) return;
+  const bf16* e = embed + (size_t)tokens[b * tok_stride] * d + f;
+  *(float4*)(x + (size_t)b * d + f) = float4{bf2f(e[0]), bf2f(e[1]), bf2f(e[2]), bf2f(e[3])};
+}
+
+// ------------------------------------------------------------------ RMSNorm
+// x_out (frag layout bf16) = src_row / sqrt(mean(src_row^2) + eps) * gain.
+__global__ __launch_bounds__(256) void k_rmsnorm(const float* __restrict__ src, const int* __restrict__ idx, int d,
+                                                 const float* __restrict__ gain, float eps, bf16* __restrict__ x,
+                                                 int KB) {
+  __shared__ float red[4];
+  const int m = blockIdx.x;
+  const float* row = src + (size_t)(idx ? idx[m] : m) * d;
+  float ss = 0.f;
+  for (int c = threadIdx.x * 8; c < d; c += 256 * 8) {
+    const float4 a = *(const float4*)(row + c), b = *(const float4*)(row + c + 4);
+    ss += a.x * a.x + a.y * a.y + a.z * a.z + a.w * a.w + b.x * b.x + b.y * b.y + b.z * b.z + b.w * b.w;
+  }
+  for (int o = 32; o > 0; o >>= 1) ss += __shfl_xor(ss, o);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  const float tot = red[0] + red[1] + red[2] + red[3];
+  const float inv = 1.0f / sqrtf(tot / (float)d + eps);
+  for (int c = threadIdx.x * 8; c < d; c += 256 * 8) {
+    const float4 a = *(const float4*)(row + c), b = *(const float4*)(row + c + 4);
+    const float4 ga = *(const float4*)(gain + c), gb = *(const float4*)(gain + c + 4);
+    u16x8 o = {f2bf(a.x * inv * ga.x), f2bf(a.y * inv * ga.y), f2bf(a.z * inv * ga.z), f2bf(a.w * inv * ga.w),
+               f2bf(b.x * inv * gb.x), f2bf(b.y * inv * gb.y), f2bf(b.z * inv * gb.z), f2bf(b.w * inv * gb.w)};
+    *(u16x8*)(x + frag_off(m, c, KB)) = o;
+  }
+}
+
+// ------------------------------------------------------------------ logits
+// One workgroup per head row: greedy bin token (ties to the lower id) and
+// margin p1 - p2 with the softmax normaliser over the whole vocabulary (Eq. 1).
+struct Top2 { float v1; int i1; float v2; int i2; };
+
+__device__ __forceinline__ bool better(float va, int ia, float vb, int ib) {
+  return va > vb || (va == vb && ia < ib);
+}
+
+__device__ __forceinline__ Top2 merge2(const Top2& a, const Top2& b) {
+  Top2 r;
+  if (better(a.v1, a.i1, b.v1, b.i1)) {
+    r.v1 = a.v1; r.i1 = a.i1;
+    if (better(a.v2, a.i2, b.v1, b.i1)) { r.v2 = a.v2; r.i2 = a.i2; } else { r.v2 = b.v1; r.i2 = b.i1; }
+  } else {
+    r.v1 = b.v1; r.i1 = b.i1;
+    if (better(a.v1, a.i1, b.v2, b.i2)) { r.v2 = a.v1; r.i2 = a.i1; } else { r.v2 = b.v2; r.i2 = b.i2; }
+  }
+  return r;
+}
+
+__global__ __launch_bounds__(256) void k_logits_reduce(const float* __restrict__ logits, int V, int bin_lo,
+                                                       int full_vocab, int* __restrict__ tok_out,
+                                                       float* __restrict__ margin_out, int out_stride, int out_col,
+                                                       int rows_per_ep) {
+  __shared__ float s_f[256];
+  __shared__ Top2 s_t[256];
+  const int r = blockIdx.x;
+  const float* z = logits + (size_t)r * V;
+  const int lo = full_vocab ? 0 : bin_lo;
+  const float NEG = -INFINITY;
+  float mx = NEG;
+  Top2 t = {NEG, 0x7fffffff, NEG, 0x7fffffff};
+  for (int i = lo + threadIdx.x; i < V; i += 256) {
+    const float v = z[i];
+    mx = fmaxf(mx, v);
+    if (i >= bin_lo) {
+      Top2 c = {v, i, NEG, 0x7fffffff};
+      t = merge2(t, c);
+    }
+  }
+  s_f[threadIdx.x] = mx;
+  s_t[threadIdx.x] = t;
+  __syncthreads();
+  for (int o = 128; o > 0; o >>= 1) {
+    if (threadIdx.x < o) {
+      s_f[threadIdx.x] = fmaxf(s_f[threadIdx.x], s_f[threadIdx.x + o]);
+      s_t[threadIdx.x] = merge2(s_t[threadIdx.x], s_t[threadIdx.x + o]);
+    }
+    __syncthreads();
+  }
+  const float M = s_f[0];
+  const Top2 best = s_t[0];
+  __syncthreads();
+  float sum = 0.f;
+  for (int i = lo + threadIdx.x; i < V; i += 256) sum += __expf(z[i] - M);
+  s_f[threadIdx.x] = sum;
+  __syncthreads();
+  for (int o = 128; o > 0; o >>= 1) {
+    if (threadIdx.x < o) s_f[threadIdx.x] += s_f[threadIdx.x + o];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    const float S = s_f[0];
+    const float m = (__expf(best.v1 - M) - __expf(best.v2 - M)) / S;
+    const int o = (r / rows_per_ep) * out_stride + out_col + r % rows_per_ep;
+    tok_out[o] = best.i1;
+    margin_out[o] = m;
+  }
+}
+
+// ------------------------------------------------------------------ gate
+struct Force { signed char f[64]; };
+
+// Alg. 1's test on the previous step's margins: m = mean (Eq. 1) or min over
+// the D positions; fire = !(m >= theta) unless forced; a fired episode's
+// cache becomes invalid.
+__global__ void k_gate(const float* __restrict__ margins, int B, int D, float theta, int use_min, Force force,
+                       int* __restrict__ valid, float* __restrict__ m_out, int* __restrict__ fire_out) {
+  const int b = threadIdx.x;
+  if (b >= B) return;
+  const float* mr = margins + (size_t)b * D;
+  float m;
+  if (use_min) {
+    m = mr[0];
+    for (int j = 1; j < D; ++j) m = fminf(m, mr[j]);
+    for (int j = 0; j < D; ++j) if (mr[j] != mr[j]) m = mr[j];   // NaN propagates
+  } else {
+    float s = 0.f;
+    for (int j = 0; j < D; ++j) s += mr[j];
+    m = s / (float)D;
+  }
+  int fire = !(m >= theta);
+  if (force.f[b] >= 0) fire = force.f[b] > 0;
+  if (fire) valid[b] = 0;
+  m_out[b] = m;
+  fire_out[b] = fire;
+}
+
+// ------------------------------------------------------------------ launchers
+hipError_t launch_pack(const bf16* src, int N, int K, bf16* dst, int Nblk, int KB, hipStream_t s) {
+  const size_t total = (size_t)Nblk * KB * 64;
+  const int blocks = (int)std::min<size_t>((total + 255) / 256, 65536);
+  hipLaunchKernelGGL(k_pack, dim3(blocks), dim3(256), 0, s, src, N, K, dst, Nblk, KB);
+  return hipGetLastError();
+}
+
+hipError_t launch_convert_gain(const bf16* src, float* dst, int n, hipStream_t s) {
+  hipLaunchKernelGGL(k_convert_gain, dim3((n + 255) / 256), dim3(256), 0, s, src, dst, n);
+  return hipGetLastError();
+}
+
+hipError_t launch_rope_table(float2* tab, int kv_pad, int head_dim, float theta, hipStream_t s) {
+  const int n = kv_pad * head_dim / 2;
+  hipLaunchKernelGGL(k_rope_table, dim3((n + 255) / 256), dim3(256), 0, s, tab, kv_pad, head_dim, theta);
+  return hipGetLastError();
+}
+
+hipError_t launch_fill_u32(uint32_t* p, uint32_t v, size_t n, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  const int blocks = (int)std::min<size_t>((n + 255) / 256, 65536);
+  hipLaunchKernelGGL(k_fill_u32, dim3(blocks), dim3(256), 0, s, p, v, n);
+  return hipGetLastError();
+}
+
+hipError_t launch_build_rows(const uint8_t* mask, const int* valid, int B, int L, int N, int P, int* rows,
+                             int* counts, int* ep_counts, int* ep_offsets, hipStream_t s) {
+  hipLaunchKernelGGL(k_build_rows, dim3(L), dim3(1024), 0, s, mask, valid, B, L, N, P, rows, counts, ep_counts,
+                     ep_offsets);
+  return hipGetLastError();
+}
+
+hipError_t launch_im2row(const uint8_t* frame, int views, int img, int patch, const int* idx, const int* pos,
+                         int M, int P, int KB, bf16* x, hipStream_t s) {
+  const int n = M * KB * 4;
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_im2row, dim3((n + 255) / 256), dim3(256), 0, s, frame, views, img, patch, idx, pos, M, P, KB, x);
+  return hipGetLastError();
+}
+
+hipError_t launch_rmsnorm(const float* src, const int* idx, int M, int d, const float* gain, float eps, bf16* x,
+                          int KB, hipStream_t s) {
+  if (M == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_rmsnorm, dim3(M), dim3(256), 0, s, src, idx, d, gain, eps, x, KB);
+  return hipGetLastError();
+}
+
+hipError_t launch_embed_tokens(const bf16* embed, const int* tokens, int tok_stride, int B, int d, float* x,
+                               hipStream_t s) {
+  dim3 grid((d / 4 + 255) / 256, B);
+  hipLaunchKernelGGL(k_embed_tokens, grid, dim3(256), 0, s, embed, tokens, tok_stride, d, x);
+  return hipGetLastError();
+}
+
+hipError_t launch_logits_reduce(const float* logits, int rows, int V, int bin_lo, int full_vocab, int* tok_out,
+                                float* margin_out, int out_stride, int out_col, int rows_per_ep, hipStream_t s) {
+  hipLaunchKernelGGL(k_logits_reduce, dim3(rows), dim3(256), 0, s, logits, V, bin_lo, full_vocab, tok_out,
+                     margin_out, out_stride, out_col, rows_per_ep);
+  return hipGetLastError();
+}
+
+hipError_t launch_gate(const float* margins, int B, int D, float theta, int use_min, const int8_t* force, int* valid,
+                       float* m_out, int* fire_out, hipStream_t s) {
+  Force f;
+  for (int b = 0; b < 64; ++b) f.f[b] = (force && b < B) ? force[b] : -1;
+  hipLaunchKernelGGL(k_gate, dim3(1), dim3(64), 0, s, margins, B, D, theta, use_min, f, valid, m_out, fire_out);
+  return hipGetLastError();
+}
+
+}  // namespace gvc

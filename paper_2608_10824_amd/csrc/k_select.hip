@@ -1,0 +1,110 @@
+// Stage 1 static-patch detection and the applied per-layer reuse proportion.
+//
+// Sec. III-B, Stage 1: corresponding p x p patches of I_t and I_{t-1} are
+// compared by cosine similarity; similarity above tau marks a patch static.
+// Stage 3 (applied): each layer reuses its own share of the static set.
+// Everything is integer: per patch the exact dot product and both squared
+// norms (int32: 588 * 255^2 < 2^31), the test dot^2 den^2 > num^2 na nb and
+// the ranking comparator dot_i^2 na_j nb_j vs dot_j^2 na_i nb_i in 128-bit
+// unsigned arithmetic, so the masks are exact.
+#include "gvc_kernels.h"
+
+namespace gvc {
+
+// One wave per patch: stats[(b*N + n)*3 + {0,1,2}] = dot, |u|^2, |v|^2.
+__global__ __launch_bounds__(64) void k_patch_stats(const uint8_t* __restrict__ ft, const uint8_t* __restrict__ fp,
+                                                    int views, int img, int patch, int* __restrict__ stats) {
+  const int n = blockIdx.x, b = blockIdx.y;
+  const int side = img / patch, per_view = side * side;
+  const int v = n / per_view, rc = n % per_view, r = rc / side, c = rc % side;
+  const int row_bytes = patch * 3;
+  const size_t frame_bytes = (size_t)views * img * img * 3;
+  const size_t base = (size_t)b * frame_bytes + ((size_t)v * img * img + (size_t)r * patch * img + (size_t)c * patch) * 3;
+  int dot = 0, na = 0, nb = 0;
+  for (int e = threadIdx.x; e < patch * row_bytes; e += 64) {
+    const int pr = e / row_bytes, pc = e % row_bytes;
+    const size_t off = base + (size_t)pr * img * 3 + pc;
+    const int u = ft[off], w = fp[off];
+    dot += u * w; na += u * u; nb += w * w;
+  }
+  for (int o = 32; o > 0; o >>= 1) {
+    dot += __shfl_down(dot, o);
+    na += __shfl_down(na, o);
+    nb += __shfl_down(nb, o);
+  }
+  if (threadIdx.x == 0) {
+    int* s = stats + ((size_t)b * gridDim.x + n) * 3;
+    s[0] = dot; s[1] = na; s[2] = nb;
+  }
+}
+
+typedef unsigned __int128 u128;
+
+struct Permille { int q[128]; };
+
+// One workgroup per episode: static flags, exact ranks, |S|, per-layer masks.
+__global__ __launch_bounds__(512) void k_rank_mask(const int* __restrict__ stats, int N, int L, long long tau_num,
+                                                   long long tau_den, Permille pm, uint8_t* __restrict__ mask,
+                                                   int* __restrict__ n_static) {
+  extern __shared__ unsigned long long sh[];   // [N] cos^2 numerator, [N] denominator (0 = not static)
+  unsigned long long* knum = sh;
+  unsigned long long* kden = sh + N;
+  __shared__ int s_count;
+  const int b = blockIdx.x;
+  if (threadIdx.x == 0) s_count = 0;
+  __syncthreads();
+  const unsigned long long num2 = (unsigned long long)(tau_num * tau_num);
+  const unsigned long long den2 = (unsigned long long)(tau_den * tau_den);
+  for (int n = threadIdx.x; n < N; n += blockDim.x) {
+    const int* s = stats + ((size_t)b * N + n) * 3;
+    const long long dot = s[0], na = s[1], nb = s[2];
+    unsigned long long kn = 0, kd = 0;   // kd == 0 marks "not static"
+    if (na == 0 && nb == 0) {
+      kn = 1; kd = 1;
+    } else if (na != 0 && nb != 0 && dot > 0) {
+      const unsigned long long d2 = (unsigned long long)dot * (unsigned long long)dot;
+      const unsigned long long nn = (unsigned long long)na * (unsigned long long)nb;
+      if ((u128)d2 * den2 > (u128)nn * num2) { kn = d2; kd = nn; }
+    }
+    knum[n] = kn; kden[n] = kd;
+    if (kd) atomicAdd(&s_count, 1);
+  }
+  __syncthreads();
+  const int S = s_count;
+  for (int n = threadIdx.x; n < N; n += blockDim.x) {
+    const unsigned long long kn = knum[n], kd = kden[n];
+    int rank = 0;
+    if (kd) {
+      for (int j = 0; j < N; ++j) {
+        const unsigned long long jd = kden[j];
+        if (!jd || j == n) continue;
+        const u128 lhs = (u128)knum[j] * kd, rhs = (u128)kn * jd;   // cos_j^2 vs cos_n^2
+        rank += (lhs > rhs) || (lhs == rhs && j < n);
+      }
+    }
+    for (int l = 0; l < L; ++l) {
+      const int k = (int)(((long long)pm.q[l] * S) / 1000);
+      mask[((size_t)b * L + l) * N + n] = (kd && rank < k) ? 1 : 0;
+    }
+  }
+  if (threadIdx.x == 0 && n_static) n_static[b] = S;
+}
+
+hipError_t launch_patch_stats(const uint8_t* ft, const uint8_t* fp, int B, int views, int img, int patch,
+                              int* stats, hipStream_t s) {
+  const int side = img / patch;
+  dim3 grid(views * side * side, B);
+  hipLaunchKernelGGL(k_patch_stats, grid, dim3(64), 0, s, ft, fp, views, img, patch, stats);
+  return hipGetLastError();
+}
+
+hipError_t launch_rank_mask(const int* stats, int B, int N, int L, long long tau_num, long long tau_den,
+                            const int* permille_host, uint8_t* mask, int* n_static, hipStream_t s) {
+  Permille pm;
+  for (int l = 0; l < 128; ++l) pm.q[l] = l < L ? permille_host[l] : 0;
+  const size_t shm = (size_t)N * 2 * sizeof(unsigned long long);
+  hipLaunchKernelGGL(k_rank_mask, dim3(B), dim3(512), shm, s, stats, N, L, tau_num, tau_den, pm, mask, n_static);
+  return hipGetLastError();
+}
+
+}  // namespace gvc

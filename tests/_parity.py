@@ -1,0 +1,78 @@
+"""Helpers shared by the GPU parity tests (comparison rules, device copies)."""
+import numpy as np
+import torch
+
+TOL = 2e-2   # max |gpu - oracle| / max |oracle| on logits, K/V and hidden states
+
+
+def rel_err(g, o) -> float:
+    g = np.asarray(g, dtype=np.float64)
+    o = np.asarray(o, dtype=np.float64)
+    den = np.abs(o).max()
+    return float(np.abs(g - o).max() / (den if den > 0 else 1.0))
+
+
+def to_dev(w, dev):
+    out = {k: v.to(dev) for k, v in w.items() if k != "layers"}
+    out["layers"] = [{k: v.to(dev) for k, v in lw.items()} for lw in w["layers"]]
+    return out
+
+
+def gpu_k(sess, l, P):
+    """K of layer l as [B][pos][H][dh] float64 for pos < P."""
+    from paper_2608_10824_amd import gvc
+    k = sess.read(gvc.STATE_K, l).float().cpu().numpy()      # [B][H][kv_pad][dh]
+    return k[:, :, :P, :].transpose(0, 2, 1, 3)
+
+
+def gpu_v(sess, l, P):
+    from paper_2608_10824_amd import gvc
+    v = sess.read(gvc.STATE_V, l).float().cpu().numpy()      # [B][H][dh][kv_pad]
+    return v[:, :, :, :P].transpose(0, 3, 1, 2)
+
+
+def check_tokens(tok_g, logits_g, tok_o, logits_o, bin_lo):
+    """Tokens must be the argmax of the GPU's own logits (ties to the lower
+    id), and equal the oracle's except where the oracle's top-2 bin gap is
+    within twice the largest logit error at that position.  Returns the
+    number of accepted near-ties."""
+    ties = 0
+    tok_g, tok_o = np.asarray(tok_g), np.asarray(tok_o)
+    for idx in np.ndindex(tok_g.shape):
+        zg = np.asarray(logits_g[idx], dtype=np.float64)
+        zo = np.asarray(logits_o[idx], dtype=np.float64)
+        bins_g = zg[bin_lo:]
+        assert tok_g[idx] == bin_lo + int(np.argmax(bins_g)), "token is not the argmax of its own logits"
+        if tok_g[idx] != tok_o[idx]:
+            eps = np.abs(zg - zo).max()
+            s = np.sort(zo[bin_lo:])[::-1]
+            assert s[0] - s[1] < 2 * eps, "token differs at %s beyond the near-tie band" % (idx,)
+            ties += 1
+    return ties
+
+
+def margin_bounds(logits_g, logits_o, bin_lo, full_vocab=True):
+    """Per-position bound on |m_gpu - m_oracle| implied by the logit error.
+
+    If every logit of a position moves by at most eps, every softmax
+    probability moves by a factor within [e^-2eps, e^2eps], so the margin
+    p1 - p2 moves by at most (p1 + p2)(e^2eps - 1), whichever ids end up
+    first and second.  fp32 rounding of the margin itself adds 1e-6."""
+    zg = np.asarray(logits_g, dtype=np.float64)
+    zo = np.asarray(logits_o, dtype=np.float64)
+    out = np.zeros(zo.shape[:-1])
+    for idx in np.ndindex(out.shape):
+        eps = np.abs(zg[idx] - zo[idx]).max()
+        dom = zo[idx] if full_vocab else zo[idx][bin_lo:]
+        p = np.exp(dom - dom.max())
+        p /= p.sum()
+        b = np.sort(np.exp(zo[idx][bin_lo:] - dom.max()) / np.exp(dom - dom.max()).sum())[::-1]
+        out[idx] = (b[0] + b[1]) * np.expm1(2 * eps) + 1e-6
+    return out
+
+
+def check_margins(m_g, m_o, logits_g, logits_o, bin_lo, full_vocab=True):
+    bound = margin_bounds(logits_g, logits_o, bin_lo, full_vocab)
+    diff = np.abs(np.asarray(m_g, dtype=np.float64) - np.asarray(m_o))
+    assert (diff <= bound).all(), "margin error %s exceeds bound %s" % (diff, bound)
+    return bound
