@@ -28,9 +28,6 @@ int32_t fail(int32_t code, const std::string& msg) {
   } while (0)
 
 constexpr size_t kAlign = 256;
-constexpr size_t kPartialBytes = size_t(64) << 20;   // split-K partial tiles
-constexpr int kTickets = 1 << 16;
-constexpr int kTargetWgs = 1024;
 
 struct Bump {
   size_t off = 0;
@@ -59,8 +56,9 @@ struct Plan {
   size_t H_off, K_off, V_off, valid_off, margins_off, head_logits_off, rowcount_off, state_bytes;
   size_t layer_kv_elems;
   // workspace
-  size_t rows_off, counts_off, epc_off, epo_off, stats_off, x_off, q_off, o_off, r_off, act_off, xdec_off,
-      logits_off, part_off, tickets_off, rope_off, decrows_off, headrows_off, tokens_off, gate_m_off, gate_f_off,
+  size_t rows_off, counts_off, epc_off, epo_off, stats_off, x_off, q_off, o_off, r_off, act_off, xdec_off, xf_off,
+      ssq_a_off, ssq_f_off,
+      logits_off, rope_off, decrows_off, headrows_off, tokens_off, gate_m_off, gate_f_off,
       ws_bytes;
 };
 
@@ -152,9 +150,10 @@ int32_t make_plan(const gvc_desc* dsc, Plan& p) {
   p.r_off = k.take((size_t)p.Mp * d.d_model * 4);
   p.act_off = k.take((size_t)p.Mp * p.KBf * 32 * 2);
   p.xdec_off = k.take((size_t)p.B * d.d_model * 4);
+  p.xf_off = k.take((size_t)((p.B + 15) / 16 * 16) * p.KBd * 32 * 2);
+  p.ssq_a_off = k.take((size_t)p.B * (d.d_model / 32) * 4);
+  p.ssq_f_off = k.take((size_t)p.B * (d.d_model / 32) * 4);
   p.logits_off = k.take((size_t)p.B * p.V * 4);
-  p.part_off = k.take(kPartialBytes);
-  p.tickets_off = k.take((size_t)kTickets * 4);
   p.rope_off = k.take((size_t)p.kv_pad * (dh / 2) * 8);
   p.decrows_off = k.take((size_t)p.D * 3 * p.B * 4);
   p.headrows_off = k.take((size_t)3 * p.B * p.head_rows * 4);
@@ -176,7 +175,7 @@ struct gvc_ctx {
   char* ws = nullptr;
   bool prefill_done = false;
   bool decode_done = false;
-  int force_splits = 0;   // GVC_FORCE_SPLITS: split every GEMM's k range this many ways (testing)
+  int force_splits = 0;   // GVC_FORCE_SPLITS: waves splitting each GEMM's k range (4 or 8; testing)
   // launch timing of one kernel class (gvc_profile_begin / _end)
   int prof_cls = -1;
   std::vector<hipEvent_t> prof_ev;
@@ -208,27 +207,19 @@ struct gvc_ctx {
 
 namespace {
 
-// Split-K and token tiling of one GEMM launch.
+// Token tiling and k split of one GEMM launch: one workgroup per (pair of
+// weight blocks, tile of up to 16 token blocks); 8 waves split k when there
+// are fewer than 256 such workgroups, else 4.  GVC_FORCE_SPLITS (4 or 8)
+// overrides the wave count.
 void tile_gemm(GemmArgs& a, int M, int force_splits) {
   a.M = M;
   a.mblocks = (M + 15) / 16;
   a.mtiles = (a.mblocks + 15) / 16;
-  const int NT = (a.mblocks + a.mtiles - 1) / a.mtiles;
-  const int tiles = (a.n_pairs + 3) / 4;
-  const int base = tiles * a.mtiles;
-  int S = 1;
-  if (base < kTargetWgs) S = (kTargetWgs + base - 1) / base;
-  S = std::min(S, std::max(1, a.KB / 8));          // at least 8 k-steps per split
-  // Partial tiles are written and read once each; keep that traffic under a
-  // quarter of the weight bytes the launch streams.
-  const size_t per_split = (size_t)base * 4 * 2 * NT * 64 * sizeof(floatx4);
-  const size_t weight_bytes = (size_t)a.n_pairs * 2 * 16 * a.KB * 32 * 2;
-  if (force_splits > 0) S = std::min(force_splits, a.KB);
-  else
-    while (S > 1 && 2 * per_split * S > weight_bytes / 4) --S;
-  while (S > 1 && (per_split * S > kPartialBytes || base > kTickets)) --S;
-  a.kb_per_split = (a.KB + S - 1) / S;
-  a.splits = (a.KB + a.kb_per_split - 1) / a.kb_per_split;
+  const int wgs = a.n_pairs * a.mtiles;
+  int KW = wgs < 256 ? 8 : 4;
+  if (force_splits == 4 || force_splits == 8) KW = force_splits;
+  a.splits = KW;
+  a.kb_per_split = (a.KB + KW - 1) / KW;
 }
 
 int nt_of(const GemmArgs& a) { return (a.mblocks + a.mtiles - 1) / a.mtiles; }
@@ -251,8 +242,6 @@ struct ProfScope {
 GemmArgs base_args(const gvc_ctx* c) {
   GemmArgs a;
   memset(&a, 0, sizeof(a));
-  a.part = c->K<floatx4>(c->p.part_off);
-  a.tickets = c->K<int>(c->p.tickets_off);
   a.e.d = c->p.d.d_model;
   a.e.head_dim = c->p.dh;
   a.e.n_heads = c->p.H;
@@ -264,6 +253,9 @@ GemmArgs base_args(const gvc_ctx* c) {
 int32_t run_gemm(gvc_ctx* c, GemmArgs& a, int epi, int M, int cls) {
   if (M <= 0) return GVC_OK;
   tile_gemm(a, M, c->force_splits);
+  // the folded RMSNorm reads at most 8 partial sums per lane, 4 lanes per wave per row
+  if (a.e.ssq_in && (a.mblocks > 1 || a.e.ssq_parts > 8 * 4 * a.splits))
+    return fail(GVC_EINVAL, "folded norm needs one token block and at most 32 parts per wave");
   ProfScope ps(c, cls);
   HIP_TRY(launch_gemm(a, epi, nt_of(a), c->stream));
   return GVC_OK;
@@ -333,6 +325,76 @@ int32_t run_layer(gvc_ctx* c, int l, const RowMap& rows, int M, float* src, floa
     a.x = reinterpret_cast<const bf16x8*>(A);
     a.e.rows = rows; a.e.resid = R; a.e.resid_mapped = 0; a.e.out = dst; a.e.out_mapped = mapped;
     int32_t r = run_gemm(c, a, EPI_RESID, M, k0 + 4);
+    if (r) return r;
+  }
+  return GVC_OK;
+}
+
+// One decoder layer of a single-token decode pass over the B rows of xdec,
+// with every RMSNorm folded into the GEMMs: the projection input is
+// bf16(x * gain) written by the previous epilogue (or the token embedding)
+// and the accumulator is scaled by 1/rms from per-workgroup partial sums of
+// squares, summed in a fixed order.  ssq_parts_in: parts of the input rows'
+// sums of squares (1 after the embedding, d/32 after a down projection).
+int32_t run_layer_decode(gvc_ctx* c, int l, const RowMap& rows, int n_keys, int ssq_parts_in) {
+  const Plan& p = c->p;
+  const int B = p.B, dm = p.d.d_model;
+  const float* gains = c->W<float>(p.gains_off) + (size_t)l * 2 * dm;
+  const float* next_gain = l + 1 < p.L ? gains + 2 * dm : c->W<float>(p.final_gain_off);
+  bf16* X = c->K<bf16>(p.x_off);
+  bf16* XF = c->K<bf16>(p.xf_off);
+  bf16* Q = c->K<bf16>(p.q_off);
+  bf16* O = c->K<bf16>(p.o_off);
+  float* R = c->K<float>(p.r_off);
+  bf16* A = c->K<bf16>(p.act_off);
+  float* xdec = c->K<float>(p.xdec_off);
+  float* ssq_a = c->K<float>(p.ssq_a_off);
+  float* ssq_f = c->K<float>(p.ssq_f_off);
+  const int parts_d = dm / 32;
+  {
+    GemmArgs a = base_args(c);
+    a.w[0] = c->packed(p.wq[l]); a.w[1] = c->packed(p.wk[l]); a.w[2] = c->packed(p.wv[l]);
+    a.wblk[0] = a.wblk[1] = a.wblk[2] = p.wq[l].Nblk;
+    a.map = MAP_QKV; a.n_pairs = 3 * p.wq[l].Nblk / 2; a.n_out = dm; a.KB = p.KBd;
+    a.x = reinterpret_cast<const bf16x8*>(X);
+    a.e.rows = rows; a.e.q = Q; a.e.kc = c->Kc(l); a.e.vc = c->Vc(l);
+    a.e.ssq_in = ssq_a; a.e.ssq_parts = ssq_parts_in; a.e.norm_eps = p.d.rms_eps; a.e.norm_dim = dm;
+    int32_t r = run_gemm(c, a, EPI_QKV, B, GVC_K_DECODE_QKV);
+    if (r) return r;
+  }
+  {
+    ProfScope ps(c, GVC_K_DECODE_ATTN);
+    HIP_TRY(launch_attn_decode(Q, c->Kc(l), c->Vc(l), B, p.H, p.dh, p.kv_pad, n_keys, O, p.KBd, c->stream));
+  }
+  {
+    GemmArgs a = base_args(c);
+    a.w[0] = c->packed(p.wo[l]); a.wblk[0] = p.wo[l].Nblk;
+    a.map = MAP_PLAIN; a.n_pairs = (p.wo[l].Nblk + 1) / 2; a.n_out = dm; a.KB = p.KBd;
+    a.x = reinterpret_cast<const bf16x8*>(O);
+    a.e.rows = rows; a.e.resid = xdec; a.e.out = R;
+    a.e.xn = XF; a.e.xn_gain = gains + dm; a.e.ssq_out = ssq_f; a.e.xn_kb = p.KBd; a.e.ssq_out_parts = parts_d;
+    int32_t r = run_gemm(c, a, EPI_RESID, B, GVC_K_DECODE_O);
+    if (r) return r;
+  }
+  {
+    GemmArgs a = base_args(c);
+    a.w[0] = c->packed(p.wg[l]); a.w[1] = c->packed(p.wu[l]);
+    a.wblk[0] = a.wblk[1] = p.wg[l].Nblk;
+    a.map = MAP_GU; a.n_pairs = p.wg[l].Nblk; a.n_out = p.F; a.KB = p.KBd;
+    a.x = reinterpret_cast<const bf16x8*>(XF);
+    a.e.rows = rows; a.e.act = A; a.e.kb_act = p.KBf; a.e.n_feat = p.F;
+    a.e.ssq_in = ssq_f; a.e.ssq_parts = parts_d; a.e.norm_eps = p.d.rms_eps; a.e.norm_dim = dm;
+    int32_t r = run_gemm(c, a, EPI_SILU, B, GVC_K_DECODE_GU);
+    if (r) return r;
+  }
+  {
+    GemmArgs a = base_args(c);
+    a.w[0] = c->packed(p.wd[l]); a.wblk[0] = p.wd[l].Nblk;
+    a.map = MAP_PLAIN; a.n_pairs = (p.wd[l].Nblk + 1) / 2; a.n_out = dm; a.KB = p.KBf;
+    a.x = reinterpret_cast<const bf16x8*>(A);
+    a.e.rows = rows; a.e.resid = R; a.e.out = xdec;
+    a.e.xn = X; a.e.xn_gain = next_gain; a.e.ssq_out = ssq_a; a.e.xn_kb = p.KBd; a.e.ssq_out_parts = parts_d;
+    int32_t r = run_gemm(c, a, EPI_RESID, B, GVC_K_DECODE_DOWN);
     if (r) return r;
   }
   return GVC_OK;
@@ -544,16 +606,26 @@ int32_t gvc_decode_actions(gvc_ctx* c, int32_t* tokens_out, float* margins_out, 
     float* lg = c->K<float>(p.logits_off);
     for (int j = 1; j < p.D; ++j) {
       const int* src = forced_tokens ? forced_tokens + (j - 1) : tok + (j - 1);
-      HIP_TRY(launch_embed_tokens(c->W<bf16>(p.embed_off), src, p.D, p.B, p.d.d_model, xdec, s));
+      HIP_TRY(launch_embed_tokens(c->W<bf16>(p.embed_off), src, p.D, p.B, p.d.d_model, xdec,
+                                  c->W<float>(p.gains_off), c->K<bf16>(p.x_off), p.KBd, c->K<float>(p.ssq_a_off), s));
       const RowMap rows = c->dec_rows(j);
       const int pos = p.P + j - 1;
       for (int l = 0; l < p.L; ++l) {
-        int32_t r = run_layer(c, l, rows, p.B, xdec, xdec, false, true, pos + 1, 0, nullptr, nullptr);
+        int32_t r = run_layer_decode(c, l, rows, pos + 1, l == 0 ? 1 : p.d.d_model / 32);
         if (r) return r;
       }
-      RowMap hr{nullptr, rows.ep, rows.pos};
-      int32_t r = run_head(c, hr, xdec, p.B, lg, GVC_K_DECODE_HEAD);
-      if (r) return r;
+      {
+        // LM head on the folded final norm written by the last down projection
+        GemmArgs a = base_args(c);
+        a.w[0] = c->packed(p.lm); a.wblk[0] = p.lm.Nblk;
+        a.map = MAP_PLAIN; a.n_pairs = (p.lm.Nblk + 1) / 2; a.n_out = p.V; a.KB = p.KBd;
+        a.x = c->K<bf16x8>(p.x_off);
+        a.e.rows = rows; a.e.store = lg; a.e.ld_store = p.V;
+        a.e.ssq_in = c->K<float>(p.ssq_a_off); a.e.ssq_parts = p.d.d_model / 32;
+        a.e.norm_eps = p.d.rms_eps; a.e.norm_dim = p.d.d_model;
+        int32_t r = run_gemm(c, a, EPI_STORE, p.B, GVC_K_DECODE_HEAD);
+        if (r) return r;
+      }
       HIP_TRY(launch_logits_reduce(lg, p.B, p.V, p.bin_lo, full, tok, mg, p.D, j, 1, s));
       if (logits_out)
         HIP_TRY(hipMemcpy2DAsync(logits_out + (size_t)j * p.V, (size_t)p.D * p.V * 4, lg, (size_t)p.V * 4,

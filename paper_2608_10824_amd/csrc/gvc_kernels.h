@@ -72,6 +72,14 @@ struct EpiArgs {
   // EPI_EMBED
   float* h0; const bf16* embed; const int* text_ids; const float* extra;
   int n_patches, n_text, n_extra;
+  // Folded RMSNorm (decode): the GEMM input is bf16(x * gain) and the
+  // accumulator is scaled by 1/sqrt(sum(x^2)/norm_dim + norm_eps), the sum
+  // of squares of row m being the sum of ssq_in[m * ssq_parts + 0..parts-1].
+  const float* ssq_in; int ssq_parts; float norm_eps; int norm_dim;
+  // EPI_RESID, when xn != nullptr: also writes bf16(out * xn_gain) in frag
+  // layout (xn_kb k-fragments) and, per row, this pair's sum of squares of
+  // out into ssq_out[m * ssq_out_parts + pair].
+  bf16* xn; const float* xn_gain; float* ssq_out; int xn_kb; int ssq_out_parts;
 };
 
 struct GemmArgs {
@@ -81,13 +89,14 @@ struct GemmArgs {
   int n_pairs;          // pairs of 16-row blocks (one pair per wave)
   int n_out;            // output features of the (first) matrix, for MAP_PLAIN
   int KB;               // k-fragments (K padded / 32)
-  int splits, kb_per_split;
+  int splits, kb_per_split;   // waves per workgroup splitting k, k-steps per wave
   const bf16x8* x;      // frag-layout activations
   int M, mblocks, mtiles;
-  floatx4* part;        // split-K partials
-  int* tickets;
   EpiArgs e;
 };
+
+// k-steps per pipelined register chunk for a tile of NT blocks of 16 token rows.
+constexpr int gemm_pf(int NT) { return NT == 1 ? 8 : (NT <= 3 ? 4 : (NT <= 6 ? 2 : 1)); }
 
 // ------------------------------------------------------------------ launchers
 // All launchers enqueue on `s` and return hipGetLastError().
@@ -114,12 +123,11 @@ hipError_t launch_attn_prefill(const bf16* q, const bf16* kc, const bf16* vc, co
 hipError_t launch_attn_decode(const bf16* q, const bf16* kc, const bf16* vc, int B, int H, int head_dim,
                               int kv_pad, int n_keys, bf16* o, int KB, hipStream_t s);
 hipError_t launch_embed_tokens(const bf16* embed, const int* tokens, int tok_stride, int B, int d,
-                               float* x, hipStream_t s);
+                               float* x, const float* gain, bf16* xn, int KB, float* ssq, hipStream_t s);
 hipError_t launch_logits_reduce(const float* logits, int rows, int V, int bin_lo, int full_vocab,
                                 int* tok_out, float* margin_out, int out_stride, int out_col,
                                 int rows_per_ep, hipStream_t s);
 hipError_t launch_gate(const float* margins, int B, int D, float theta, int use_min, const int8_t* force,
                        int* valid, float* m_out, int* fire_out, hipStream_t s);
-hipError_t launch_select_tokens(const int* src, int src_stride, int col, int B, int* dst, hipStream_t s);
 
 }  // namespace gvc

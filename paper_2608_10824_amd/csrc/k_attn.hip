@@ -117,34 +117,55 @@ __global__ __launch_bounds__(64) void k_attn_prefill(const bf16* __restrict__ q,
 }
 
 // One workgroup per (head, episode): a single query at position n_keys-1.
+// Scores: DH/8 lanes per key, each lane a 16-byte run of dims, so one wave
+// instruction reads whole key rows contiguously; partial dots are summed
+// across the lane group.  Values: the cache is dim-major, so a lane reads
+// 8 consecutive keys of one dim and a wave instruction reads 4 dims x 16
+// chunks = 4 contiguous 256-byte runs.  Both phases issue a batch of loads
+// (clamped addresses, results masked) before consuming any of them, so the
+// kernel pays the memory latency a few times rather than once per key group.
 template <int DH>
 __global__ __launch_bounds__(256) void k_attn_decode(const bf16* __restrict__ q, const bf16* __restrict__ kc,
                                                      const bf16* __restrict__ vc, int H, int kv_pad, int n_keys,
                                                      bf16* __restrict__ o, int KB) {
-  extern __shared__ float sc[];          // [kv_pad] scores
-  __shared__ float qs[DH];
+  extern __shared__ float sc[];          // [kv_pad] scores, then probabilities
   __shared__ float red[8];
-  __shared__ float part[256];
+  constexpr int LPK = DH / 8;            // lanes per key
+  constexpr int KPI = 256 / LPK;         // keys per load round
+  constexpr int U = 8;                   // load rounds per batch
+  constexpr int ND = DH / 16;            // dims per thread in the value phase
+  constexpr int UC = 3;                  // 8-key chunks per lane per value batch
   const int h = blockIdx.x, b = blockIdx.y;
   const int d = H * DH;
   const int tid = threadIdx.x;
-  if (tid < DH) qs[tid] = bf2f(q[(size_t)b * d + h * DH + tid]);
-  __syncthreads();
-  const bf16* kbase = kc + (size_t)(b * H + h) * kv_pad * DH;
+  const int sub = tid % LPK, kg = tid / LPK;
+  float qv[8];
+  {
+    const u16x8 qq = *(const u16x8*)(q + (size_t)b * d + h * DH + sub * 8);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) qv[i] = bf2f(qq[i]);
+  }
+  const bf16* kbase = kc + (size_t)(b * H + h) * kv_pad * DH + sub * 8;
   const float scale = 1.0f / sqrtf((float)DH);
   float mx = -INFINITY;
-  for (int j = tid; j < n_keys; j += 256) {
-    const bf16* kr = kbase + (size_t)j * DH;
-    float s = 0.f;
-#pragma unroll 4
-    for (int c = 0; c < DH; c += 8) {
-      const u16x8 kv = *(const u16x8*)(kr + c);
+  for (int j0 = 0; j0 < n_keys; j0 += KPI * U) {
+    u16x8 kv[U];
 #pragma unroll
-      for (int i = 0; i < 8; ++i) s += qs[c + i] * bf2f(kv[i]);
+    for (int u = 0; u < U; ++u) kv[u] = *(const u16x8*)(kbase + (size_t)min(j0 + u * KPI + kg, n_keys - 1) * DH);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int j = j0 + u * KPI + kg;
+      float s = 0.f;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) s += qv[i] * bf2f(kv[u][i]);
+#pragma unroll
+      for (int x = LPK / 2; x > 0; x >>= 1) s += __shfl_xor(s, x);
+      s *= scale;
+      if (j < n_keys) {
+        if (sub == 0) sc[j] = s;
+        mx = fmaxf(mx, s);
+      }
     }
-    s *= scale;
-    sc[j] = s;
-    mx = fmaxf(mx, s);
   }
   for (int x = 32; x > 0; x >>= 1) mx = fmaxf(mx, __shfl_xor(mx, x));
   if ((tid & 63) == 0) red[tid >> 6] = mx;
@@ -157,24 +178,43 @@ __global__ __launch_bounds__(256) void k_attn_decode(const bf16* __restrict__ q,
     sm += p;
   }
   for (int x = 32; x > 0; x >>= 1) sm += __shfl_xor(sm, x);
-  __syncthreads();
   if ((tid & 63) == 0) red[4 + (tid >> 6)] = sm;
+  for (int j = n_keys + tid; j < (n_keys + 7) / 8 * 8; j += 256) sc[j] = 0.f;   // pad the last 8-key chunk
   __syncthreads();
   const float inv = 1.0f / (red[4] + red[5] + red[6] + red[7]);
-  // o[dim] = sum_j p_j V^T[dim][j]; 256/DH threads split the keys of one dim
-  constexpr int SPL = 256 / DH;
-  const int dim = tid % DH, sp = tid / DH;
-  const bf16* vr = vc + ((size_t)(b * H + h) * DH + dim) * kv_pad;
-  float acc = 0.f;
-  const int per = (n_keys + SPL - 1) / SPL;
-  const int j0 = sp * per, j1 = min(n_keys, j0 + per);
-  for (int j = j0; j < j1; ++j) acc += sc[j] * bf2f(vr[j]);
-  part[tid] = acc;
-  __syncthreads();
-  if (sp == 0) {
-    float t = 0.f;
-    for (int s = 0; s < SPL; ++s) t += part[s * DH + dim];
-    o[frag_off(b, h * DH + dim, KB)] = f2bf(t * inv);
+  // o[dim] = sum_j p_j V^T[dim][j]: lane16 walks 8-key chunks, 16 dim groups
+  const int l16 = tid & 15, dg = tid >> 4;
+  const int nchunk = (n_keys + 7) / 8;
+  const bf16* vb = vc + (size_t)(b * H + h) * DH * kv_pad + (size_t)dg * kv_pad;
+  float acc[ND];
+#pragma unroll
+  for (int i = 0; i < ND; ++i) acc[i] = 0.f;
+  for (int c0 = 0; c0 < nchunk; c0 += 16 * UC) {
+    u16x8 vv[ND][UC];
+#pragma unroll
+    for (int i = 0; i < ND; ++i)
+#pragma unroll
+      for (int u = 0; u < UC; ++u)
+        vv[i][u] = *(const u16x8*)(vb + (size_t)(16 * i) * kv_pad + min(c0 + 16 * u + l16, nchunk - 1) * 8);
+#pragma unroll
+    for (int u = 0; u < UC; ++u) {
+      const int c = c0 + 16 * u + l16;
+      if (c < nchunk) {
+        const float4 p0 = *(const float4*)(sc + c * 8), p1 = *(const float4*)(sc + c * 8 + 4);
+        const float pp[8] = {p0.x, p0.y, p0.z, p0.w, p1.x, p1.y, p1.z, p1.w};
+#pragma unroll
+        for (int i = 0; i < ND; ++i)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) acc[i] += pp[e] * bf2f(vv[i][u][e]);
+      }
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < ND; ++i) {
+    float t = acc[i];
+#pragma unroll
+    for (int x = 8; x > 0; x >>= 1) t += __shfl_xor(t, x);
+    if (l16 == 0) o[frag_off(b, h * DH + dg + 16 * i, KB)] = f2bf(t * inv);
   }
 }
 

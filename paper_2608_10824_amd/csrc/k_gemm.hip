@@ -7,14 +7,14 @@
 //  * MFMA v_mfma_f32_16x16x32_bf16 with the weight block as the A operand
 //    (16 output features) and 16 token rows as the B operand; every lane loads
 //    16 contiguous bytes of both operands straight from their packed layouts;
-//  * one wave owns a PAIR of 16-row weight blocks for all the tile's token
-//    rows; the pair is chosen so that the epilogue's partner values sit in
-//    the same lane and register: RoPE dims (i, i + d_h/2), SwiGLU (gate j, up j);
-//  * 4 waves per workgroup share the token fragments through LDS (NT > 1);
-//  * weight fragments are prefetched PF k-steps ahead in registers;
-//  * split-K across workgroups: partial tiles go to a workspace, the last
-//    workgroup of a tile (atomic ticket) sums them in fixed split order, so
-//    results are bitwise reproducible, then runs the epilogue.
+//  * one workgroup owns a PAIR of 16-row weight blocks for all the tile's
+//    token rows; the pair is chosen so that the epilogue's partner values
+//    sit in the same lane and register: RoPE dims (i, i + d_h/2), SwiGLU
+//    (gate j, up j);
+//  * weight and token fragments are prefetched a chunk ahead in registers;
+//  * the k range is split across the waves of one workgroup and summed in
+//    LDS in a fixed order, so results are bitwise reproducible and no
+//    workgroup ever waits on another.
 #include "gvc_kernels.h"
 
 namespace gvc {
@@ -43,14 +43,22 @@ __device__ __forceinline__ void map_pair(const GemmArgs& a, int pair, int& mat_a
 
 __device__ __forceinline__ float silu_f(float g) { return g / (1.0f + __expf(-g)); }
 
+// Epilogue of one lane: 4 consecutive output features of block A and of
+// block B for token row m.  Every lane of the wave calls it (some epilogues
+// shuffle across lanes); `valid` says whether row m exists (m is already
+// clamped into range for address arithmetic).  rs scales the accumulators
+// (folded RMSNorm, 1 otherwise).
 template <int EPI>
-__device__ __forceinline__ void epilogue(const GemmArgs& a, int pair, int lane, int m, const floatx4& va,
-                                         const floatx4& vb, bool b_ok) {
+__device__ __forceinline__ void epilogue(const GemmArgs& a, int pair, int lane, int m, floatx4 va, floatx4 vb,
+                                         bool b_ok, bool valid, float rs) {
   const EpiArgs& e = a.e;
   int mat_a, blk_a, mat_b, blk_b; bool bo;
   map_pair(a, pair, mat_a, blk_a, mat_b, blk_b, bo);
+  va *= rs;
+  vb *= rs;
   const int sub = (lane >> 4) * 4;   // first of the 4 features this lane holds
   if constexpr (EPI == EPI_QKV) {
+    if (!valid) return;
     const int dh = e.head_dim, half = dh >> 1;
     const int head = blk_a / (dh >> 4);
     const int ia = (blk_a % (dh >> 4)) * 16 + sub;   // dim within head, < half
@@ -93,33 +101,52 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, int pair, int lane, 
     const int d = e.d;
     const size_t ri = (size_t)(e.resid_mapped ? e.rows.idx[m] : m) * d;
     const size_t oi = (size_t)(e.out_mapped ? e.rows.idx[m] : m) * d;
-    const int fa = blk_a * 16 + sub;
-    {
-      const float4 r = *(const float4*)(e.resid + ri + fa);
-      float4 o; o.x = r.x + va[0]; o.y = r.y + va[1]; o.z = r.z + va[2]; o.w = r.w + va[3];
-      *(float4*)(e.out + oi + fa) = o;
-    }
+    const int fa = blk_a * 16 + sub, fb = blk_b * 16 + sub;
+    const float4 r0 = *(const float4*)(e.resid + ri + fa);
+    const float4 oa = {r0.x + va[0], r0.y + va[1], r0.z + va[2], r0.w + va[3]};
+    float4 ob = {0.f, 0.f, 0.f, 0.f};
     if (b_ok) {
-      const int fb = blk_b * 16 + sub;
-      const float4 r = *(const float4*)(e.resid + ri + fb);
-      float4 o; o.x = r.x + vb[0]; o.y = r.y + vb[1]; o.z = r.z + vb[2]; o.w = r.w + vb[3];
-      *(float4*)(e.out + oi + fb) = o;
+      const float4 r1 = *(const float4*)(e.resid + ri + fb);
+      ob = float4{r1.x + vb[0], r1.y + vb[1], r1.z + vb[2], r1.w + vb[3]};
+    }
+    if (valid) {
+      *(float4*)(e.out + oi + fa) = oa;
+      if (b_ok) *(float4*)(e.out + oi + fb) = ob;
+    }
+    if (e.xn) {   // folded RMSNorm input of the next projection
+      const float4 ga = *(const float4*)(e.xn_gain + fa);
+      float ss = oa.x * oa.x + oa.y * oa.y + oa.z * oa.z + oa.w * oa.w;
+      if (valid)
+        *(u16x4*)(e.xn + frag_off(m, fa, e.xn_kb)) =
+            u16x4{f2bf(oa.x * ga.x), f2bf(oa.y * ga.y), f2bf(oa.z * ga.z), f2bf(oa.w * ga.w)};
+      if (b_ok) {
+        const float4 gb = *(const float4*)(e.xn_gain + fb);
+        ss += ob.x * ob.x + ob.y * ob.y + ob.z * ob.z + ob.w * ob.w;
+        if (valid)
+          *(u16x4*)(e.xn + frag_off(m, fb, e.xn_kb)) =
+              u16x4{f2bf(ob.x * gb.x), f2bf(ob.y * gb.y), f2bf(ob.z * gb.z), f2bf(ob.w * gb.w)};
+      }
+      ss += __shfl_xor(ss, 16);
+      ss += __shfl_xor(ss, 32);
+      if (valid && lane < 16) e.ssq_out[(size_t)m * e.ssq_out_parts + pair] = ss;
     }
   } else if constexpr (EPI == EPI_SILU) {
     const int f = blk_a * 16 + sub;
-    if (f < e.n_feat) {
+    if (valid && f < e.n_feat) {
       u16x4 o;
 #pragma unroll
       for (int i = 0; i < 4; ++i) o[i] = f2bf(silu_f(va[i]) * vb[i]);
       *(u16x4*)(e.act + frag_off(m, f, e.kb_act)) = o;
     }
   } else if constexpr (EPI == EPI_STORE) {
+    if (!valid) return;
     float* o = e.store + (size_t)m * e.ld_store;
     const int fa = blk_a * 16 + sub;
     if (fa < a.n_out) *(float4*)(o + fa) = float4{va[0], va[1], va[2], va[3]};
     const int fb = blk_b * 16 + sub;
     if (b_ok && fb < a.n_out) *(float4*)(o + fb) = float4{vb[0], vb[1], vb[2], vb[3]};
   } else {  // EPI_EMBED
+    if (!valid) return;
     const int d = e.d;
     const int pos = e.rows.pos[m], b = e.rows.ep[m];
     float* h = e.h0 + (size_t)e.rows.idx[m] * d;
@@ -145,124 +172,148 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, int pair, int lane, 
   }
 }
 
-template <int NT, int PF, int EPI>
-__global__ __launch_bounds__(256) void k_gemm(const GemmArgs a) {
-  constexpr int XS = NT > 1 ? NT * PF * 64 : 1;
-  __shared__ bf16x8 xs[XS];
-  __shared__ int s_last;
-
+// One workgroup owns one pair of weight blocks and NT blocks of 16 token
+// rows; its KW waves split the k range and their accumulators are summed
+// through LDS in wave order (deterministic, no cross-workgroup traffic).
+// Each wave streams its share in chunks of PF k-steps, double-buffered in
+// registers with no branch between a chunk's loads and its MFMAs, so two
+// chunks are in flight; the prefetch of the chunk after the last re-reads
+// the last chunk instead of branching.  Token fragments come straight from
+// the (L2-resident) activations.
+template <int KW, int NT, int PF, int EPI>
+__global__ __launch_bounds__(KW * 64) void k_gemm_ks(const GemmArgs a) {
+  __shared__ floatx4 red[KW][2][64];
+  __shared__ float ssq_red[KW][16];
+  __shared__ float rscale[16];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int split = blockIdx.x % a.splits, tile = blockIdx.x / a.splits, mt = blockIdx.y;
-  const int pair = tile * 4 + wave;
-  const bool p_ok = pair < a.n_pairs;
+  const int pair = blockIdx.x, mt = blockIdx.y;
+  // Folded RMSNorm (single token block): lane (row r = lane % 16, chunk
+  // wave * 4 + lane / 16) loads up to SQ of the row's partial sums of squares
+  // now and adds them after the main loop, so the loads overlap the stream.
+  constexpr int SQ = 8;
+  float sq[SQ];
+  const bool fold = NT == 1 && a.e.ssq_in != nullptr;
+  if (fold) {
+    const int r = min(lane & 15, a.M - 1);
+    const int nch = KW * 4, ch = wave * 4 + (lane >> 4);
+    const int per = (a.e.ssq_parts + nch - 1) / nch;
+    const float* sp = a.e.ssq_in + (size_t)r * a.e.ssq_parts;
+#pragma unroll
+    for (int i = 0; i < SQ; ++i) {
+      const int idx = ch * per + i;
+      const float v = sp[min(idx, a.e.ssq_parts - 1)];
+      sq[i] = (i < per && idx < a.e.ssq_parts) ? v : 0.f;
+    }
+  }
   int mat_a, blk_a, mat_b, blk_b; bool b_ok;
-  map_pair(a, p_ok ? pair : 0, mat_a, blk_a, mat_b, blk_b, b_ok);
+  map_pair(a, pair, mat_a, blk_a, mat_b, blk_b, b_ok);
   const bf16x8* wa = a.w[mat_a] + (size_t)blk_a * a.KB * 64 + lane;
   const bf16x8* wb = a.w[mat_b] + (size_t)blk_b * a.KB * 64 + lane;
-
-  const int kb0 = split * a.kb_per_split;
+  const int mb0 = mt * NT;
+  // token block t of this tile, clamped to the last existing block (its
+  // results for rows >= M are never stored)
+  const bf16x8* xg[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t) xg[t] = a.x + (size_t)min(mb0 + t, a.mblocks - 1) * a.KB * 64 + lane;
+  const int kb0 = min(a.KB, wave * a.kb_per_split);
   const int kb1 = min(a.KB, kb0 + a.kb_per_split);
   const int nsteps = kb1 - kb0;
-  const int mb0 = mt * NT;  // first token block of this tile
-  const bf16x8* xg = a.x + (size_t)mb0 * a.KB * 64;
+  const int nchunks = nsteps / PF;
 
   floatx4 acc_a[NT], acc_b[NT];
 #pragma unroll
   for (int t = 0; t < NT; ++t) { acc_a[t] = floatx4{0, 0, 0, 0}; acc_b[t] = floatx4{0, 0, 0, 0}; }
-
-  bf16x8 ra[PF], rb[PF], rx[NT == 1 ? PF : 1];
-  const bf16x8 zero8 = bf16x8{};
-#pragma unroll
-  for (int p = 0; p < PF; ++p) {
-    if (p < nsteps) {
-      ra[p] = wa[(size_t)(kb0 + p) * 64];
-      rb[p] = wb[(size_t)(kb0 + p) * 64];
-      if constexpr (NT == 1) rx[p] = mb0 < a.mblocks ? xg[(size_t)(kb0 + p) * 64 + lane] : zero8;
-    }
-  }
-
-  for (int base = 0; base < nsteps; base += PF) {
-    if constexpr (NT > 1) {
-      __syncthreads();
-      for (int e = threadIdx.x; e < NT * PF * 64; e += 256) {
-        const int t = e / (PF * 64), p = (e >> 6) % PF, ln = e & 63;
-        const int kb = kb0 + base + p;
-        bf16x8 v = zero8;
-        if (kb < kb1 && mb0 + t < a.mblocks) v = xg[((size_t)t * a.KB + kb) * 64 + ln];
-        xs[e] = v;
-      }
-      __syncthreads();
-    }
+  bf16x8 a0[PF], b0[PF], x0[PF][NT], a1[PF], b1[PF], x1[PF][NT];
+  auto load = [&](bf16x8 (&A)[PF], bf16x8 (&Bv)[PF], bf16x8 (&X)[PF][NT], int c) {
+    const size_t kb = (size_t)(kb0 + min(c, nchunks - 1) * PF) * 64;
 #pragma unroll
     for (int p = 0; p < PF; ++p) {
-      const int s = base + p;
-      if (s < nsteps) {
-        const bf16x8 a0 = ra[p], a1 = rb[p];
-        bf16x8 x0 = zero8;
-        if constexpr (NT == 1) x0 = rx[p];
-        if (s + PF < nsteps) {
-          ra[p] = wa[(size_t)(kb0 + s + PF) * 64];
-          rb[p] = wb[(size_t)(kb0 + s + PF) * 64];
-          if constexpr (NT == 1) rx[p] = mb0 < a.mblocks ? xg[(size_t)(kb0 + s + PF) * 64 + lane] : zero8;
-        }
+      A[p] = wa[kb + p * 64];
+      Bv[p] = wb[kb + p * 64];
 #pragma unroll
-        for (int t = 0; t < NT; ++t) {
-          const bf16x8 xb = NT > 1 ? xs[(t * PF + p) * 64 + lane] : x0;
-          acc_a[t] = mfma16(a0, xb, acc_a[t]);
-          acc_b[t] = mfma16(a1, xb, acc_b[t]);
-        }
+      for (int t = 0; t < NT; ++t) X[p][t] = xg[t][kb + p * 64];
+    }
+  };
+  auto compute = [&](const bf16x8 (&A)[PF], const bf16x8 (&Bv)[PF], const bf16x8 (&X)[PF][NT]) {
+#pragma unroll
+    for (int p = 0; p < PF; ++p)
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        acc_a[t] = mfma16(A[p], X[p][t], acc_a[t]);
+        acc_b[t] = mfma16(Bv[p], X[p][t], acc_b[t]);
       }
+  };
+  if (nchunks > 0) {
+    load(a0, b0, x0, 0);
+    int c = 0;
+    for (; c + 1 < nchunks; c += 2) {
+      load(a1, b1, x1, c + 1);
+      compute(a0, b0, x0);
+      load(a0, b0, x0, c + 2);
+      compute(a1, b1, x1);
+    }
+    if (c < nchunks) compute(a0, b0, x0);
+  }
+  for (int s = nchunks * PF; s < nsteps; ++s) {   // ragged k tail
+    const size_t kb = (size_t)(kb0 + s) * 64;
+    const bf16x8 wva = wa[kb], wvb = wb[kb];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      const bf16x8 xv = xg[t][kb];
+      acc_a[t] = mfma16(wva, xv, acc_a[t]);
+      acc_b[t] = mfma16(wvb, xv, acc_b[t]);
     }
   }
-
+  if (fold) {
+    float t = 0.f;
+#pragma unroll
+    for (int i = 0; i < SQ; ++i) t += sq[i];
+    t += __shfl_xor(t, 16);
+    t += __shfl_xor(t, 32);
+    if (lane < 16) ssq_red[wave][lane] = t;
+    __syncthreads();
+    if (wave == 0 && lane < 16) {
+      float u = ssq_red[0][lane];
+#pragma unroll
+      for (int w = 1; w < KW; ++w) u += ssq_red[w][lane];
+      rscale[lane] = 1.0f / sqrtf(u / (float)a.e.norm_dim + a.e.norm_eps);
+    }
+  }
+  // Reduce over the KW waves, one token block per round; wave t % KW keeps
+  // the sum of block t and runs its epilogue.
   const int col = lane & 15;
-  if (a.splits > 1) {
-    const int tile_id = tile * a.mtiles + mt;
-    floatx4* P = a.part + ((size_t)tile_id * a.splits * 4 + wave) * 2 * NT * 64 + lane;
-    const size_t split_stride = (size_t)4 * 2 * NT * 64;
-#pragma unroll
-    for (int t = 0; t < NT; ++t) {
-      const int m = (mb0 + t) * 16 + col;
-      if (m < a.M) {
-        P[split * split_stride + (size_t)t * 64] = acc_a[t];
-        P[split * split_stride + (size_t)(NT + t) * 64] = acc_b[t];
-      }
-    }
-    __threadfence();
-    __syncthreads();
-    if (threadIdx.x == 0) s_last = atomicAdd(&a.tickets[tile_id], 1) == a.splits - 1;
-    __syncthreads();
-    if (!s_last) return;
-    __threadfence();
-#pragma unroll
-    for (int t = 0; t < NT; ++t) {
-      const int m = (mb0 + t) * 16 + col;
-      floatx4 sa = floatx4{0, 0, 0, 0}, sb = floatx4{0, 0, 0, 0};
-      if (m < a.M) {
-        for (int s = 0; s < a.splits; ++s) {
-          sa += P[s * split_stride + (size_t)t * 64];
-          sb += P[s * split_stride + (size_t)(NT + t) * 64];
-        }
-      }
-      acc_a[t] = sa; acc_b[t] = sb;
-    }
-    if (threadIdx.x == 0) a.tickets[tile_id] = 0;
-  }
-
-  if (!p_ok) return;
 #pragma unroll
   for (int t = 0; t < NT; ++t) {
+    red[wave][0][lane] = acc_a[t];
+    red[wave][1][lane] = acc_b[t];
+    __syncthreads();
+    if (wave == t % KW) {
+      floatx4 sa = red[0][0][lane], sb = red[0][1][lane];
+#pragma unroll
+      for (int w = 1; w < KW; ++w) { sa += red[w][0][lane]; sb += red[w][1][lane]; }
+      acc_a[t] = sa; acc_b[t] = sb;
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    if (wave != t % KW) continue;
     const int m = (mb0 + t) * 16 + col;
-    if (m < a.M) epilogue<EPI>(a, pair, lane, m, acc_a[t], acc_b[t], b_ok);
+    const float rs = fold ? rscale[col] : 1.0f;
+    epilogue<EPI>(a, pair, lane, min(m, a.M - 1), acc_a[t], acc_b[t], b_ok, m < a.M, rs);
   }
 }
 
 template <int EPI, int NT>
 static hipError_t launch_nt(const GemmArgs& a, hipStream_t s) {
-  constexpr int PF = NT == 1 ? 8 : (NT <= 8 ? 4 : 2);
-  const int tiles = (a.n_pairs + 3) / 4;
-  dim3 grid(tiles * a.splits, a.mtiles);
-  hipLaunchKernelGGL((k_gemm<NT, PF, EPI>), grid, dim3(256), 0, s, a);
+  constexpr int PF = gemm_pf(NT);
+  const dim3 grid(a.n_pairs, a.mtiles);
+  if (a.splits == 8)
+    hipLaunchKernelGGL((k_gemm_ks<8, NT, PF, EPI>), grid, dim3(8 * 64), 0, s, a);
+  else if (a.splits == 4)
+    hipLaunchKernelGGL((k_gemm_ks<4, NT, PF, EPI>), grid, dim3(4 * 64), 0, s, a);
+  else
+    return hipErrorInvalidValue;
   return hipGetLastError();
 }
 

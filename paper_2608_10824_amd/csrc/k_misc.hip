@@ -141,13 +141,27 @@ __global__ void k_im2row(const uint8_t* __restrict__ frame, int views, int img, 
   *(u16x8*)(x + frag_off(m, k0, KB)) = v;
 }
 
-__global__ void k_embed_tokens(const bf16* __restrict__ embed, const int* __restrict__ tokens, int tok_stride, int d,
-                               float* __restrict__ x) {
-  const int b = blockIdx.y;
-  const int f = (blockIdx.x * blockDim.x + threadIdx.x) * 4;
-  if (f >= d) return;
-  const bf16* e = embed + (size_t)tokens[b * tok_stride] * d + f;
-  *(float4*)(x + (size_t)b * d + f) = float4{bf2f(e[0]), bf2f(e[1]), bf2f(e[2]), bf2f(e[3])};
+// Decode input row b: x = E[token], plus the folded-norm input bf16(x * gain)
+// (frag layout) and the row's sum of squares (one part).
+__global__ __launch_bounds__(256) void k_embed_tokens(const bf16* __restrict__ embed, const int* __restrict__ tokens,
+                                                      int tok_stride, int d, float* __restrict__ x,
+                                                      const float* __restrict__ gain, bf16* __restrict__ xn, int KB,
+                                                      float* __restrict__ ssq) {
+  __shared__ float red[4];
+  const int b = blockIdx.x;
+  const bf16* e = embed + (size_t)tokens[b * tok_stride] * d;
+  float ss = 0.f;
+  for (int f = threadIdx.x * 4; f < d; f += 1024) {
+    const float4 v = float4{bf2f(e[f]), bf2f(e[f + 1]), bf2f(e[f + 2]), bf2f(e[f + 3])};
+    *(float4*)(x + (size_t)b * d + f) = v;
+    const float4 g = *(const float4*)(gain + f);
+    *(u16x4*)(xn + frag_off(b, f, KB)) = u16x4{f2bf(v.x * g.x), f2bf(v.y * g.y), f2bf(v.z * g.z), f2bf(v.w * g.w)};
+    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+  }
+  for (int o = 32; o > 0; o >>= 1) ss += __shfl_xor(ss, o);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  if (threadIdx.x == 0) ssq[b] = red[0] + red[1] + red[2] + red[3];
 }
 
 // ------------------------------------------------------------------ RMSNorm
@@ -325,9 +339,8 @@ hipError_t launch_rmsnorm(const float* src, const int* idx, int M, int d, const 
 }
 
 hipError_t launch_embed_tokens(const bf16* embed, const int* tokens, int tok_stride, int B, int d, float* x,
-                               hipStream_t s) {
-  dim3 grid((d / 4 + 255) / 256, B);
-  hipLaunchKernelGGL(k_embed_tokens, grid, dim3(256), 0, s, embed, tokens, tok_stride, d, x);
+                               const float* gain, bf16* xn, int KB, float* ssq, hipStream_t s) {
+  hipLaunchKernelGGL(k_embed_tokens, dim3(B), dim3(256), 0, s, embed, tokens, tok_stride, d, x, gain, xn, KB, ssq);
   return hipGetLastError();
 }
 
