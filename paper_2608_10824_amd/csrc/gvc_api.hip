@@ -28,6 +28,7 @@ int32_t fail(int32_t code, const std::string& msg) {
   } while (0)
 
 constexpr size_t kAlign = 256;
+constexpr int kMaxNT = 5;   // token blocks per GEMM workgroup (best of 2..16 on the 7B prompt pass)
 
 struct Bump {
   size_t off = 0;
@@ -208,15 +209,15 @@ struct gvc_ctx {
 namespace {
 
 // Token tiling and k split of one GEMM launch: one workgroup per (pair of
-// weight blocks, tile of up to 16 token blocks); 8 waves split k when there
-// are fewer than 256 such workgroups, else 4.  GVC_FORCE_SPLITS (4 or 8)
-// overrides the wave count.
+// weight blocks, tile of at most kMaxNT blocks of 16 token rows).  Its waves
+// split the k range: 8 for long k ranges with few pairs, else 4 (measured on
+// the 7B shapes: more waves per workgroup lower the streaming rate).
+// GVC_FORCE_SPLITS (4 or 8) overrides the wave count (testing).
 void tile_gemm(GemmArgs& a, int M, int force_splits) {
   a.M = M;
   a.mblocks = (M + 15) / 16;
-  a.mtiles = (a.mblocks + 15) / 16;
-  const int wgs = a.n_pairs * a.mtiles;
-  int KW = wgs < 256 ? 8 : 4;
+  a.mtiles = (a.mblocks + kMaxNT - 1) / kMaxNT;
+  int KW = (a.n_pairs < 256 && a.KB > 200) ? 8 : 4;
   if (force_splits == 4 || force_splits == 8) KW = force_splits;
   a.splits = KW;
   a.kb_per_split = (a.KB + KW - 1) / KW;

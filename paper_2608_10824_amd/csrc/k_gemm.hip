@@ -41,6 +41,8 @@ __device__ __forceinline__ void map_pair(const GemmArgs& a, int pair, int& mat_a
   }
 }
 
+__device__ __forceinline__ bf16x8 wload(const bf16x8* p) { return *p; }
+
 __device__ __forceinline__ float silu_f(float g) { return g / (1.0f + __expf(-g)); }
 
 // Epilogue of one lane: 4 consecutive output features of block A and of
@@ -215,9 +217,10 @@ __global__ __launch_bounds__(KW * 64) void k_gemm_ks(const GemmArgs a) {
   const bf16x8* xg[NT];
 #pragma unroll
   for (int t = 0; t < NT; ++t) xg[t] = a.x + (size_t)min(mb0 + t, a.mblocks - 1) * a.KB * 64 + lane;
+  // this wave's contiguous share of the k range
+  constexpr int kst = 1;
   const int kb0 = min(a.KB, wave * a.kb_per_split);
-  const int kb1 = min(a.KB, kb0 + a.kb_per_split);
-  const int nsteps = kb1 - kb0;
+  const int nsteps = min(a.KB, kb0 + a.kb_per_split) - kb0;
   const int nchunks = nsteps / PF;
 
   floatx4 acc_a[NT], acc_b[NT];
@@ -225,13 +228,14 @@ __global__ __launch_bounds__(KW * 64) void k_gemm_ks(const GemmArgs a) {
   for (int t = 0; t < NT; ++t) { acc_a[t] = floatx4{0, 0, 0, 0}; acc_b[t] = floatx4{0, 0, 0, 0}; }
   bf16x8 a0[PF], b0[PF], x0[PF][NT], a1[PF], b1[PF], x1[PF][NT];
   auto load = [&](bf16x8 (&A)[PF], bf16x8 (&Bv)[PF], bf16x8 (&X)[PF][NT], int c) {
-    const size_t kb = (size_t)(kb0 + min(c, nchunks - 1) * PF) * 64;
+    const size_t kb = (size_t)(kb0 + min(c, nchunks - 1) * PF * kst) * 64;
 #pragma unroll
     for (int p = 0; p < PF; ++p) {
-      A[p] = wa[kb + p * 64];
-      Bv[p] = wb[kb + p * 64];
+      const size_t o = kb + (size_t)p * kst * 64;
+      A[p] = wload(wa + o);
+      Bv[p] = wload(wb + o);
 #pragma unroll
-      for (int t = 0; t < NT; ++t) X[p][t] = xg[t][kb + p * 64];
+      for (int t = 0; t < NT; ++t) X[p][t] = xg[t][o];
     }
   };
   auto compute = [&](const bf16x8 (&A)[PF], const bf16x8 (&Bv)[PF], const bf16x8 (&X)[PF][NT]) {
@@ -255,7 +259,7 @@ __global__ __launch_bounds__(KW * 64) void k_gemm_ks(const GemmArgs a) {
     if (c < nchunks) compute(a0, b0, x0);
   }
   for (int s = nchunks * PF; s < nsteps; ++s) {   // ragged k tail
-    const size_t kb = (size_t)(kb0 + s) * 64;
+    const size_t kb = (size_t)(kb0 + s * kst) * 64;
     const bf16x8 wva = wa[kb], wvb = wb[kb];
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
@@ -325,17 +329,6 @@ static hipError_t launch_epi(const GemmArgs& a, int NT, hipStream_t s) {
     case 3: return launch_nt<EPI, 3>(a, s);
     case 4: return launch_nt<EPI, 4>(a, s);
     case 5: return launch_nt<EPI, 5>(a, s);
-    case 6: return launch_nt<EPI, 6>(a, s);
-    case 7: return launch_nt<EPI, 7>(a, s);
-    case 8: return launch_nt<EPI, 8>(a, s);
-    case 9: return launch_nt<EPI, 9>(a, s);
-    case 10: return launch_nt<EPI, 10>(a, s);
-    case 11: return launch_nt<EPI, 11>(a, s);
-    case 12: return launch_nt<EPI, 12>(a, s);
-    case 13: return launch_nt<EPI, 13>(a, s);
-    case 14: return launch_nt<EPI, 14>(a, s);
-    case 15: return launch_nt<EPI, 15>(a, s);
-    case 16: return launch_nt<EPI, 16>(a, s);
     default: return hipErrorInvalidValue;
   }
 }

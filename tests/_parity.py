@@ -76,3 +76,36 @@ def check_margins(m_g, m_o, logits_g, logits_o, bin_lo, full_vocab=True):
     diff = np.abs(np.asarray(m_g, dtype=np.float64) - np.asarray(m_o))
     assert (diff <= bound).all(), "margin error %s exceeds bound %s" % (diff, bound)
     return bound
+
+
+# ---------------------------------------------------------------- 7B helpers
+def layer_w64(w_dev, l):
+    """float64 CPU copy of layer l of device weights (synth layout)."""
+    return {k: v.float().cpu().numpy().astype(np.float64) for k, v in w_dev["layers"][l].items()}
+
+
+def glob_w64(w_dev):
+    return {k: w_dev[k].float().cpu().numpy().astype(np.float64) for k in ("embed", "lm_head", "final_norm")}
+
+
+def state64(sess, item, layer, b, P):
+    """One episode's state item as float64: H [P][d], K/V [kv][H][dh]."""
+    from paper_2608_10824_amd import gvc
+    if item == gvc.STATE_H:
+        return sess.read(item, layer)[b].double().cpu().numpy()
+    if item == gvc.STATE_K:
+        return sess.read(item, layer)[b].double().cpu().numpy().transpose(1, 0, 2)[:P]
+    return sess.read(item, layer)[b].double().cpu().numpy().transpose(2, 0, 1)[:P]
+
+
+def check_layer_sampled(cfg, wl, h_in, h_out, K, V, sample_pos):
+    """Recompute one layer for the sampled rows with the oracle from the GPU's
+    own inputs (h_in = GPU H[l], K/V = GPU cache of layer l for the other
+    keys) and compare fresh K/V and the layer output.  Returns the errors."""
+    from oracle.llama import layer_rows
+    Ko, Vo = K.copy(), V.copy()
+    out = layer_rows(wl, h_in, list(sample_pos), list(sample_pos), Ko, Vo, cfg.n_heads, cfg.rms_eps,
+                     cfg.rope_theta)
+    sp = list(sample_pos)
+    errs = {"k": rel_err(K[sp], Ko[sp]), "v": rel_err(V[sp], Vo[sp]), "out": rel_err(h_out[sp], out)}
+    return errs

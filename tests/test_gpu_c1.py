@@ -1,6 +1,8 @@
-"""Parity of the HIP path with the oracle on the tiny config (2 layers, d=256,
-64 patches + 8 text tokens, FFN 688 with a ragged k-tail).  Every call goes
-through the C ABI."""
+"""Parity of the HIP path with the oracle, every element, on the tiny config
+(2 layers, d=256, 4 heads of 64, FFN 688) and on a mid-size config (d=2048,
+16 heads of 128, FFN 5504: several pipelined k chunks per wave plus a ragged
+k tail), both with 64 patches + 8 text tokens (72 rows: five 16-row token
+blocks, the last one partial).  Every call goes through the C ABI."""
 import numpy as np
 import pytest
 import torch
@@ -12,11 +14,11 @@ from tests._parity import TOL, rel_err, to_dev, gpu_k, gpu_v, check_tokens, chec
 pytestmark = pytest.mark.gpu
 
 
-@pytest.fixture(scope="module")
-def c1():
+@pytest.fixture(scope="module", params=["C1", "MID"])
+def c1(request):
     from paper_2608_10824_amd.session import Session
     from paper_2608_10824_amd import gvc
-    cfg = synth.config_c1()
+    cfg = synth.config_c1() if request.param == "C1" else synth.config_mid()
     w = synth.model_weights(cfg)
     si = synth.step_inputs(cfg, 45)
     dev = torch.device("cuda:0")
