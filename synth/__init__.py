@@ -14,9 +14,10 @@ x ^= x>>16, all mod 2^32.  It is evaluated in int64 torch arithmetic with the
 32x32-bit products split into 16-bit halves so nothing overflows; integer
 arithmetic makes CPU and GPU results identical.
 
-Weights are uniform on [-a, a) with a a power of two: a 24-bit hash value k
-maps to (k - 2^23) * a / 2^23, exact in fp32, then rounded to bf16 with
-round-to-nearest-even (torch's fp32->bf16 cast).
+Weights are uniform on [-a, a) with a = 2^s: a 24-bit hash value k maps to
+(k - 2^23) * 2^(s-23) in one IEEE fp32 multiply (exact for integer s), then
+rounds to bf16 with round-to-nearest-even (torch's fp32->bf16 cast); the
+bits are the same on every device.
 """
 from .hashgen import lowbias32, hash_u32, uniform_f32, uniform_bf16, uniform_u8
 from .configs import VLAConfig, config_c1, config_mid, config_c2, config_c3, config_c4, config_c5, ALL_CONFIGS
