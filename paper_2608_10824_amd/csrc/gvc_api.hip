@@ -58,7 +58,7 @@ struct Plan {
   size_t layer_kv_elems;
   // workspace
   size_t rows_off, counts_off, epc_off, epo_off, stats_off, x_off, q_off, o_off, r_off, act_off, xdec_off, xf_off,
-      ssq_a_off, ssq_f_off,
+      ssq_a_off, ssq_f_off, qraw_off, kraw_off,
       logits_off, rope_off, decrows_off, headrows_off, tokens_off, gate_m_off, gate_f_off,
       ws_bytes;
 };
@@ -152,8 +152,10 @@ int32_t make_plan(const gvc_desc* dsc, Plan& p) {
   p.act_off = k.take((size_t)p.Mp * p.KBf * 32 * 2);
   p.xdec_off = k.take((size_t)p.B * d.d_model * 4);
   p.xf_off = k.take((size_t)((p.B + 15) / 16 * 16) * p.KBd * 32 * 2);
-  p.ssq_a_off = k.take((size_t)p.B * (d.d_model / 32) * 4);
-  p.ssq_f_off = k.take((size_t)p.B * (d.d_model / 32) * 4);
+  p.qraw_off = k.take((size_t)p.B * d.d_model * 4);
+  p.kraw_off = k.take((size_t)p.B * d.d_model * 4);
+  p.ssq_a_off = k.take((size_t)p.B * (d.d_model / 16) * 4);
+  p.ssq_f_off = k.take((size_t)p.B * (d.d_model / 16) * 4);
   p.logits_off = k.take((size_t)p.B * p.V * 4);
   p.rope_off = k.take((size_t)p.kv_pad * (dh / 2) * 8);
   p.decrows_off = k.take((size_t)p.D * 3 * p.B * 4);
@@ -254,8 +256,8 @@ GemmArgs base_args(const gvc_ctx* c) {
 int32_t run_gemm(gvc_ctx* c, GemmArgs& a, int epi, int M, int cls) {
   if (M <= 0) return GVC_OK;
   tile_gemm(a, M, c->force_splits);
-  // the folded RMSNorm reads at most 8 partial sums per lane, 4 lanes per wave per row
-  if (a.e.ssq_in && (a.mblocks > 1 || a.e.ssq_parts > 8 * 4 * a.splits))
+  // the folded RMSNorm reads at most 16 partial sums per lane, 4 lanes per wave per row
+  if (a.e.ssq_in && (a.mblocks > 1 || a.e.ssq_parts > 16 * 4 * a.splits))
     return fail(GVC_EINVAL, "folded norm needs one token block and at most 32 parts per wave");
   ProfScope ps(c, cls);
   HIP_TRY(launch_gemm(a, epi, nt_of(a), c->stream));
@@ -265,7 +267,7 @@ int32_t run_gemm(gvc_ctx* c, GemmArgs& a, int epi, int M, int cls) {
 // One decoder layer over M rows: `src` holds the layer input rows (mapped by
 // rows.idx when src_mapped), `dst` receives the outputs (same mapping rule).
 int32_t run_layer(gvc_ctx* c, int l, const RowMap& rows, int M, float* src, float* dst, bool mapped,
-                  bool decode, int n_keys, int max_tiles, const int* epc, const int* epo) {
+                  int max_tiles, const int* epc, const int* epo) {
   const Plan& p = c->p;
   const float* gains = c->W<float>(p.gains_off) + (size_t)l * 2 * p.d.d_model;
   bf16* X = c->K<bf16>(p.x_off);
@@ -273,7 +275,7 @@ int32_t run_layer(gvc_ctx* c, int l, const RowMap& rows, int M, float* src, floa
   bf16* O = c->K<bf16>(p.o_off);
   float* R = c->K<float>(p.r_off);
   bf16* A = c->K<bf16>(p.act_off);
-  const int k0 = decode ? GVC_K_DECODE_QKV : GVC_K_PREFILL_QKV;   // class of this layer's QKV launch
+  const int k0 = GVC_K_PREFILL_QKV;   // class of this layer's QKV launch; the others follow in order
   {
     ProfScope ps(c, GVC_K_NORM);
     HIP_TRY(launch_rmsnorm(src, mapped ? rows.idx : nullptr, M, p.d.d_model, gains, p.d.rms_eps, X, p.KBd, c->stream));
@@ -290,11 +292,8 @@ int32_t run_layer(gvc_ctx* c, int l, const RowMap& rows, int M, float* src, floa
   }
   {
     ProfScope ps(c, k0 + 1);
-    if (decode)
-      HIP_TRY(launch_attn_decode(Q, c->Kc(l), c->Vc(l), p.B, p.H, p.dh, p.kv_pad, n_keys, O, p.KBd, c->stream));
-    else
-      HIP_TRY(launch_attn_prefill(Q, c->Kc(l), c->Vc(l), rows.pos, epc, epo, p.B, p.H, p.dh, p.kv_pad, max_tiles, O,
-                                  p.KBd, c->stream));
+    HIP_TRY(launch_attn_prefill(Q, c->Kc(l), c->Vc(l), rows.pos, epc, epo, p.B, p.H, p.dh, p.kv_pad, max_tiles, O,
+                                p.KBd, c->stream));
   }
   {
     GemmArgs a = base_args(c);
@@ -344,33 +343,36 @@ int32_t run_layer_decode(gvc_ctx* c, int l, const RowMap& rows, int n_keys, int 
   const float* next_gain = l + 1 < p.L ? gains + 2 * dm : c->W<float>(p.final_gain_off);
   bf16* X = c->K<bf16>(p.x_off);
   bf16* XF = c->K<bf16>(p.xf_off);
-  bf16* Q = c->K<bf16>(p.q_off);
   bf16* O = c->K<bf16>(p.o_off);
   float* R = c->K<float>(p.r_off);
   bf16* A = c->K<bf16>(p.act_off);
   float* xdec = c->K<float>(p.xdec_off);
   float* ssq_a = c->K<float>(p.ssq_a_off);
   float* ssq_f = c->K<float>(p.ssq_f_off);
-  const int parts_d = dm / 32;
+  const int parts_d = dm / 16;   // one partial sum of squares per 16-row block of the producing GEMM
+  float* qraw = c->K<float>(p.qraw_off);
+  float* kraw = c->K<float>(p.kraw_off);
   {
+    // q and k leave un-rotated in fp32; the decode attention applies RoPE
     GemmArgs a = base_args(c);
     a.w[0] = c->packed(p.wq[l]); a.w[1] = c->packed(p.wk[l]); a.w[2] = c->packed(p.wv[l]);
     a.wblk[0] = a.wblk[1] = a.wblk[2] = p.wq[l].Nblk;
-    a.map = MAP_QKV; a.n_pairs = 3 * p.wq[l].Nblk / 2; a.n_out = dm; a.KB = p.KBd;
+    a.map = MAP_QKV_SINGLE; a.n_pairs = 3 * p.wq[l].Nblk; a.n_out = dm; a.KB = p.KBd;
     a.x = reinterpret_cast<const bf16x8*>(X);
-    a.e.rows = rows; a.e.q = Q; a.e.kc = c->Kc(l); a.e.vc = c->Vc(l);
+    a.e.rows = rows; a.e.qraw = qraw; a.e.kraw = kraw; a.e.vc = c->Vc(l);
     a.e.ssq_in = ssq_a; a.e.ssq_parts = ssq_parts_in; a.e.norm_eps = p.d.rms_eps; a.e.norm_dim = dm;
-    int32_t r = run_gemm(c, a, EPI_QKV, B, GVC_K_DECODE_QKV);
+    int32_t r = run_gemm(c, a, EPI_QKV_RAW, B, GVC_K_DECODE_QKV);
     if (r) return r;
   }
   {
     ProfScope ps(c, GVC_K_DECODE_ATTN);
-    HIP_TRY(launch_attn_decode(Q, c->Kc(l), c->Vc(l), B, p.H, p.dh, p.kv_pad, n_keys, O, p.KBd, c->stream));
+    HIP_TRY(launch_attn_decode(qraw, kraw, c->Kc(l), c->Vc(l), c->K<float2>(p.rope_off), B, p.H, p.dh, p.kv_pad,
+                               n_keys - 1, O, p.KBd, c->stream));
   }
   {
     GemmArgs a = base_args(c);
     a.w[0] = c->packed(p.wo[l]); a.wblk[0] = p.wo[l].Nblk;
-    a.map = MAP_PLAIN; a.n_pairs = (p.wo[l].Nblk + 1) / 2; a.n_out = dm; a.KB = p.KBd;
+    a.map = MAP_SINGLE; a.n_pairs = p.wo[l].Nblk; a.n_out = dm; a.KB = p.KBd;
     a.x = reinterpret_cast<const bf16x8*>(O);
     a.e.rows = rows; a.e.resid = xdec; a.e.out = R;
     a.e.xn = XF; a.e.xn_gain = gains + dm; a.e.ssq_out = ssq_f; a.e.xn_kb = p.KBd; a.e.ssq_out_parts = parts_d;
@@ -391,7 +393,7 @@ int32_t run_layer_decode(gvc_ctx* c, int l, const RowMap& rows, int n_keys, int 
   {
     GemmArgs a = base_args(c);
     a.w[0] = c->packed(p.wd[l]); a.wblk[0] = p.wd[l].Nblk;
-    a.map = MAP_PLAIN; a.n_pairs = (p.wd[l].Nblk + 1) / 2; a.n_out = dm; a.KB = p.KBf;
+    a.map = MAP_SINGLE; a.n_pairs = p.wd[l].Nblk; a.n_out = dm; a.KB = p.KBf;
     a.x = reinterpret_cast<const bf16x8*>(A);
     a.e.rows = rows; a.e.resid = R; a.e.out = xdec;
     a.e.xn = X; a.e.xn_gain = next_gain; a.e.ssq_out = ssq_a; a.e.xn_kb = p.KBd; a.e.ssq_out_parts = parts_d;
@@ -572,8 +574,8 @@ int32_t gvc_step_prefill(gvc_ctx* c, const uint8_t* frame_t, const int32_t* text
   }
   const int max_tiles = (p.P + 15) / 16;
   for (int l = 0; l < p.L; ++l) {
-    int32_t r = run_layer(c, l, c->rows(l), c->counts[l], c->H(l), c->H(l + 1), true, false, 0, max_tiles,
-                          epc + l * p.B, epo + l * p.B);
+    int32_t r = run_layer(c, l, c->rows(l), c->counts[l], c->H(l), c->H(l + 1), true, max_tiles, epc + l * p.B,
+                          epo + l * p.B);
     if (r) return r;
   }
   int32_t r = run_head(c, c->head_rows(), c->H(p.L), p.B * p.head_rows, c->S<float>(p.head_logits_off),
@@ -612,7 +614,7 @@ int32_t gvc_decode_actions(gvc_ctx* c, int32_t* tokens_out, float* margins_out, 
       const RowMap rows = c->dec_rows(j);
       const int pos = p.P + j - 1;
       for (int l = 0; l < p.L; ++l) {
-        int32_t r = run_layer_decode(c, l, rows, pos + 1, l == 0 ? 1 : p.d.d_model / 32);
+        int32_t r = run_layer_decode(c, l, rows, pos + 1, l == 0 ? 1 : p.d.d_model / 16);
         if (r) return r;
       }
       {
@@ -622,7 +624,7 @@ int32_t gvc_decode_actions(gvc_ctx* c, int32_t* tokens_out, float* margins_out, 
         a.map = MAP_PLAIN; a.n_pairs = (p.lm.Nblk + 1) / 2; a.n_out = p.V; a.KB = p.KBd;
         a.x = c->K<bf16x8>(p.x_off);
         a.e.rows = rows; a.e.store = lg; a.e.ld_store = p.V;
-        a.e.ssq_in = c->K<float>(p.ssq_a_off); a.e.ssq_parts = p.d.d_model / 32;
+        a.e.ssq_in = c->K<float>(p.ssq_a_off); a.e.ssq_parts = p.d.d_model / 16;
         a.e.norm_eps = p.d.rms_eps; a.e.norm_dim = p.d.d_model;
         int32_t r = run_gemm(c, a, EPI_STORE, p.B, GVC_K_DECODE_HEAD);
         if (r) return r;

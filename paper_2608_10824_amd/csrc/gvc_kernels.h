@@ -45,8 +45,10 @@ __device__ __forceinline__ size_t frag_off(int m, int k, int KB) {
 }
 
 // ------------------------------------------------------------------ GEMM
-enum { MAP_PLAIN = 0, MAP_QKV = 1, MAP_GU = 2 };
-enum { EPI_QKV = 0, EPI_RESID = 1, EPI_SILU = 2, EPI_STORE = 3, EPI_EMBED = 4 };
+// Work units of a GEMM launch.  Pair maps give a workgroup two 16-row weight
+// blocks whose epilogue partners share lanes; single maps give it one block.
+enum { MAP_PLAIN = 0, MAP_QKV = 1, MAP_GU = 2, MAP_SINGLE = 3, MAP_QKV_SINGLE = 4 };
+enum { EPI_QKV = 0, EPI_RESID = 1, EPI_SILU = 2, EPI_STORE = 3, EPI_EMBED = 4, EPI_QKV_RAW = 5 };
 
 struct RowMap {
   const int* idx;   // row index into the residual / output arrays
@@ -56,7 +58,8 @@ struct RowMap {
 
 struct EpiArgs {
   RowMap rows;
-  // EPI_QKV
+  // EPI_QKV (and EPI_QKV_RAW: q, k before RoPE as fp32 [M][d] in qraw, kraw)
+  float* qraw; float* kraw;
   bf16* q;            // [Mp][d] row-major, after RoPE
   bf16* kc;           // this layer's K cache
   bf16* vc;           // this layer's V cache (transposed)
@@ -86,7 +89,7 @@ struct GemmArgs {
   const bf16x8* w[3];   // packed matrices (fragment units)
   int wblk[3];          // 16-row blocks per matrix
   int map;
-  int n_pairs;          // pairs of 16-row blocks (one pair per wave)
+  int n_pairs;          // work units (pairs, or single blocks for the single maps)
   int n_out;            // output features of the (first) matrix, for MAP_PLAIN
   int KB;               // k-fragments (K padded / 32)
   int splits, kb_per_split;   // waves per workgroup splitting k, k-steps per wave
@@ -120,8 +123,8 @@ hipError_t launch_gemm(const GemmArgs& a, int epi, int NT, hipStream_t s);
 hipError_t launch_attn_prefill(const bf16* q, const bf16* kc, const bf16* vc, const int* rows_pos,
                                const int* ep_counts, const int* ep_offsets, int B, int H, int head_dim,
                                int kv_pad, int max_tiles, bf16* o, int KB, hipStream_t s);
-hipError_t launch_attn_decode(const bf16* q, const bf16* kc, const bf16* vc, int B, int H, int head_dim,
-                              int kv_pad, int n_keys, bf16* o, int KB, hipStream_t s);
+hipError_t launch_attn_decode(const float* qraw, const float* kraw, bf16* kc, const bf16* vc, const float2* rope,
+                              int B, int H, int head_dim, int kv_pad, int pos, bf16* o, int KB, hipStream_t s);
 hipError_t launch_embed_tokens(const bf16* embed, const int* tokens, int tok_stride, int B, int d,
                                float* x, const float* gain, bf16* xn, int KB, float* ssq, hipStream_t s);
 hipError_t launch_logits_reduce(const float* logits, int rows, int V, int bin_lo, int full_vocab,

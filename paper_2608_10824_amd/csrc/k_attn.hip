@@ -116,48 +116,91 @@ __global__ __launch_bounds__(64) void k_attn_prefill(const bf16* __restrict__ q,
   }
 }
 
-// One workgroup per (head, episode): a single query at position n_keys-1.
-// Scores: DH/8 lanes per key, each lane a 16-byte run of dims, so one wave
-// instruction reads whole key rows contiguously; partial dots are summed
-// across the lane group.  Values: the cache is dim-major, so a lane reads
-// 8 consecutive keys of one dim and a wave instruction reads 4 dims x 16
-// chunks = 4 contiguous 256-byte runs.  Both phases issue a batch of loads
-// (clamped addresses, results masked) before consuming any of them, so the
-// kernel pays the memory latency a few times rather than once per key group.
-template <int DH>
-__global__ __launch_bounds__(256) void k_attn_decode(const bf16* __restrict__ q, const bf16* __restrict__ kc,
-                                                     const bf16* __restrict__ vc, int H, int kv_pad, int n_keys,
+// Single-query attention of a decode pass at position pos.  One workgroup
+// per (head, episode, value slice): q and the new key arrive un-rotated in
+// fp32; every workgroup rotates them (RoPE, pairing dim i with i + DH/2), the
+// first slice also stores the rotated key (bf16) into the cache, and each
+// computes all pos + 1 scores but only its DH/NQ value dimensions, so a head
+// spreads over NQ workgroups without any cross-workgroup combine.
+// The first batch of key rows and the value runs are loaded before anything
+// else, so their latency overlaps the rotation; longer sequences loop.
+// Scores: DH/8 lanes per key, each a 16-byte run of dims (a wave instruction
+// reads whole key rows); the new key comes from LDS, never from the cache
+// slot being written.  Values: the cache is dim-major, so a lane reads 8
+// consecutive keys of one dim.
+template <int DH, int NQ>
+__global__ __launch_bounds__(512) void k_attn_decode(const float* __restrict__ qraw, const float* __restrict__ kraw,
+                                                     bf16* __restrict__ kc, const bf16* __restrict__ vc,
+                                                     const float2* __restrict__ rope, int H, int kv_pad, int pos,
                                                      bf16* __restrict__ o, int KB) {
   extern __shared__ float sc[];          // [kv_pad] scores, then probabilities
-  __shared__ float red[8];
+  __shared__ float qs[DH], kn[DH];
+  __shared__ float red[16];
+  constexpr int NT = 512;
   constexpr int LPK = DH / 8;            // lanes per key
-  constexpr int KPI = 256 / LPK;         // keys per load round
-  constexpr int U = 8;                   // load rounds per batch
-  constexpr int ND = DH / 16;            // dims per thread in the value phase
-  constexpr int UC = 3;                  // 8-key chunks per lane per value batch
-  const int h = blockIdx.x, b = blockIdx.y;
-  const int d = H * DH;
+  constexpr int KPI = NT / LPK;          // keys per load round
+  constexpr int U = 10;                  // load rounds per batch
+  constexpr int DQ = DH / NQ;            // value dims of this workgroup
+  constexpr int DG = NT / 16;            // dim groups
+  constexpr int ND = (DQ + DG - 1) / DG; // dims per thread in the value phase
+  constexpr int UC = 2;                  // 8-key chunks per lane per value batch
+  const int h = blockIdx.x, b = blockIdx.y, qd = blockIdx.z;
+  const int d = H * DH, half = DH / 2;
   const int tid = threadIdx.x;
+  const int n_keys = pos + 1;
+  const int nchunk = (n_keys + 7) / 8;
+  bf16* kbase = kc + (size_t)(b * H + h) * kv_pad * DH;
   const int sub = tid % LPK, kg = tid / LPK;
-  float qv[8];
-  {
-    const u16x8 qq = *(const u16x8*)(q + (size_t)b * d + h * DH + sub * 8);
+  const bf16* ksub = kbase + sub * 8;
+  const int last_cached = max(pos - 1, 0);
+  // value-phase mapping: lane16 walks 8-key chunks, DG dim groups
+  const int l16 = tid & 15, dg = tid >> 4;
+  const bf16* vb = vc + (size_t)(b * H + h) * DH * kv_pad + (size_t)(qd * DQ) * kv_pad;
+  u16x8 kv[U], vv[ND][UC];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) qv[i] = bf2f(qq[i]);
+  for (int u = 0; u < U; ++u) kv[u] = *(const u16x8*)(ksub + (size_t)min(u * KPI + kg, last_cached) * DH);
+#pragma unroll
+  for (int i = 0; i < ND; ++i)
+#pragma unroll
+    for (int u = 0; u < UC; ++u)
+      vv[i][u] = *(const u16x8*)(vb + (size_t)min(dg + DG * i, DQ - 1) * kv_pad + min(16 * u + l16, nchunk - 1) * 8);
+  if (tid < half) {
+    const float2 cs = rope[(size_t)pos * half + tid];
+    const float* qr = qraw + (size_t)b * d + h * DH;
+    const float* kr = kraw + (size_t)b * d + h * DH;
+    const float q0 = qr[tid], q1 = qr[tid + half], k0 = kr[tid], k1 = kr[tid + half];
+    qs[tid] = q0 * cs.x - q1 * cs.y;
+    qs[tid + half] = q1 * cs.x + q0 * cs.y;
+    const bf16 ka = f2bf(k0 * cs.x - k1 * cs.y), kb = f2bf(k1 * cs.x + k0 * cs.y);
+    kn[tid] = bf2f(ka);
+    kn[tid + half] = bf2f(kb);
+    if (qd == 0) {
+      kbase[(size_t)pos * DH + tid] = ka;
+      kbase[(size_t)pos * DH + tid + half] = kb;
+    }
   }
-  const bf16* kbase = kc + (size_t)(b * H + h) * kv_pad * DH + sub * 8;
+  __syncthreads();
+  float qv[8], kv_new[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) { qv[i] = qs[sub * 8 + i]; kv_new[i] = kn[sub * 8 + i]; }
   const float scale = 1.0f / sqrtf((float)DH);
   float mx = -INFINITY;
   for (int j0 = 0; j0 < n_keys; j0 += KPI * U) {
-    u16x8 kv[U];
+    if (j0 > 0) {
 #pragma unroll
-    for (int u = 0; u < U; ++u) kv[u] = *(const u16x8*)(kbase + (size_t)min(j0 + u * KPI + kg, n_keys - 1) * DH);
+      for (int u = 0; u < U; ++u) kv[u] = *(const u16x8*)(ksub + (size_t)min(j0 + u * KPI + kg, last_cached) * DH);
+    }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int j = j0 + u * KPI + kg;
       float s = 0.f;
+      if (j == pos) {
 #pragma unroll
-      for (int i = 0; i < 8; ++i) s += qv[i] * bf2f(kv[u][i]);
+        for (int i = 0; i < 8; ++i) s += qv[i] * kv_new[i];
+      } else {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) s += qv[i] * bf2f(kv[u][i]);
+      }
 #pragma unroll
       for (int x = LPK / 2; x > 0; x >>= 1) s += __shfl_xor(s, x);
       s *= scale;
@@ -170,32 +213,36 @@ __global__ __launch_bounds__(256) void k_attn_decode(const bf16* __restrict__ q,
   for (int x = 32; x > 0; x >>= 1) mx = fmaxf(mx, __shfl_xor(mx, x));
   if ((tid & 63) == 0) red[tid >> 6] = mx;
   __syncthreads();
-  mx = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+  mx = red[0];
+#pragma unroll
+  for (int w = 1; w < NT / 64; ++w) mx = fmaxf(mx, red[w]);
   float sm = 0.f;
-  for (int j = tid; j < n_keys; j += 256) {
+  for (int j = tid; j < n_keys; j += NT) {
     const float p = __expf(sc[j] - mx);
     sc[j] = p;
     sm += p;
   }
   for (int x = 32; x > 0; x >>= 1) sm += __shfl_xor(sm, x);
-  if ((tid & 63) == 0) red[4 + (tid >> 6)] = sm;
-  for (int j = n_keys + tid; j < (n_keys + 7) / 8 * 8; j += 256) sc[j] = 0.f;   // pad the last 8-key chunk
   __syncthreads();
-  const float inv = 1.0f / (red[4] + red[5] + red[6] + red[7]);
-  // o[dim] = sum_j p_j V^T[dim][j]: lane16 walks 8-key chunks, 16 dim groups
-  const int l16 = tid & 15, dg = tid >> 4;
-  const int nchunk = (n_keys + 7) / 8;
-  const bf16* vb = vc + (size_t)(b * H + h) * DH * kv_pad + (size_t)dg * kv_pad;
+  if ((tid & 63) == 0) red[8 + (tid >> 6)] = sm;
+  for (int j = n_keys + tid; j < nchunk * 8; j += NT) sc[j] = 0.f;   // pad the last 8-key chunk
+  __syncthreads();
+  float tot = 0.f;
+#pragma unroll
+  for (int w = 0; w < NT / 64; ++w) tot += red[8 + w];
+  const float inv = 1.0f / tot;
   float acc[ND];
 #pragma unroll
   for (int i = 0; i < ND; ++i) acc[i] = 0.f;
   for (int c0 = 0; c0 < nchunk; c0 += 16 * UC) {
-    u16x8 vv[ND][UC];
+    if (c0 > 0) {
 #pragma unroll
-    for (int i = 0; i < ND; ++i)
+      for (int i = 0; i < ND; ++i)
 #pragma unroll
-      for (int u = 0; u < UC; ++u)
-        vv[i][u] = *(const u16x8*)(vb + (size_t)(16 * i) * kv_pad + min(c0 + 16 * u + l16, nchunk - 1) * 8);
+        for (int u = 0; u < UC; ++u)
+          vv[i][u] = *(const u16x8*)(vb + (size_t)min(dg + DG * i, DQ - 1) * kv_pad +
+                                     min(c0 + 16 * u + l16, nchunk - 1) * 8);
+    }
 #pragma unroll
     for (int u = 0; u < UC; ++u) {
       const int c = c0 + 16 * u + l16;
@@ -214,7 +261,8 @@ __global__ __launch_bounds__(256) void k_attn_decode(const bf16* __restrict__ q,
     float t = acc[i];
 #pragma unroll
     for (int x = 8; x > 0; x >>= 1) t += __shfl_xor(t, x);
-    if (l16 == 0) o[frag_off(b, h * DH + dg + 16 * i, KB)] = f2bf(t * inv);
+    const int dim = dg + DG * i;
+    if (l16 == 0 && dim < DQ) o[frag_off(b, h * DH + qd * DQ + dim, KB)] = f2bf(t * inv);
   }
 }
 
@@ -233,14 +281,15 @@ hipError_t launch_attn_prefill(const bf16* q, const bf16* kc, const bf16* vc, co
   return hipGetLastError();
 }
 
-hipError_t launch_attn_decode(const bf16* q, const bf16* kc, const bf16* vc, int B, int H, int head_dim, int kv_pad,
-                              int n_keys, bf16* o, int KB, hipStream_t s) {
-  dim3 grid(H, B);
+hipError_t launch_attn_decode(const float* qraw, const float* kraw, bf16* kc, const bf16* vc, const float2* rope,
+                              int B, int H, int head_dim, int kv_pad, int pos, bf16* o, int KB, hipStream_t s) {
   const size_t shm = (size_t)kv_pad * sizeof(float);
   if (head_dim == 128)
-    hipLaunchKernelGGL(k_attn_decode<128>, grid, dim3(256), shm, s, q, kc, vc, H, kv_pad, n_keys, o, KB);
+    hipLaunchKernelGGL((k_attn_decode<128, 4>), dim3(H, B, 4), dim3(512), shm, s, qraw, kraw, kc, vc, rope, H, kv_pad,
+                       pos, o, KB);
   else if (head_dim == 64)
-    hipLaunchKernelGGL(k_attn_decode<64>, grid, dim3(256), shm, s, q, kc, vc, H, kv_pad, n_keys, o, KB);
+    hipLaunchKernelGGL((k_attn_decode<64, 4>), dim3(H, B, 4), dim3(512), shm, s, qraw, kraw, kc, vc, rope, H, kv_pad,
+                       pos, o, KB);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();

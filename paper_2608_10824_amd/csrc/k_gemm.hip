@@ -33,6 +33,10 @@ __device__ __forceinline__ void map_pair(const GemmArgs& a, int pair, int& mat_a
     blk_b = blk_a + per_head;
   } else if (a.map == MAP_GU) {
     mat_a = 0; mat_b = 1; blk_a = blk_b = pair;
+  } else if (a.map == MAP_SINGLE) {
+    mat_a = mat_b = 0; blk_a = blk_b = pair; b_ok = false;
+  } else if (a.map == MAP_QKV_SINGLE) {
+    mat_a = mat_b = pair / a.wblk[0]; blk_a = blk_b = pair % a.wblk[0]; b_ok = false;
   } else {
     mat_a = mat_b = 0;
     blk_a = 2 * pair;
@@ -98,6 +102,21 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, int pair, int lane, 
         v[(size_t)(ia + i) * e.kv_pad] = f2bf(ra[i]);
         v[(size_t)(ia + half + i) * e.kv_pad] = f2bf(rb[i]);
       }
+    }
+  } else if constexpr (EPI == EPI_QKV_RAW) {
+    // single block of q, k or v for decode rows: q and k stay fp32 and
+    // un-rotated (the decode attention rotates them), v goes to the cache
+    if (!valid) return;
+    const int f = blk_a * 16 + sub;
+    if (mat_a == 0) {
+      *(float4*)(e.qraw + (size_t)m * e.d + f) = float4{va[0], va[1], va[2], va[3]};
+    } else if (mat_a == 1) {
+      *(float4*)(e.kraw + (size_t)m * e.d + f) = float4{va[0], va[1], va[2], va[3]};
+    } else {
+      const int dh = e.head_dim, head = f / dh, dim = f % dh;
+      bf16* v = e.vc + ((size_t)(e.rows.ep[m] * e.n_heads + head) * dh + dim) * e.kv_pad + e.rows.pos[m];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) v[(size_t)i * e.kv_pad] = f2bf(va[i]);
     }
   } else if constexpr (EPI == EPI_RESID) {
     const int d = e.d;
@@ -182,7 +201,7 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, int pair, int lane, 
 // chunks are in flight; the prefetch of the chunk after the last re-reads
 // the last chunk instead of branching.  Token fragments come straight from
 // the (L2-resident) activations.
-template <int KW, int NT, int PF, int EPI>
+template <int KW, int NT, int PF, int EPI, bool ONE>
 __global__ __launch_bounds__(KW * 64) void k_gemm_ks(const GemmArgs a) {
   __shared__ floatx4 red[KW][2][64];
   __shared__ float ssq_red[KW][16];
@@ -192,7 +211,7 @@ __global__ __launch_bounds__(KW * 64) void k_gemm_ks(const GemmArgs a) {
   // Folded RMSNorm (single token block): lane (row r = lane % 16, chunk
   // wave * 4 + lane / 16) loads up to SQ of the row's partial sums of squares
   // now and adds them after the main loop, so the loads overlap the stream.
-  constexpr int SQ = 8;
+  constexpr int SQ = 16;
   float sq[SQ];
   const bool fold = NT == 1 && a.e.ssq_in != nullptr;
   if (fold) {
@@ -214,9 +233,16 @@ __global__ __launch_bounds__(KW * 64) void k_gemm_ks(const GemmArgs a) {
   const int mb0 = mt * NT;
   // token block t of this tile, clamped to the last existing block (its
   // results for rows >= M are never stored)
+  // Lanes of token rows >= M re-read the last valid row of their block:
+  // those output columns are never stored, and the shared address keeps a
+  // decode launch (M = 1) from fetching 15 padding rows per fragment.
   const bf16x8* xg[NT];
 #pragma unroll
-  for (int t = 0; t < NT; ++t) xg[t] = a.x + (size_t)min(mb0 + t, a.mblocks - 1) * a.KB * 64 + lane;
+  for (int t = 0; t < NT; ++t) {
+    const int mb = min(mb0 + t, a.mblocks - 1);
+    const int xl = (lane & 48) | min(lane & 15, a.M - 1 - mb * 16);
+    xg[t] = a.x + (size_t)mb * a.KB * 64 + xl;
+  }
   // this wave's contiguous share of the k range
   constexpr int kst = 1;
   const int kb0 = min(a.KB, wave * a.kb_per_split);
@@ -233,7 +259,7 @@ __global__ __launch_bounds__(KW * 64) void k_gemm_ks(const GemmArgs a) {
     for (int p = 0; p < PF; ++p) {
       const size_t o = kb + (size_t)p * kst * 64;
       A[p] = wload(wa + o);
-      Bv[p] = wload(wb + o);
+      if constexpr (!ONE) Bv[p] = wload(wb + o);
 #pragma unroll
       for (int t = 0; t < NT; ++t) X[p][t] = xg[t][o];
     }
@@ -244,7 +270,7 @@ __global__ __launch_bounds__(KW * 64) void k_gemm_ks(const GemmArgs a) {
 #pragma unroll
       for (int t = 0; t < NT; ++t) {
         acc_a[t] = mfma16(A[p], X[p][t], acc_a[t]);
-        acc_b[t] = mfma16(Bv[p], X[p][t], acc_b[t]);
+        if constexpr (!ONE) acc_b[t] = mfma16(Bv[p], X[p][t], acc_b[t]);
       }
   };
   if (nchunks > 0) {
@@ -260,12 +286,13 @@ __global__ __launch_bounds__(KW * 64) void k_gemm_ks(const GemmArgs a) {
   }
   for (int s = nchunks * PF; s < nsteps; ++s) {   // ragged k tail
     const size_t kb = (size_t)(kb0 + s * kst) * 64;
-    const bf16x8 wva = wa[kb], wvb = wb[kb];
+    const bf16x8 wva = wa[kb];
+    const bf16x8 wvb = ONE ? wva : wb[kb];
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
       const bf16x8 xv = xg[t][kb];
       acc_a[t] = mfma16(wva, xv, acc_a[t]);
-      acc_b[t] = mfma16(wvb, xv, acc_b[t]);
+      if constexpr (!ONE) acc_b[t] = mfma16(wvb, xv, acc_b[t]);
     }
   }
   if (fold) {
@@ -308,17 +335,28 @@ __global__ __launch_bounds__(KW * 64) void k_gemm_ks(const GemmArgs a) {
   }
 }
 
-template <int EPI, int NT>
-static hipError_t launch_nt(const GemmArgs& a, hipStream_t s) {
+template <int EPI, int NT, bool ONE>
+static hipError_t launch_one(const GemmArgs& a, hipStream_t s) {
   constexpr int PF = gemm_pf(NT);
   const dim3 grid(a.n_pairs, a.mtiles);
   if (a.splits == 8)
-    hipLaunchKernelGGL((k_gemm_ks<8, NT, PF, EPI>), grid, dim3(8 * 64), 0, s, a);
+    hipLaunchKernelGGL((k_gemm_ks<8, NT, PF, EPI, ONE>), grid, dim3(8 * 64), 0, s, a);
   else if (a.splits == 4)
-    hipLaunchKernelGGL((k_gemm_ks<4, NT, PF, EPI>), grid, dim3(4 * 64), 0, s, a);
+    hipLaunchKernelGGL((k_gemm_ks<4, NT, PF, EPI, ONE>), grid, dim3(4 * 64), 0, s, a);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();
+}
+
+template <int EPI, int NT>
+static hipError_t launch_nt(const GemmArgs& a, hipStream_t s) {
+  const bool one = a.map == MAP_SINGLE || a.map == MAP_QKV_SINGLE;
+  if constexpr (EPI == EPI_RESID || EPI == EPI_STORE || EPI == EPI_QKV_RAW) {
+    if (one) return NT == 1 ? launch_one<EPI, 1, true>(a, s) : hipErrorInvalidValue;
+  }
+  if (one) return hipErrorInvalidValue;
+  if constexpr (EPI == EPI_QKV_RAW) return hipErrorInvalidValue;
+  else return launch_one<EPI, NT, false>(a, s);
 }
 
 template <int EPI>
@@ -340,6 +378,7 @@ hipError_t launch_gemm(const GemmArgs& a, int epi, int NT, hipStream_t s) {
     case EPI_SILU: return launch_epi<EPI_SILU>(a, NT, s);
     case EPI_STORE: return launch_epi<EPI_STORE>(a, NT, s);
     case EPI_EMBED: return launch_epi<EPI_EMBED>(a, NT, s);
+    case EPI_QKV_RAW: return launch_epi<EPI_QKV_RAW>(a, NT, s);
     default: return hipErrorInvalidValue;
   }
 }
