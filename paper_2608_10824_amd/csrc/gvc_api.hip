@@ -210,14 +210,17 @@ struct gvc_ctx {
 
 namespace {
 
-// Token tiling and k split of one GEMM launch: one workgroup per (pair of
-// weight blocks, tile of at most kMaxNT blocks of 16 token rows).  Its waves
-// split the k range: 8 for long k ranges with few pairs, else 4 (measured on
-// the 7B shapes: more waves per workgroup lower the streaming rate).
-// GVC_FORCE_SPLITS (4 or 8) overrides the wave count (testing).
+// Token tiling and k split of one GEMM launch: one workgroup per (work
+// unit, tile of at most kMaxNT blocks of 16 token rows); its waves split the
+// k range 4 ways (8 for long k ranges with few units).  Measured on the 7B
+// prompt pass: more concurrent weight streams beat reading the weights once
+// per 160 rows (two token groups sharing a k share were 10-50% slower), so
+// each token tile streams the weights itself.  GVC_FORCE_SPLITS (4 or 8)
+// overrides the wave count (testing).
 void tile_gemm(GemmArgs& a, int M, int force_splits) {
   a.M = M;
   a.mblocks = (M + 15) / 16;
+  a.tgroups = 1;
   a.mtiles = (a.mblocks + kMaxNT - 1) / kMaxNT;
   int KW = (a.n_pairs < 256 && a.KB > 200) ? 8 : 4;
   if (force_splits == 4 || force_splits == 8) KW = force_splits;
@@ -225,7 +228,9 @@ void tile_gemm(GemmArgs& a, int M, int force_splits) {
   a.kb_per_split = (a.KB + KW - 1) / KW;
 }
 
-int nt_of(const GemmArgs& a) { return (a.mblocks + a.mtiles - 1) / a.mtiles; }
+int nt_of(const GemmArgs& a) {
+  return (a.mblocks + a.mtiles * a.tgroups - 1) / (a.mtiles * a.tgroups);
+}
 
 // Start / stop events around a launch of class `cls` when it is profiled.
 struct ProfScope {

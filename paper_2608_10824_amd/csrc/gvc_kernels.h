@@ -92,7 +92,8 @@ struct GemmArgs {
   int n_pairs;          // work units (pairs, or single blocks for the single maps)
   int n_out;            // output features of the (first) matrix, for MAP_PLAIN
   int KB;               // k-fragments (K padded / 32)
-  int splits, kb_per_split;   // waves per workgroup splitting k, k-steps per wave
+  int splits, kb_per_split;   // waves per workgroup (token groups x k shares), k-steps per share
+  int tgroups;                // token groups per workgroup (KT)
   const bf16x8* x;      // frag-layout activations
   int M, mblocks, mtiles;
   EpiArgs e;

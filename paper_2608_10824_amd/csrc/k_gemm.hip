@@ -193,27 +193,38 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, int pair, int lane, 
   }
 }
 
-// One workgroup owns one pair of weight blocks and NT blocks of 16 token
-// rows; its KW waves split the k range and their accumulators are summed
-// through LDS in wave order (deterministic, no cross-workgroup traffic).
-// Each wave streams its share in chunks of PF k-steps, double-buffered in
-// registers with no branch between a chunk's loads and its MFMAs, so two
-// chunks are in flight; the prefetch of the chunk after the last re-reads
-// the last chunk instead of branching.  Token fragments come straight from
-// the (L2-resident) activations.
-template <int KW, int NT, int PF, int EPI, bool ONE>
-__global__ __launch_bounds__(KW * 64) void k_gemm_ks(const GemmArgs a) {
+// One workgroup owns one pair of weight blocks (one block for the single
+// maps) and a tile of KT x NT blocks of 16 token rows.  Its KT * KS waves are
+// KT token groups (NT blocks each) times KS shares of the k range: the waves
+// of one k share read the same weight fragments at the same time, so the
+// weights leave HBM once per workgroup while each wave keeps only NT token
+// blocks in registers.  The k shares are summed through LDS in a fixed order
+// (deterministic, no cross-workgroup traffic).  Each wave streams its share
+// in chunks of PF k-steps, double-buffered in registers with no branch
+// between a chunk's loads and its MFMAs, so two chunks are in flight; the
+// prefetch of the chunk after the last re-reads the last chunk instead of
+// branching.  Token fragments come straight from the (L2-resident)
+// activations.
+template <int KS, int KT, int NT, int PF, int EPI, bool ONE>
+__global__ __launch_bounds__(KS * KT * 64) void k_gemm_ks(const GemmArgs a) {
+  constexpr int KW = KS * KT;
   __shared__ floatx4 red[KW][2][64];
   __shared__ float ssq_red[KW][16];
   __shared__ float rscale[16];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int pair = blockIdx.x, mt = blockIdx.y;
+  const int tg = wave / KS, ks = wave % KS;
+  // XCD-aware order: workgroup ids go round-robin over the 8 XCDs, so the
+  // token tiles of one work unit get ids 8 apart -- same XCD, dispatched
+  // together -- and the later tiles find the unit's weights in that L2.
+  const int grp = blockIdx.x / (8 * a.mtiles), r8 = blockIdx.x % (8 * a.mtiles);
+  const int pair = grp * 8 + (r8 & 7), mt = r8 >> 3;
+  if (pair >= a.n_pairs) return;
   // Folded RMSNorm (single token block): lane (row r = lane % 16, chunk
   // wave * 4 + lane / 16) loads up to SQ of the row's partial sums of squares
   // now and adds them after the main loop, so the loads overlap the stream.
   constexpr int SQ = 16;
   float sq[SQ];
-  const bool fold = NT == 1 && a.e.ssq_in != nullptr;
+  const bool fold = NT == 1 && KT == 1 && a.e.ssq_in != nullptr;
   if (fold) {
     const int r = min(lane & 15, a.M - 1);
     const int nch = KW * 4, ch = wave * 4 + (lane >> 4);
@@ -230,9 +241,7 @@ __global__ __launch_bounds__(KW * 64) void k_gemm_ks(const GemmArgs a) {
   map_pair(a, pair, mat_a, blk_a, mat_b, blk_b, b_ok);
   const bf16x8* wa = a.w[mat_a] + (size_t)blk_a * a.KB * 64 + lane;
   const bf16x8* wb = a.w[mat_b] + (size_t)blk_b * a.KB * 64 + lane;
-  const int mb0 = mt * NT;
-  // token block t of this tile, clamped to the last existing block (its
-  // results for rows >= M are never stored)
+  const int mb0 = (mt * KT + tg) * NT;   // first token block of this wave
   // Lanes of token rows >= M re-read the last valid row of their block:
   // those output columns are never stored, and the shared address keeps a
   // decode launch (M = 1) from fetching 15 padding rows per fragment.
@@ -244,8 +253,7 @@ __global__ __launch_bounds__(KW * 64) void k_gemm_ks(const GemmArgs a) {
     xg[t] = a.x + (size_t)mb * a.KB * 64 + xl;
   }
   // this wave's contiguous share of the k range
-  constexpr int kst = 1;
-  const int kb0 = min(a.KB, wave * a.kb_per_split);
+  const int kb0 = min(a.KB, ks * a.kb_per_split);
   const int nsteps = min(a.KB, kb0 + a.kb_per_split) - kb0;
   const int nchunks = nsteps / PF;
 
@@ -254,12 +262,12 @@ __global__ __launch_bounds__(KW * 64) void k_gemm_ks(const GemmArgs a) {
   for (int t = 0; t < NT; ++t) { acc_a[t] = floatx4{0, 0, 0, 0}; acc_b[t] = floatx4{0, 0, 0, 0}; }
   bf16x8 a0[PF], b0[PF], x0[PF][NT], a1[PF], b1[PF], x1[PF][NT];
   auto load = [&](bf16x8 (&A)[PF], bf16x8 (&Bv)[PF], bf16x8 (&X)[PF][NT], int c) {
-    const size_t kb = (size_t)(kb0 + min(c, nchunks - 1) * PF * kst) * 64;
+    const size_t kb = (size_t)(kb0 + min(c, nchunks - 1) * PF) * 64;
 #pragma unroll
     for (int p = 0; p < PF; ++p) {
-      const size_t o = kb + (size_t)p * kst * 64;
-      A[p] = wload(wa + o);
-      if constexpr (!ONE) Bv[p] = wload(wb + o);
+      const size_t o = kb + (size_t)p * 64;
+      A[p] = wa[o];
+      if constexpr (!ONE) Bv[p] = wb[o];
 #pragma unroll
       for (int t = 0; t < NT; ++t) X[p][t] = xg[t][o];
     }
@@ -285,7 +293,7 @@ __global__ __launch_bounds__(KW * 64) void k_gemm_ks(const GemmArgs a) {
     if (c < nchunks) compute(a0, b0, x0);
   }
   for (int s = nchunks * PF; s < nsteps; ++s) {   // ragged k tail
-    const size_t kb = (size_t)(kb0 + s * kst) * 64;
+    const size_t kb = (size_t)(kb0 + s) * 64;
     const bf16x8 wva = wa[kb];
     const bf16x8 wvb = ONE ? wva : wb[kb];
 #pragma unroll
@@ -310,53 +318,75 @@ __global__ __launch_bounds__(KW * 64) void k_gemm_ks(const GemmArgs a) {
       rscale[lane] = 1.0f / sqrtf(u / (float)a.e.norm_dim + a.e.norm_eps);
     }
   }
-  // Reduce over the KW waves, one token block per round; wave t % KW keeps
-  // the sum of block t and runs its epilogue.
+  // Reduce over the KS k shares of each token group, one token block per
+  // round; the wave with ks == t % KS keeps the sum of block t and runs its
+  // epilogue.
   const int col = lane & 15;
 #pragma unroll
   for (int t = 0; t < NT; ++t) {
     red[wave][0][lane] = acc_a[t];
-    red[wave][1][lane] = acc_b[t];
+    if constexpr (!ONE) red[wave][1][lane] = acc_b[t];
     __syncthreads();
-    if (wave == t % KW) {
-      floatx4 sa = red[0][0][lane], sb = red[0][1][lane];
+    if (ks == t % KS) {
+      floatx4 sa = red[tg * KS][0][lane], sb = ONE ? sa : red[tg * KS][1][lane];
 #pragma unroll
-      for (int w = 1; w < KW; ++w) { sa += red[w][0][lane]; sb += red[w][1][lane]; }
+      for (int w = 1; w < KS; ++w) {
+        sa += red[tg * KS + w][0][lane];
+        if constexpr (!ONE) sb += red[tg * KS + w][1][lane];
+      }
       acc_a[t] = sa; acc_b[t] = sb;
     }
     __syncthreads();
   }
 #pragma unroll
   for (int t = 0; t < NT; ++t) {
-    if (wave != t % KW) continue;
+    if (ks != t % KS) continue;
     const int m = (mb0 + t) * 16 + col;
     const float rs = fold ? rscale[col] : 1.0f;
     epilogue<EPI>(a, pair, lane, min(m, a.M - 1), acc_a[t], acc_b[t], b_ok, m < a.M, rs);
   }
 }
 
-template <int EPI, int NT, bool ONE>
+template <int EPI, int KT, int NT, bool ONE>
 static hipError_t launch_one(const GemmArgs& a, hipStream_t s) {
   constexpr int PF = gemm_pf(NT);
-  const dim3 grid(a.n_pairs, a.mtiles);
-  if (a.splits == 8)
-    hipLaunchKernelGGL((k_gemm_ks<8, NT, PF, EPI, ONE>), grid, dim3(8 * 64), 0, s, a);
-  else if (a.splits == 4)
-    hipLaunchKernelGGL((k_gemm_ks<4, NT, PF, EPI, ONE>), grid, dim3(4 * 64), 0, s, a);
-  else
-    return hipErrorInvalidValue;
-  return hipGetLastError();
+  const dim3 grid((a.n_pairs + 7) / 8 * 8 * a.mtiles);
+  const int ks = a.splits / KT;
+  if constexpr (KT == 1) {
+    if (ks == 8) {
+      hipLaunchKernelGGL((k_gemm_ks<8, 1, NT, PF, EPI, ONE>), grid, dim3(8 * 64), 0, s, a);
+      return hipGetLastError();
+    }
+    if (ks == 4) {
+      hipLaunchKernelGGL((k_gemm_ks<4, 1, NT, PF, EPI, ONE>), grid, dim3(4 * 64), 0, s, a);
+      return hipGetLastError();
+    }
+  } else {
+    if (ks == 4) {
+      hipLaunchKernelGGL((k_gemm_ks<4, KT, NT, PF, EPI, ONE>), grid, dim3(4 * KT * 64), 0, s, a);
+      return hipGetLastError();
+    }
+    if (ks == 2) {
+      hipLaunchKernelGGL((k_gemm_ks<2, KT, NT, PF, EPI, ONE>), grid, dim3(2 * KT * 64), 0, s, a);
+      return hipGetLastError();
+    }
+  }
+  return hipErrorInvalidValue;
 }
 
 template <int EPI, int NT>
 static hipError_t launch_nt(const GemmArgs& a, hipStream_t s) {
   const bool one = a.map == MAP_SINGLE || a.map == MAP_QKV_SINGLE;
   if constexpr (EPI == EPI_RESID || EPI == EPI_STORE || EPI == EPI_QKV_RAW) {
-    if (one) return NT == 1 ? launch_one<EPI, 1, true>(a, s) : hipErrorInvalidValue;
+    if (one) return (NT == 1 && a.tgroups == 1) ? launch_one<EPI, 1, 1, true>(a, s) : hipErrorInvalidValue;
   }
   if (one) return hipErrorInvalidValue;
-  if constexpr (EPI == EPI_QKV_RAW) return hipErrorInvalidValue;
-  else return launch_one<EPI, NT, false>(a, s);
+  if constexpr (EPI == EPI_QKV_RAW) {
+    return hipErrorInvalidValue;
+  } else {
+    if (a.tgroups == 1) return launch_one<EPI, 1, NT, false>(a, s);
+    return hipErrorInvalidValue;
+  }
 }
 
 template <int EPI>

@@ -104,9 +104,10 @@ def config_c1() -> VLAConfig:
 def config_mid() -> VLAConfig:
     """Mid-size decoder for complete (every element) parity checks: 2 layers,
     d=2048, 16 heads of 128, FFN 5504, vocab 4096 (last 256 are action bins),
-    112x112 frame -> 64 patches, 8 text tokens, 7 action tokens."""
+    two 112x112 views -> 128 patches, 8 text tokens (136 prompt rows), 7
+    action tokens."""
     return VLAConfig(name="MID", n_layers=2, d_model=2048, n_heads=16, ffn=5504, vocab=4096,
-                     img=112, n_text=8, tau=(99, 100), theta=0.1, seed=11,
+                     img=112, n_views=2, n_text=8, tau=(99, 100), theta=0.1, seed=11,
                      wscale_log2=-5, bin_scale_log2=-1)
 
 

@@ -1,7 +1,8 @@
 """Parity of the HIP path with the oracle, every element, on the tiny config
-(2 layers, d=256, 4 heads of 64, FFN 688) and on a mid-size config (d=2048,
-16 heads of 128, FFN 5504: several pipelined k chunks per wave plus a ragged
-k tail), both with 64 patches + 8 text tokens (72 rows: five 16-row token
+(2 layers, d=256, 4 heads of 64, FFN 688; 64 patches + 8 text tokens = 72
+rows: five 16-row token blocks, the last one partial) and on a mid-size
+config (d=2048, 16 heads of 128, FFN 5504: several pipelined k chunks per
+wave plus a ragged k tail; two views, 136 rows: two token groups of 16-row
 blocks, the last one partial).  Every call goes through the C ABI."""
 import numpy as np
 import pytest
@@ -20,7 +21,7 @@ def c1(request):
     from paper_2608_10824_amd import gvc
     cfg = synth.config_c1() if request.param == "C1" else synth.config_mid()
     w = synth.model_weights(cfg)
-    si = synth.step_inputs(cfg, 45)
+    si = synth.step_inputs(cfg, 45 * cfg.n_views)
     dev = torch.device("cuda:0")
     s = Session(cfg, to_dev(w, dev), device=dev)
     o = OracleVLA(cfg, w)
