@@ -236,7 +236,7 @@ def main():
         "gate_fired_steps": sum(fired),
         "roofline": {"bound": "hbm", "achieved": gu_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": gu_gbs / HBM_PEAK_GBS, "traffic": traffic,
-                     "kernel": "k_gemm_ks<4,1,8,EPI_SILU,false> (decode gate/up projection, M=1)",
+                     "kernel": "k_gemm_ks<KS=4,KT=1,NT=1,PF=8,EPI_SILU,ONE=false> (decode gate/up projection, M=1)",
                      "bytes_per_launch": gu_bytes, "avg_launch_us": gu_avg_s * 1e6, "launches": gu_n,
                      "region_ms_per_step": dt2 * 1e3 / args.steps},
     }

@@ -20,7 +20,7 @@ rounds to bf16 with round-to-nearest-even (torch's fp32->bf16 cast); the
 bits are the same on every device.
 """
 from .hashgen import lowbias32, hash_u32, uniform_f32, uniform_bf16, uniform_u8
-from .configs import VLAConfig, config_c1, config_mid, config_c2, config_c3, config_c4, config_c5, ALL_CONFIGS
+from .configs import VLAConfig, config_c1, config_mid, config_c4_tiny, config_c2, config_c3, config_c4, config_c5, ALL_CONFIGS
 from .workload import (
     TensorId, layer_weights, global_weights, model_weights,
     random_frame, changed_patch_order, perturb_patches, text_ids, extra_rows,
@@ -29,7 +29,7 @@ from .workload import (
 
 __all__ = [
     "lowbias32", "hash_u32", "uniform_f32", "uniform_bf16", "uniform_u8",
-    "VLAConfig", "config_c1", "config_mid", "config_c2", "config_c3", "config_c4", "config_c5", "ALL_CONFIGS",
+    "VLAConfig", "config_c1", "config_mid", "config_c4_tiny", "config_c2", "config_c3", "config_c4", "config_c5", "ALL_CONFIGS",
     "TensorId", "layer_weights", "global_weights", "model_weights",
     "random_frame", "changed_patch_order", "perturb_patches", "text_ids", "extra_rows",
     "step_inputs", "c3_episode_frames", "reuse_schedule",

@@ -111,6 +111,16 @@ def config_mid() -> VLAConfig:
                      wscale_log2=-5, bin_scale_log2=-1)
 
 
+def config_c4_tiny() -> VLAConfig:
+    """Tiny parallel-decoded action chunk for complete parity: the C1 decoder
+    with two views (128 patches), 8 text tokens, 1 proprio row and 8
+    action-query rows decoded in one pass; gate on the minimum margin."""
+    return VLAConfig(name="C4T", n_layers=2, d_model=256, n_heads=4, ffn=688, vocab=1024,
+                     img=112, n_views=2, n_text=8, n_proprio=1, n_action_q=8, n_decode=8,
+                     parallel_decode=True, reduce_min=True, tau=(99, 100), theta=0.1, seed=6,
+                     wscale_log2=-4, bin_scale_log2=0)
+
+
 def config_c2() -> VLAConfig:
     """Llama-2-7B shape, 256 visual + 20 text tokens, one step at 50% reuse,
     then 7-token autoregressive action decode."""

@@ -1,0 +1,174 @@
+"""Edge cases of the HIP path, every element checked against the oracle (or
+bit-exactly against another GPU run where the method fixes the result):
+parallel-decoded action chunk, identical frames, no static patch, all-zero
+frames, a single action token, per-episode static counts, the largest
+frame the library accepts.  Every call goes through the C ABI."""
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle.vla import OracleVLA
+from oracle import patches as op
+from oracle.margin import gate_fires
+from tests._parity import TOL, rel_err, to_dev, check_tokens, check_margins
+
+pytestmark = pytest.mark.gpu
+DEV = torch.device("cuda:0")
+
+
+def _session(cfg, w):
+    from paper_2608_10824_amd.session import Session
+    return Session(cfg, to_dev(w, DEV), device=DEV)
+
+
+def _state(s, cfg):
+    from paper_2608_10824_amd import gvc
+    H = [s.read(gvc.STATE_H, l).cpu().numpy() for l in range(cfg.n_layers + 1)]
+    K = [s.read(gvc.STATE_K, l).float().cpu().numpy() for l in range(cfg.n_layers)]
+    V = [s.read(gvc.STATE_V, l).float().cpu().numpy() for l in range(cfg.n_layers)]
+    return H, K, V, s.read(gvc.STATE_HEAD_LOGITS).cpu().numpy()
+
+
+def test_parallel_action_chunk_complete_parity():
+    """Two views, a proprio row and 8 action-query rows decoded in one pass
+    (the OFT variant, Sec. V-A): state, the 8 positions' logits, tokens,
+    margins and the minimum-margin gate."""
+    from paper_2608_10824_amd import gvc
+    cfg = synth.config_c4_tiny()
+    w = synth.model_weights(cfg)
+    si = synth.step_inputs(cfg, 90)
+    s = _session(cfg, w)
+    o = OracleVLA(cfg, w)
+    fp, ft, ids, ex = si["frame_prev"], si["frame_t"], si["text_ids"], si["extra_rows"]
+    s.step_prefill(fp.to(DEV), ids.to(DEV), ex.to(DEV))
+    o.step_prefill(fp.numpy(), ids.numpy(), ex.numpy())
+    s.decode_actions()
+    o.decode_actions()
+    s.margin_gate(force=[0])
+    o.margin_gate(force=[0])
+    mask, _ = s.select_static(ft.to(DEV), fp.to(DEV))
+    mo, _ = o.select_static(ft.numpy(), fp.numpy())
+    assert np.array_equal(mask.cpu().numpy().astype(bool), mo)
+    s.step_prefill(ft.to(DEV), ids.to(DEV), ex.to(DEV), mask)
+    o.step_prefill(ft.numpy(), ids.numpy(), ex.numpy(), mo)
+    H, K, V, z = _state(s, cfg)
+    for l in range(cfg.n_layers + 1):
+        assert rel_err(H[l], o.H[l]) <= TOL
+    assert rel_err(z, o.head_logits) <= TOL
+    tok, mg, lg = s.decode_actions(logits=True)
+    tok_o, mg_o, lg_o = o.decode_actions()
+    torch.cuda.synchronize()
+    assert rel_err(lg.cpu().numpy(), lg_o) <= TOL
+    check_tokens(tok.cpu().numpy(), lg.cpu().numpy(), tok_o, lg_o, cfg.bin_lo)
+    check_margins(mg.cpu().numpy(), mg_o, lg.cpu().numpy(), lg_o, cfg.bin_lo)
+    m, fire = s.margin_gate()
+    assert abs(m[0] - float(mg.cpu().numpy()[0].min())) <= 1e-6
+    assert fire[0] == gate_fires(m[0], cfg.theta)
+    s.close()
+
+
+def test_identical_frame_full_reuse_is_bit_identical():
+    """After a full step, the same frame with every patch reused recomputes
+    only the text rows; with deterministic, row-independent kernels the
+    whole state must equal the previous step bit for bit."""
+    cfg = synth.config_c1()
+    w = synth.model_weights(cfg)
+    si = synth.step_inputs(cfg, 45)
+    s = _session(cfg, w)
+    fp, ids = si["frame_prev"].to(DEV), si["text_ids"].to(DEV)
+    s.step_prefill(fp, ids)
+    ref = _state(s, cfg)
+    mask, n_static = s.select_static(fp, fp)
+    assert n_static.item() == cfg.n_patches and bool(mask.all())
+    s.step_prefill(fp, ids, None, mask)
+    got = _state(s, cfg)
+    from paper_2608_10824_amd import gvc
+    assert s.read(gvc.STATE_ROWS).cpu().tolist() == [cfg.n_text] * cfg.n_layers
+    for a, b in zip(got[0] + got[1] + got[2] + [got[3]], ref[0] + ref[1] + ref[2] + [ref[3]]):
+        assert np.array_equal(a, b)
+    s.close()
+
+
+def test_no_static_patch_equals_fresh_full_pass():
+    cfg = synth.config_c1()
+    w = synth.model_weights(cfg)
+    si = synth.step_inputs(cfg, 0)
+    s = _session(cfg, w)
+    fp, ft, ids = si["frame_prev"].to(DEV), si["frame_t"].to(DEV), si["text_ids"].to(DEV)
+    s.step_prefill(fp, ids)
+    mask, n_static = s.select_static(ft, fp)
+    assert n_static.item() == 0 and not bool(mask.any())
+    s.step_prefill(ft, ids, None, mask)
+    got = _state(s, cfg)
+    s2 = _session(cfg, w)
+    s2.step_prefill(ft, ids)
+    ref = _state(s2, cfg)
+    for a, b in zip(got[0] + [got[3]], ref[0] + [ref[3]]):
+        assert np.array_equal(a, b)
+    s.close()
+    s2.close()
+
+
+def test_zero_frames_and_per_episode_counts():
+    """All-zero patches are static against all-zero patches and dynamic
+    against anything else; episodes of one batch keep their own counts."""
+    cfg = synth.config_c1().with_(batch=3)
+    w = synth.model_weights(cfg)
+    s = _session(cfg, w)
+    si = synth.step_inputs(cfg, [0, 17, 64])
+    fp, ft = si["frame_prev"].clone(), si["frame_t"].clone()
+    fp[2] = 0
+    ft[2] = 0
+    ft[1, 0, :14, :14, :] = 0          # patch 0 of episode 1: zero vs non-zero
+    mask, n_static = s.select_static(ft.to(DEV), fp.to(DEV))
+    exp = []
+    for b in range(cfg.batch):
+        m, n, st, _ = op.select_static(ft[b].numpy(), fp[b].numpy(), cfg.patch, cfg.tau, cfg.permille())
+        exp.append(m)
+        assert n_static[b].item() == n
+    assert np.array_equal(mask.cpu().numpy().astype(bool), np.stack(exp))
+    assert n_static.cpu().tolist()[2] == cfg.n_patches
+    ids = si["text_ids"].to(DEV)
+    s.step_prefill(fp.to(DEV), ids)
+    s.decode_actions()
+    s.margin_gate(force=[0, 0, 0])
+    s.step_prefill(ft.to(DEV), ids, None, mask)
+    from paper_2608_10824_amd import gvc
+    rows = s.read(gvc.STATE_ROWS).cpu().tolist()
+    assert rows == [sum(cfg.prompt_len - int(e[l].sum()) for e in exp) for l in range(cfg.n_layers)]
+    s.close()
+
+
+def test_single_action_token():
+    """D = 1: the prompt pass's head row gives the only token; no decode pass."""
+    cfg = synth.config_c1().with_(n_decode=1)
+    w = synth.model_weights(cfg)
+    si = synth.step_inputs(cfg, 45)
+    s = _session(cfg, w)
+    o = OracleVLA(cfg, w)
+    s.step_prefill(si["frame_prev"].to(DEV), si["text_ids"].to(DEV))
+    o.step_prefill(si["frame_prev"].numpy(), si["text_ids"].numpy())
+    tok, mg, lg = s.decode_actions(logits=True)
+    tok_o, mg_o, lg_o = o.decode_actions()
+    torch.cuda.synchronize()
+    assert rel_err(lg.cpu().numpy(), lg_o) <= TOL
+    check_tokens(tok.cpu().numpy(), lg.cpu().numpy(), tok_o, lg_o, cfg.bin_lo)
+    check_margins(mg.cpu().numpy(), mg_o, lg.cpu().numpy(), lg_o, cfg.bin_lo)
+    s.close()
+
+
+def test_largest_frame_selection():
+    """1024 patches (448 x 448, p = 14), the most the library accepts:
+    exact masks and ranking-dependent per-layer counts against the oracle."""
+    cfg = synth.config_c1().with_(img=448, reuse_permille=[700, 300])
+    w = synth.model_weights(cfg)
+    s = _session(cfg, w)
+    si = synth.step_inputs(cfg, 600)
+    mask, n_static = s.select_static(si["frame_t"].to(DEV), si["frame_prev"].to(DEV))
+    m, n, _, _ = op.select_static(si["frame_t"][0].numpy(), si["frame_prev"][0].numpy(), cfg.patch, cfg.tau,
+                                  cfg.permille())
+    assert n == 600 and n_static.item() == 600
+    assert np.array_equal(mask[0].cpu().numpy().astype(bool), m)
+    assert mask[0].sum(dim=1).cpu().tolist() == [420, 180]
+    s.close()
