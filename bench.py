@@ -23,7 +23,7 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
 # sources of the dominant kernel; its stored traffic figure is used only while they are unchanged
-KERNEL_SOURCES = ("paper_2608_10824_amd/csrc/k_gemm.hip", "paper_2608_10824_amd/csrc/gvc_kernels.h")
+KERNEL_SOURCES = ("paper_2608_10824_amd/csrc/k_decode.hip", "paper_2608_10824_amd/csrc/gvc_kernels.h")
 BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 
 
@@ -91,7 +91,7 @@ def stored_traffic(kernel_sources):
     """HBM bytes per launch of the dominant kernel from the committed rocprofv3
     counter summary, or None when the kernel sources changed since."""
     import hashlib
-    path = os.path.join(ROOT, "profiles", "traffic_decode_gate_up_c2.md")
+    path = os.path.join(ROOT, "profiles", "traffic_decode_pass_c2.md")
     if not os.path.exists(path):
         return None
     h = hashlib.sha256()
@@ -179,25 +179,31 @@ def main():
 
     # second region, same steps: phase events and the dominant kernel's launches
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
-    launches_per_step = (cfg.n_decode - 1) * cfg.n_layers
-    gvc.profile_begin(s.ctx, gvc.K_DECODE_GU, launches_per_step * args.steps + 8)
+    launches_per_step = cfg.n_decode - 1
+    gvc.profile_begin(s.ctx, gvc.K_DECODE_PASS, launches_per_step * args.steps + 8)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
         control_step(evs[i])
     torch.cuda.synchronize()
     dt2 = time.perf_counter() - t0
-    gu_ms, gu_n = gvc.profile_end(s.ctx)
+    dk_ms, dk_n = gvc.profile_end(s.ctx)
     note("profiled region done")
+    if dk_n == 0:
+        raise SystemExit("bench: the single-launch decode pass did not run (GVC_DECODE=legacy or an ineligible shape)")
     prefill_ms = sum(e[0].elapsed_time(e[1]) for e in evs) / args.steps
     decode_ms = sum(e[1].elapsed_time(e[2]) for e in evs) / args.steps
 
     d, F, V, L, P = cfg.d_model, cfg.ffn, cfg.vocab, cfg.n_layers, cfg.prompt_len
     traffic = stored_traffic(KERNEL_SOURCES)
-    # dominant kernel: decode gate/up GEMM, one launch per layer per decode pass
-    gu_bytes = 2 * F * d * 2 + d * 2 + F * 2
-    gu_avg_s = gu_ms / 1e3 / max(gu_n, 1)
-    gu_gbs = gu_bytes / gu_avg_s / 1e9
+    # dominant kernel: the single-launch decode pass (all layers of one token),
+    # one launch per decode pass; algorithmic bytes = every layer's weights
+    # once + the K and V rows of positions 0..pos read by the attention,
+    # averaged over the passes (pass j attends over P + j keys)
+    n_pass = cfg.n_decode - 1
+    dk_bytes = L * layer_weight_bytes(cfg) + sum(L * 2 * (P + j) * d * 2 for j in range(1, n_pass + 1)) / n_pass
+    dk_avg_s = dk_ms / 1e3 / max(dk_n, 1)
+    dk_gbs = dk_bytes / dk_avg_s / 1e9
     # prompt pass algorithmic work: the recomputed rows of every layer, their
     # attention over the keys up to each row's position, and the head row
     mask = s.mask[0].cpu().numpy().astype(bool)              # [L][N]
@@ -234,10 +240,10 @@ def main():
         "decode_gbs": decode_bytes / (decode_ms / 1e3) / 1e9,
         "decode_hbm_frac": decode_bytes / (decode_ms / 1e3) / 1e9 / HBM_PEAK_GBS,
         "gate_fired_steps": sum(fired),
-        "roofline": {"bound": "hbm", "achieved": gu_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": gu_gbs / HBM_PEAK_GBS, "traffic": traffic,
-                     "kernel": "k_gemm_ks<KS=4,KT=1,NT=1,PF=8,EPI_SILU,ONE=false> (decode gate/up projection, M=1)",
-                     "bytes_per_launch": gu_bytes, "avg_launch_us": gu_avg_s * 1e6, "launches": gu_n,
+        "roofline": {"bound": "hbm", "achieved": dk_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": dk_gbs / HBM_PEAK_GBS, "traffic": traffic,
+                     "kernel": "k_decode_pass<128> (one decode pass over all 32 layers, cooperative grid)",
+                     "bytes_per_launch": dk_bytes, "avg_launch_us": dk_avg_s * 1e6, "launches": dk_n,
                      "region_ms_per_step": dt2 * 1e3 / args.steps},
     }
     if not args.no_cpu_baseline:

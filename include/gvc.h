@@ -211,7 +211,7 @@ enum gvc_kernel_class {
   GVC_K_DECODE_DOWN = 4, GVC_K_DECODE_HEAD = 5,
   GVC_K_PREFILL_QKV = 6, GVC_K_PREFILL_ATTN = 7, GVC_K_PREFILL_O = 8, GVC_K_PREFILL_GU = 9,
   GVC_K_PREFILL_DOWN = 10, GVC_K_PREFILL_HEAD = 11, GVC_K_EMBED = 12, GVC_K_NORM = 13,
-  GVC_K_SELECT = 14, GVC_K_COUNT = 15
+  GVC_K_SELECT = 14, GVC_K_DECODE_PASS = 15, GVC_K_COUNT = 16
 };
 
 /* Starts timing every launch of kernel class `cls` (enum gvc_kernel_class):

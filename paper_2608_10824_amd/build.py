@@ -16,7 +16,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libgvc.so")
-SOURCES = ["k_gemm.hip", "k_select.hip", "k_misc.hip", "k_attn.hip", "gvc_api.hip"]
+SOURCES = ["k_gemm.hip", "k_select.hip", "k_misc.hip", "k_attn.hip", "k_decode.hip", "gvc_api.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

@@ -59,7 +59,7 @@ struct Plan {
   // workspace
   size_t rows_off, counts_off, epc_off, epo_off, stats_off, x_off, q_off, o_off, r_off, act_off, xdec_off, xf_off,
       ssq_a_off, ssq_f_off, qraw_off, kraw_off,
-      logits_off, rope_off, decrows_off, headrows_off, tokens_off, gate_m_off, gate_f_off,
+      logits_off, rope_off, decrows_off, headrows_off, tokens_off, gate_m_off, gate_f_off, qkv3_off, bar_off,
       ws_bytes;
 };
 
@@ -163,6 +163,8 @@ int32_t make_plan(const gvc_desc* dsc, Plan& p) {
   p.tokens_off = k.take((size_t)p.B * p.D * 4);
   p.gate_m_off = k.take((size_t)p.B * 4);
   p.gate_f_off = k.take((size_t)p.B * 4);
+  p.qkv3_off = k.take((size_t)3 * p.B * d.d_model * 4);
+  p.bar_off = k.take((size_t)kDecodeBarWords * 4);
   p.ws_bytes = k.off;
   return GVC_OK;
 }
@@ -179,6 +181,12 @@ struct gvc_ctx {
   bool prefill_done = false;
   bool decode_done = false;
   int force_splits = 0;   // GVC_FORCE_SPLITS: waves splitting each GEMM's k range (4 or 8; testing)
+  // persistent decode pass (k_decode.hip): eligible shape, its grid and LDS
+  bool persist = false;
+  int persist_wg = 0;
+  DecodeArgs dargs{};
+  bool persist_ran = false;       // a launch sequence ran since the last check of the abort word
+  uint32_t abort_word = 0;        // host copy, read by margin_gate
   // launch timing of one kernel class (gvc_profile_begin / _end)
   int prof_cls = -1;
   std::vector<hipEvent_t> prof_ev;
@@ -441,6 +449,76 @@ int32_t gvc_sizes(const gvc_desc* desc, size_t* weight_bytes, size_t* state_byte
   return GVC_OK;
 }
 
+namespace {
+
+// The persistent decode pass serves one episode with sequential decoding,
+// when every layer's packed matrices sit at one uniform stride, each
+// workgroup's share of a step fits kDecodeMaxSeg blocks and the grid of one
+// workgroup per compute unit can be co-resident.  GVC_DECODE=legacy turns
+// it off (per-step launches).
+bool setup_persist(gvc_ctx* c) {
+  const Plan& p = c->p;
+  const char* mode = getenv("GVC_DECODE");
+  if (mode && strcmp(mode, "legacy") == 0) return false;
+  if (p.B != 1 || p.d.parallel_decode || p.D < 2) return false;
+  const int d = p.d.d_model, F = p.F;
+  if (d % 256 || d > 8192 || F > 16384 || (p.dh != 64 && p.dh != 128) || F % 16) return false;
+  const size_t u = sizeof(bf16x8);
+  auto at = [&](const Packed& m) { return (long long)(m.off / u); };
+  const long long qkv_stride = at(p.wk[0]) - at(p.wq[0]), gu_stride = at(p.wu[0]) - at(p.wg[0]);
+  const long long layer_stride = p.L > 1 ? at(p.wq[1]) - at(p.wq[0]) : 0;
+  for (int l = 0; l < p.L; ++l) {
+    const long long s = l * layer_stride;
+    if (at(p.wq[l]) != at(p.wq[0]) + s || at(p.wk[l]) != at(p.wq[l]) + qkv_stride ||
+        at(p.wv[l]) != at(p.wq[l]) + 2 * qkv_stride || at(p.wo[l]) != at(p.wo[0]) + s ||
+        at(p.wg[l]) != at(p.wg[0]) + s || at(p.wu[l]) != at(p.wg[l]) + gu_stride || at(p.wd[l]) != at(p.wd[0]) + s)
+      return false;
+  }
+  int G = 0, coop = 0;
+  if (hipDeviceGetAttribute(&G, hipDeviceAttributeMultiprocessorCount, c->device) != hipSuccess) return false;
+  if (hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, c->device) != hipSuccess || !coop) return false;
+  auto ceil_div = [](int a, int b) { return (a + b - 1) / b; };
+  if (G < 1 || p.H > G || p.H > kDecodeMaxHeads) return false;
+  const int n_slices = std::min(G / p.H, d / 16);
+  if (3 * ceil_div(p.dh / 16, n_slices) > kDecodeMaxSeg || 2 * ceil_div(F / 16, G) > kDecodeMaxSeg ||
+      ceil_div(d / 16, G) > kDecodeMaxSeg || ceil_div(ceil_div(d / 16, n_slices), 8) > kDecodeMaxSeg)
+    return false;
+  int act = std::max({d * 4, p.KBf * 32 * 2, p.KBd * 32 * 2, decode_pass_score_offset() + p.kv_pad * 4});
+  act = (act + 15) / 16 * 16;
+  const void* f = decode_pass_kernel(p.dh);
+  const size_t lds = decode_pass_lds_bytes(act);
+  if (hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess) {
+    (void)hipGetLastError();
+    return false;
+  }
+  int per_cu = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, f, decode_pass_threads(), lds) != hipSuccess ||
+      per_cu < 1) {
+    (void)hipGetLastError();
+    return false;
+  }
+  DecodeArgs& a = c->dargs;
+  memset(&a, 0, sizeof(a));
+  a.wq = c->packed(p.wq[0]); a.wo = c->packed(p.wo[0]); a.wg = c->packed(p.wg[0]); a.wd = c->packed(p.wd[0]);
+  a.qkv_stride = (size_t)qkv_stride; a.gu_stride = (size_t)gu_stride; a.layer_stride = (size_t)layer_stride;
+  a.kc = c->Kc(0); a.vc = c->Vc(0); a.kv_layer_elems = p.layer_kv_elems;
+  a.gains = c->W<float>(p.gains_off);
+  a.rope = c->K<float2>(p.rope_off);
+  a.x = c->K<float>(p.xdec_off);
+  a.r = c->K<float>(p.r_off);
+  a.qkv = c->K<float>(p.qkv3_off);
+  a.act = c->K<bf16>(p.act_off);
+  a.bar = c->K<unsigned>(p.bar_off);
+  a.timeout_ticks = 50000000;   // 0.5 s at the 100 MHz wall clock
+  a.L = p.L; a.d = d; a.F = F; a.H = p.H; a.head_dim = p.dh; a.KBd = p.KBd; a.KBf = p.KBf; a.kv_pad = p.kv_pad;
+  a.act_bytes = act;
+  a.eps = p.d.rms_eps;
+  c->persist_wg = G;
+  return true;
+}
+
+}  // namespace
+
 int32_t gvc_init_cache(const gvc_desc* desc, const gvc_weights* wt, void* weight_arena, size_t weight_bytes,
                        void* state, size_t state_bytes, void* workspace, size_t workspace_bytes, void* stream,
                        gvc_ctx** out) {
@@ -522,6 +600,7 @@ int32_t gvc_init_cache(const gvc_desc* desc, const gvc_weights* wt, void* weight
   INIT_TRY(hipMemcpyAsync(c->K<int>(p.decrows_off), dec.data(), dec.size() * 4, hipMemcpyHostToDevice, s));
   INIT_TRY(hipMemcpyAsync(c->K<int>(p.headrows_off), head.data(), head.size() * 4, hipMemcpyHostToDevice, s));
   INIT_TRY(hipStreamSynchronize(s));
+  c->persist = setup_persist(c);
 #undef INIT_TRY
   *out = c;
   return GVC_OK;
@@ -618,20 +697,39 @@ int32_t gvc_decode_actions(gvc_ctx* c, int32_t* tokens_out, float* margins_out, 
                                   c->W<float>(p.gains_off), c->K<bf16>(p.x_off), p.KBd, c->K<float>(p.ssq_a_off), s));
       const RowMap rows = c->dec_rows(j);
       const int pos = p.P + j - 1;
-      for (int l = 0; l < p.L; ++l) {
-        int32_t r = run_layer_decode(c, l, rows, pos + 1, l == 0 ? 1 : p.d.d_model / 16);
-        if (r) return r;
+      GemmArgs hd = base_args(c);
+      hd.w[0] = c->packed(p.lm); hd.wblk[0] = p.lm.Nblk;
+      hd.map = MAP_PLAIN; hd.n_pairs = (p.lm.Nblk + 1) / 2; hd.n_out = p.V; hd.KB = p.KBd;
+      hd.x = c->K<bf16x8>(p.x_off);
+      hd.e.rows = rows; hd.e.store = lg; hd.e.ld_store = p.V;
+      if (c->persist) {
+        // all layers in one cooperative launch, then the final norm and the head
+        if (j == 1) HIP_TRY(launch_fill_u32(c->K<uint32_t>(p.bar_off), 0u, kDecodeBarWords, s));
+        DecodeArgs a = c->dargs;
+        a.pos = pos;
+        a.bar_base = (unsigned)((j - 1) * decode_grid_barriers(p.L));
+        a.hbar_base = (unsigned)((j - 1) * decode_head_barriers(p.L));
+        {
+          ProfScope ps(c, GVC_K_DECODE_PASS);
+          HIP_TRY(launch_decode_pass(a, c->persist_wg, s));
+        }
+        c->persist_ran = true;
+        {
+          ProfScope ps(c, GVC_K_NORM);
+          HIP_TRY(launch_rmsnorm(xdec, nullptr, p.B, p.d.d_model, c->W<float>(p.final_gain_off), p.d.rms_eps,
+                                 c->K<bf16>(p.x_off), p.KBd, s));
+        }
+      } else {
+        for (int l = 0; l < p.L; ++l) {
+          int32_t r = run_layer_decode(c, l, rows, pos + 1, l == 0 ? 1 : p.d.d_model / 16);
+          if (r) return r;
+        }
+        // the LM head reads the folded final norm written by the last down projection
+        hd.e.ssq_in = c->K<float>(p.ssq_a_off); hd.e.ssq_parts = p.d.d_model / 16;
+        hd.e.norm_eps = p.d.rms_eps; hd.e.norm_dim = p.d.d_model;
       }
       {
-        // LM head on the folded final norm written by the last down projection
-        GemmArgs a = base_args(c);
-        a.w[0] = c->packed(p.lm); a.wblk[0] = p.lm.Nblk;
-        a.map = MAP_PLAIN; a.n_pairs = (p.lm.Nblk + 1) / 2; a.n_out = p.V; a.KB = p.KBd;
-        a.x = c->K<bf16x8>(p.x_off);
-        a.e.rows = rows; a.e.store = lg; a.e.ld_store = p.V;
-        a.e.ssq_in = c->K<float>(p.ssq_a_off); a.e.ssq_parts = p.d.d_model / 16;
-        a.e.norm_eps = p.d.rms_eps; a.e.norm_dim = p.d.d_model;
-        int32_t r = run_gemm(c, a, EPI_STORE, p.B, GVC_K_DECODE_HEAD);
+        int32_t r = run_gemm(c, hd, EPI_STORE, p.B, GVC_K_DECODE_HEAD);
         if (r) return r;
       }
       HIP_TRY(launch_logits_reduce(lg, p.B, p.V, p.bin_lo, full, tok, mg, p.D, j, 1, s));
@@ -662,7 +760,15 @@ int32_t gvc_margin_gate(gvc_ctx* c, float theta, int32_t reduce, float* margin_o
   std::vector<int> hf(p.B);
   HIP_TRY(hipMemcpyAsync(hm.data(), m, (size_t)p.B * 4, hipMemcpyDeviceToHost, c->stream));
   HIP_TRY(hipMemcpyAsync(hf.data(), f, (size_t)p.B * 4, hipMemcpyDeviceToHost, c->stream));
+  const bool check_abort = c->persist_ran;
+  if (check_abort)
+    HIP_TRY(hipMemcpyAsync(&c->abort_word, c->K<uint32_t>(p.bar_off) + kDecodeAbortWord, 4, hipMemcpyDeviceToHost,
+                           c->stream));
   HIP_TRY(hipStreamSynchronize(c->stream));
+  if (check_abort) {
+    c->persist_ran = false;
+    if (c->abort_word) return fail(GVC_EDEVICE, "decode pass: grid barrier timed out");
+  }
   for (int b = 0; b < p.B; ++b) {
     if (margin_out) margin_out[b] = hm[b];
     if (fire_out) fire_out[b] = (uint8_t)(hf[b] != 0);

@@ -102,6 +102,39 @@ struct GemmArgs {
 // k-steps per pipelined register chunk for a tile of NT blocks of 16 token rows.
 constexpr int gemm_pf(int NT) { return NT == 1 ? 8 : (NT <= 3 ? 4 : (NT <= 6 ? 2 : 1)); }
 
+// ------------------------------------------------------------------ persistent decode pass
+// One single-token pass over all layers for one episode (k_decode.hip).
+constexpr int kDecodeMaxSeg = 8;       // weight blocks per workgroup per step
+constexpr int kDecodeAbortWord = 512;  // barrier words: abort flag
+constexpr int kDecodeXccWord = 544;    // barrier words: set when a workgroup is not on XCD blockIdx % 8
+constexpr int kDecodeHeadWord = 1024;  // barrier words: per-head counters, 32 words apart
+constexpr int kDecodeMaxHeads = 64;
+constexpr int kDecodeBarWords = kDecodeHeadWord + 32 * kDecodeMaxHeads;   // zeroed before a launch sequence
+// grid barriers and per-head barriers of one pass over L layers
+constexpr int decode_grid_barriers(int L) { return 1 + 3 * L; }
+constexpr int decode_head_barriers(int L) { return L; }
+
+struct DecodeArgs {
+  // packed weights of layer 0 (k = q + qkv_stride, v = q + 2 qkv_stride,
+  // up = gate + gu_stride); layer l's are l * layer_stride further (bf16x8 units)
+  const bf16x8* wq; const bf16x8* wo; const bf16x8* wg; const bf16x8* wd;
+  size_t qkv_stride, gu_stride, layer_stride;
+  bf16* kc; bf16* vc;          // layer 0 caches (episode 0); layer l at l * kv_layer_elems
+  size_t kv_layer_elems;
+  const float* gains;          // [L][2][d]: attention norm, FFN norm
+  const float2* rope;          // [kv_pad][head_dim/2]
+  float* x;                    // [d] layer input / output (in place)
+  float* r;                    // [d] residual after attention
+  float* qkv;                  // [3d] q, k, v before RoPE
+  bf16* act;                   // [F] SwiGLU output
+  unsigned* bar;               // kDecodeBarWords barrier words
+  unsigned bar_base;           // grid barriers completed by earlier launches since the words were zeroed
+  unsigned hbar_base;          // per-head barriers completed by earlier launches
+  long long timeout_ticks;     // barrier wait limit in wall-clock ticks (100 MHz)
+  int L, d, F, H, head_dim, KBd, KBf, kv_pad, pos, act_bytes;
+  float eps;
+};
+
 // ------------------------------------------------------------------ launchers
 // All launchers enqueue on `s` and return hipGetLastError().
 hipError_t launch_pack(const bf16* src, int N, int K, bf16* dst, int Nblk, int KB, hipStream_t s);
@@ -131,6 +164,11 @@ hipError_t launch_embed_tokens(const bf16* embed, const int* tokens, int tok_str
 hipError_t launch_logits_reduce(const float* logits, int rows, int V, int bin_lo, int full_vocab,
                                 int* tok_out, float* margin_out, int out_stride, int out_col,
                                 int rows_per_ep, hipStream_t s);
+size_t decode_pass_lds_bytes(int act_bytes);
+int decode_pass_threads();
+int decode_pass_score_offset();
+const void* decode_pass_kernel(int head_dim);
+hipError_t launch_decode_pass(const DecodeArgs& a, int n_wg, hipStream_t s);   // cooperative launch
 hipError_t launch_gate(const float* margins, int B, int D, float theta, int use_min, const int8_t* force,
                        int* valid, float* m_out, int* fire_out, hipStream_t s);
 

@@ -1,0 +1,617 @@
+// Persistent decode pass for a single episode: every decoder layer of one
+// single-token pass (Sec. IV, autoregressive action decode) in one
+// cooperative launch of one workgroup per compute unit.
+//
+// A pass at batch 1 streams all decoder weights once and does almost no
+// arithmetic, so its time is set by how continuously HBM is kept busy.  As
+// separate launches, each step of a layer pays a launch gap, a ramp-up and a
+// tail.  Here the weights never wait for the data: each compute wave streams
+// its share of every matrix of every layer, in order, into a ring of 16
+// one-KiB fragments in LDS with direct global->LDS loads, and the ring keeps
+// running across the grid-wide barriers that separate the steps.  Only the
+// multiply waits for the activation vector.
+//
+// Steps of a layer (one grid barrier after each):
+//  1. QKV projection of RMSNorm(x); the raw q, k, v are published.
+//  2. Attention + output projection: the workgroups of head h (one per
+//     slice of the output rows, all on one XCD) each compute the head's
+//     attention over the cache (the new key and value from the raw q, k, v
+//     with RoPE) and multiply it by their slice of W_o's head-h columns,
+//     adding the result into the residual row r (= x, set in step 1) with
+//     device-scope atomic adds.  This takes the attention output's round
+//     trip through memory and one barrier off the critical path; the order
+//     of the head contributions per output is not fixed.
+//  3. Gate/up projection of RMSNorm(r) and SwiGLU; the activation is published.
+//  4. Down projection; x = r + result.
+//
+// Workgroup layout: 8 compute waves and 1 synchronising wave.
+//  * Compute waves stage each step's input into LDS (with the RMSNorm
+//    applied), split each block's k range 8 ways (the output projection:
+//    its blocks), multiply on MFMA and leave one partial sum per output per
+//    wave in LDS.
+//  * The synchronising wave sums the partials in a fixed order, applies the
+//    epilogue, publishes the results and runs the grid barrier.  It issues no
+//    weight loads, so its stores and barrier loads never queue behind the
+//    ring in the in-order memory counter.
+//  * Data crossing workgroups is written and read with device-coherent (sc1)
+//    buffer accesses; the barrier and the residual adds use device-scope
+//    atomics.  No cache write-back or invalidation is needed.
+//
+// Work split over the G workgroups (weights as 16-row blocks, see
+// gvc_kernels.h): QKV blocks [i*3d/16/G, (i+1)*3d/16/G); down projection
+// block i; gate/up pairs [i*F/16/G, (i+1)*F/16/G); step 2: head i % H,
+// output slice i / H of min(G/H, d/16) slices.
+#include "gvc_kernels.h"
+
+namespace gvc {
+
+namespace {
+
+constexpr int kWaves = 8;                      // compute waves
+constexpr int kThreads = (kWaves + 1) * 64;    // plus the synchronising wave
+constexpr int kRing = 16;                      // weight fragments in flight per compute wave
+constexpr int kSC1 = 16;                       // buffer cache policy: device-coherent access
+constexpr int kSC0 = 1;                        // buffer cache policy: coherent within an XCD
+constexpr int kRingBytes = kWaves * kRing * 1024;
+constexpr int kRedBytes = kWaves * kDecodeMaxSeg * 16 * 4;
+constexpr int kScoreOffset = 256;              // attention scores follow the head output in the act region
+
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x0F70);
+}
+__device__ __forceinline__ void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(0xC07F); }
+
+__device__ __forceinline__ rsrc_t rsrc(const void* p, size_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
+}
+__device__ __forceinline__ float ld_f32(rsrc_t r, int off) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, kSC1));
+}
+__device__ __forceinline__ u32x4 ld_b128(rsrc_t r, int off) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kSC1);
+}
+// Exchange within one XCD (device-coherent when `xl` is false): stores are
+// written through to the XCD's L2, loads with sc0 miss in the CU's L1.
+__device__ __forceinline__ float ld_f32_x(rsrc_t r, int off, bool xl) {
+  return xl ? __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, kSC0))
+            : __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, kSC1));
+}
+__device__ __forceinline__ void st_f32_x(rsrc_t r, int off, float v, bool xl) {
+  if (xl)
+    __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, v), r, off, 0, kSC0);
+  else
+    __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, v), r, off, 0, kSC1);
+}
+__device__ __forceinline__ u16x8 ld_plain_b128(rsrc_t r, int off) {
+  return __builtin_bit_cast(u16x8, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+}
+__device__ __forceinline__ void st_f32(rsrc_t r, int off, float v) {
+  __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, v), r, off, 0, kSC1);
+}
+__device__ __forceinline__ void st_b16(rsrc_t r, int off, bf16 v) {
+  __builtin_amdgcn_raw_buffer_store_b16(v, r, off, 0, kSC1);
+}
+
+#define GP(p) ((const void __attribute__((address_space(1)))*)(p))
+#define LP(p) ((void __attribute__((address_space(3)))*)(p))
+
+// Grid barrier number k of this launch (k >= 1), run by the whole
+// synchronising wave.  Per-XCD group counters feed one global counter; the
+// targets grow with k, so the counters are zeroed once per launch sequence.
+// Returns false after a timeout or when another workgroup timed out.
+__device__ bool grid_sync(const DecodeArgs& a, unsigned k) {
+  wait_vm<0>();   // this wave's coherent stores and atomics have completed
+  int ok = 1;
+  if ((threadIdx.x & 63) == 0) {
+    const unsigned G = gridDim.x, g = blockIdx.x & 7;
+    const unsigned ng = G < 8 ? G : 8;
+    const unsigned gsz = (G - g + 7) / 8;
+    const unsigned kk = a.bar_base + k;
+    const unsigned old = __hip_atomic_fetch_add(a.bar + 32 * (1 + g), 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (old == gsz * kk - 1) __hip_atomic_fetch_add(a.bar, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const long long t0 = wall_clock64();
+    while (__hip_atomic_load(a.bar, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < ng * kk) {
+      if (__hip_atomic_load(a.bar + kDecodeAbortWord, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ||
+          wall_clock64() - t0 > a.timeout_ticks) {
+        __hip_atomic_store(a.bar + kDecodeAbortWord, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        ok = 0;
+        break;
+      }
+      __builtin_amdgcn_s_sleep(1);
+    }
+  }
+  return __builtin_amdgcn_readfirstlane(ok) != 0;
+}
+
+// Barrier of the n workgroups of head h (number k of this launch), run by
+// the synchronising wave; same timeout and abort rules as grid_sync.
+__device__ bool head_sync(const DecodeArgs& a, int h, unsigned n, unsigned k) {
+  wait_vm<0>();
+  int ok = 1;
+  if ((threadIdx.x & 63) == 0) {
+    unsigned* ctr = a.bar + kDecodeHeadWord + 32 * h;
+    const unsigned target = n * (a.hbar_base + k);
+    __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const long long t0 = wall_clock64();
+    while (__hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
+      if (__hip_atomic_load(a.bar + kDecodeAbortWord, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ||
+          wall_clock64() - t0 > a.timeout_ticks) {
+        __hip_atomic_store(a.bar + kDecodeAbortWord, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        ok = 0;
+        break;
+      }
+      __builtin_amdgcn_s_sleep(1);
+    }
+  }
+  return __builtin_amdgcn_readfirstlane(ok) != 0;
+}
+
+// Staging of a step's input into LDS by the compute waves (threads 0..511;
+// the synchronising wave only joins the block barrier).  Their coherent
+// loads queue behind the ring in the memory counter, but the ring's loads
+// have landed during the grid barrier, and one round trip with 512 threads
+// beats several with one wave.
+//
+// act[0..n) = bf16(src * gain / rms(src)), src fp32 [n], n % 4 == 0,
+// n <= 8192; act[n..npad) = 0.
+__device__ __forceinline__ void stage_norm(rsrc_t src, const float* __restrict__ gain, int n, int npad, float eps,
+                                           bf16* act, float* wred) {
+  const int tid = threadIdx.x;
+  const bool cw = tid < kWaves * 64;
+  float4 y[4];
+  float ss = 0.f;
+  if (cw) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int c = tid + i * kWaves * 64;
+      if (c < n / 4) {
+        const float4 v = __builtin_bit_cast(float4, ld_b128(src, c * 16));
+        const float4 g = *(const float4*)(gain + c * 4);
+        ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+        y[i] = float4{v.x * g.x, v.y * g.y, v.z * g.z, v.w * g.w};
+      }
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) ss += __shfl_xor(ss, o);
+    if ((tid & 63) == 0) wred[tid >> 6] = ss;
+  }
+  __syncthreads();
+  if (cw) {
+    float tot = 0.f;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) tot += wred[w];
+    const float inv = 1.0f / sqrtf(tot / (float)n + eps);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int c = tid + i * kWaves * 64;
+      if (c < n / 4)
+        *(u16x4*)(act + c * 4) = u16x4{f2bf(y[i].x * inv), f2bf(y[i].y * inv), f2bf(y[i].z * inv), f2bf(y[i].w * inv)};
+    }
+    for (int e = n + tid; e < npad; e += kWaves * 64) act[e] = 0;
+  }
+}
+
+// act[0..n) = src bf16 [n] (n % 8 == 0, n <= 8 * 2048), act[n..npad) = 0.
+__device__ __forceinline__ void stage_copy(rsrc_t src, int n, int npad, bf16* act) {
+  const int tid = threadIdx.x;
+  if (tid >= kWaves * 64) return;
+  u32x4 v[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int c = tid + i * kWaves * 64;
+    if (c < n / 8) v[i] = ld_b128(src, c * 16);
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int c = tid + i * kWaves * 64;
+    if (c < n / 8) *(u32x4*)(act + c * 8) = v[i];
+  }
+  for (int e = n + tid; e < npad; e += kWaves * 64) act[e] = 0;
+}
+
+// Sum over the compute waves of the partials of block s (16 outputs),
+// in wave order; lane t < 16 gets output t.
+__device__ __forceinline__ float sum_partials(const float* red, int s, int t) {
+  float v = 0.f;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) v += red[(w * kDecodeMaxSeg + s) * 16 + t];
+  return v;
+}
+
+// Attention of head h for the single token at position pos, computed by each
+// of the head's workgroups in full (they share the head's cache lines in
+// one L2); the output (DH values, bf16) goes to oact in LDS.  The compute
+// waves issue their first loads of the cached keys before the first block
+// barrier; meanwhile the synchronising wave applies RoPE to the new q and k
+// and, when `append`, writes the new key and value into the caches (for
+// later passes).  Position pos itself is read from LDS.
+template <int DH>
+__device__ __forceinline__ void attn_head(int h, int pos, int d, int kv_pad, bool append, bool xl, bf16* lkc,
+                                          bf16* lvc, const float2* rp, rsrc_t r_qkv, float* qs, float* kn, float* vn,
+                                          float* wred, float* sc, bf16* oact) {
+  const int tid = threadIdx.x, lane = tid & 63, wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const bool syncw = wv == kWaves;
+  constexpr int half = DH / 2;
+  constexpr int NT = kWaves * 64;
+  constexpr int LPK = DH / 8, KPI = NT / LPK, U = 5;   // score phase: 8 dims per lane, U key rounds per batch
+  constexpr int CG = NT / DH, UV = 5;                  // value phase: CG chunk groups per dim, UV chunks per batch
+  const int n_keys = pos + 1, nchunk = (n_keys + 7) / 8;
+  const int last_cached = max(pos - 1, 0);
+  bf16* kbase = lkc + (size_t)h * kv_pad * DH;
+  bf16* vbase = lvc + (size_t)h * DH * kv_pad;
+  const rsrc_t r_k = rsrc(kbase, (size_t)kv_pad * DH * 2);
+  const rsrc_t r_v = rsrc(vbase, (size_t)kv_pad * DH * 2);
+  const int sub = tid % LPK, kg = tid / LPK;           // score phase: key slice, key of the round
+  const int koff = sub * 16;
+  const int dim = tid / CG, cg = tid % CG;             // value phase: dim, chunk group
+  const int voff = dim * kv_pad * 2;
+  u16x8 kv[U];
+  if (!syncw) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) kv[u] = ld_plain_b128(r_k, koff + min(u * KPI + kg, last_cached) * DH * 2);
+  } else {
+    for (int i = lane; i < half; i += 64) {
+      const float2 cs = rp[i];
+      const int qo = h * DH + i;
+      const float q0 = ld_f32_x(r_qkv, qo * 4, xl), q1 = ld_f32_x(r_qkv, (qo + half) * 4, xl);
+      const float k0 = ld_f32_x(r_qkv, (d + qo) * 4, xl), k1 = ld_f32_x(r_qkv, (d + qo + half) * 4, xl);
+      qs[i] = q0 * cs.x - q1 * cs.y;
+      qs[i + half] = q1 * cs.x + q0 * cs.y;
+      const bf16 ka = f2bf(k0 * cs.x - k1 * cs.y), kb = f2bf(k1 * cs.x + k0 * cs.y);
+      kn[i] = bf2f(ka);
+      kn[i + half] = bf2f(kb);
+      if (append) {
+        st_b16(r_k, (pos * DH + i) * 2, ka);
+        st_b16(r_k, (pos * DH + i + half) * 2, kb);
+      }
+    }
+    for (int i = lane; i < DH; i += 64) {
+      const bf16 v = f2bf(ld_f32_x(r_qkv, (2 * d + h * DH + i) * 4, xl));
+      vn[i] = bf2f(v);
+      if (append) st_b16(r_v, (i * kv_pad + pos) * 2, v);
+    }
+  }
+  __syncthreads();
+  // scores q . k_j / sqrt(d_h), j <= pos
+  float mx = -INFINITY;
+  if (!syncw) {
+    float qv[8], kv_new[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) { qv[i] = qs[sub * 8 + i]; kv_new[i] = kn[sub * 8 + i]; }
+    const float scale = 1.0f / sqrtf((float)DH);
+    for (int j0 = 0; j0 < n_keys; j0 += KPI * U) {
+      if (j0 > 0) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) kv[u] = ld_plain_b128(r_k, koff + min(j0 + u * KPI + kg, last_cached) * DH * 2);
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int j = j0 + u * KPI + kg;
+        float s = 0.f;
+        if (j == pos) {
+#pragma unroll
+          for (int i = 0; i < 8; ++i) s += qv[i] * kv_new[i];
+        } else {
+#pragma unroll
+          for (int i = 0; i < 8; ++i) s += qv[i] * bf2f(kv[u][i]);
+        }
+#pragma unroll
+        for (int x = LPK / 2; x > 0; x >>= 1) s += __shfl_xor(s, x);
+        s *= scale;
+        if (j < n_keys) {
+          if (sub == 0) sc[j] = s;
+          mx = fmaxf(mx, s);
+        }
+      }
+    }
+    for (int x = 32; x > 0; x >>= 1) mx = fmaxf(mx, __shfl_xor(mx, x));
+    if (lane == 0) wred[wv] = mx;
+  }
+  __syncthreads();
+  float sm = 0.f;
+  if (!syncw) {
+    mx = wred[0];
+#pragma unroll
+    for (int w = 1; w < kWaves; ++w) mx = fmaxf(mx, wred[w]);
+    for (int j = tid; j < n_keys; j += NT) {
+      const float p = __expf(sc[j] - mx);
+      sc[j] = p;
+      sm += p;
+    }
+    for (int x = 32; x > 0; x >>= 1) sm += __shfl_xor(sm, x);
+  }
+  __syncthreads();
+  if (!syncw) {
+    if (lane == 0) wred[8 + wv] = sm;
+    for (int j = n_keys + tid; j < nchunk * 8; j += NT) sc[j] = 0.f;   // pad the last 8-key chunk
+  }
+  __syncthreads();
+  if (!syncw) {
+    float tot = 0.f;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) tot += wred[8 + w];
+    const float vnew = vn[dim];
+    float acc = 0.f;
+    u16x8 vv[UV];
+    for (int c0 = 0; c0 < nchunk; c0 += CG * UV) {
+#pragma unroll
+      for (int u = 0; u < UV; ++u) vv[u] = ld_plain_b128(r_v, voff + min(c0 + cg + CG * u, nchunk - 1) * 16);
+#pragma unroll
+      for (int u = 0; u < UV; ++u) {
+        const int c = c0 + cg + CG * u;
+        if (c < nchunk) {
+          const float4 p0 = *(const float4*)(sc + c * 8), p1 = *(const float4*)(sc + c * 8 + 4);
+          const float pp[8] = {p0.x, p0.y, p0.z, p0.w, p1.x, p1.y, p1.z, p1.w};
+#pragma unroll
+          for (int e = 0; e < 8; ++e) acc += pp[e] * (c * 8 + e == pos ? vnew : bf2f(vv[u][e]));
+        }
+      }
+    }
+#pragma unroll
+    for (int x = CG / 2; x > 0; x >>= 1) acc += __shfl_xor(acc, x);
+    if (cg == 0) oact[dim] = f2bf(acc / tot);
+  }
+  __syncthreads();
+}
+
+}  // namespace
+
+template <int DH>
+__global__ __launch_bounds__(kThreads) void k_decode_pass(const DecodeArgs a) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
+  u32x4* ring = reinterpret_cast<u32x4*>(lds);                  // [kWaves][kRing][64]
+  bf16* act = reinterpret_cast<bf16*>(lds + kRingBytes);        // staged activation; step 2: head output
+  float* sc = reinterpret_cast<float*>(lds + kRingBytes + kScoreOffset);   // step 2: attention scores
+  float* red = reinterpret_cast<float*>(lds + kRingBytes + a.act_bytes);   // [kWaves][kDecodeMaxSeg][16]
+  __shared__ float qs[DH], kn[DH], vn[DH], wred[16];
+  __shared__ float2 rp[DH / 2];
+  __shared__ int s_ok;
+
+  const int tid = threadIdx.x, lane = tid & 63, wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const bool syncw = wv == kWaves;
+  const int G = gridDim.x, gi = blockIdx.x;
+  const int d = a.d, F = a.F, H = a.H;
+  const int nq = d / 16, nf = F / 16;
+  constexpr int KH = DH / 32;   // k fragments of one head's columns
+
+  // This workgroup's blocks per step and this wave's part of them.
+  const int w8 = syncw ? 0 : wv;
+  const int k0d = w8 * a.KBd / kWaves, nkd = (w8 + 1) * a.KBd / kWaves - k0d;
+  const int k0f = w8 * a.KBf / kWaves, nkf = (w8 + 1) * a.KBf / kWaves - k0f;
+  // head ah, slice asl of nsl: this workgroup's share of steps 1 and 2
+  const int nsl = min(G / H, nq);
+  const int ah = gi % H, asl = gi / H;
+  const bool attn = asl < nsl;
+  // step 1: blocks [qb0, qb0 + nbm) of each of q, k, v within head ah's rows (k split)
+  constexpr int BH = DH / 16;
+  const int qb0 = attn ? ah * BH + asl * BH / nsl : 0, nbm = attn ? (asl + 1) * BH / nsl - asl * BH / nsl : 0;
+  const int nseg0 = 3 * nbm;
+  const int sb0 = attn ? asl * nq / nsl : 0, nsb = attn ? (asl + 1) * nq / nsl - sb0 : 0;
+  const int ob0w = w8 * nsb / kWaves, nseg_o = syncw ? 0 : (w8 + 1) * nsb / kWaves - ob0w;
+  const int gp0 = gi * nf / G, nseg2 = 2 * ((gi + 1) * nf / G - gp0);     // gate, up, gate, up, ...
+  const int db0 = gi * nq / G, nseg3 = (gi + 1) * nq / G - db0;           // down blocks (k split)
+  const int nsegs = nseg0 + nseg_o + nseg2 + nseg3;   // segments of one layer, in stream order
+
+  const rsrc_t r_x = rsrc(a.x, (size_t)d * 4), r_r = rsrc(a.r, (size_t)d * 4);
+  const rsrc_t r_qkv = rsrc(a.qkv, (size_t)3 * d * 4);
+  const rsrc_t r_act = rsrc(a.act, (size_t)F * 2);
+
+  // First fragment of segment sg of layer 0 for this wave (offset from wq,
+  // in bf16x8 units) and its length.  Everything here is wave-uniform and
+  // kept in locals: selects between kernel-argument fields would be turned
+  // into indexed private memory.
+  const bf16x8* const wq = a.wq;
+  const long long off_o = a.wo - a.wq, off_g = a.wg - a.wq, off_d = a.wd - a.wq;
+  const long long qkv_stride = (long long)a.qkv_stride, gu_stride = (long long)a.gu_stride;
+  const long long KBd = a.KBd, KBf = a.KBf;
+  auto seg_off = [=](int sg) -> long long {
+    if (sg < nseg0) {
+      const int m = sg / nbm, rb = qb0 + sg - m * nbm;
+      return m * qkv_stride + (rb * KBd + k0d) * 64;
+    }
+    sg -= nseg0;
+    if (sg < nseg_o) return off_o + ((sb0 + ob0w + sg) * KBd + ah * KH) * 64;
+    sg -= nseg_o;
+    if (sg < nseg2) return off_g + (sg & 1) * gu_stride + ((gp0 + (sg >> 1)) * KBd + k0d) * 64;
+    sg -= nseg2;
+    return off_d + ((db0 + sg) * KBf + k0f) * 64;
+  };
+  // (arithmetic rather than a select chain, which becomes an indexed table in private memory)
+  auto seg_len = [=](int sg) -> int {
+    const int in_o = (sg >= nseg0) & (sg < nseg0 + nseg_o), in_d = sg >= nseg0 + nseg_o + nseg2;
+    return nkd + in_o * (KH - nkd) + in_d * (nkf - nkd);
+  };
+
+  // Producer state of a compute wave: layer, segment, fragments left in the
+  // segment, next fragment (layer 0 address plus layer * layer_stride).
+  int p_l = 0, p_sg = 0, p_left = 0;
+  const bf16x8* p_ptr = nullptr;
+  const bf16x8* last = nullptr;
+  int slot = 0;
+  u32x4* myring = ring + wv * kRing * 64;
+  const bool streams = !syncw && (nseg0 + nseg2) * nkd + nseg_o * KH + nseg3 * nkf > 0;
+  const long long layer_stride = (long long)a.layer_stride;
+  // moves to the next non-empty segment at or after (p_l, p_sg)
+  auto settle = [&]() {
+    while (p_l < a.L) {
+      const int len = seg_len(p_sg);
+      if (len > 0) {
+        p_ptr = wq + seg_off(p_sg) + p_l * layer_stride;
+        p_left = len;
+        return;
+      }
+      if (++p_sg == nsegs) { p_sg = 0; ++p_l; }
+    }
+  };
+  auto issue = [&](int sl) {
+    const bf16x8* ptr = last;   // past the end: re-read the final fragment (in bounds, cached)
+    if (p_l < a.L) {
+      ptr = p_ptr;
+      last = ptr;
+      p_ptr += 64;
+      if (--p_left == 0) {
+        if (++p_sg == nsegs) { p_sg = 0; ++p_l; }
+        settle();
+      }
+    }
+    __builtin_amdgcn_global_load_lds(GP(ptr + lane), LP(myring + sl * 64), 16, 0, 0);
+  };
+  if (streams) {
+    settle();
+#pragma unroll 1
+    for (int f = 0; f < kRing; ++f) issue(f);
+  }
+
+  // Compute waves: nseg blocks of nk k steps each over the staged activation
+  // (k steps k0.. of act); partial sums to red[wave][block].
+  auto run_step = [&](int nseg, int nk, int k0) {
+    const bf16* abase = act + (lane >> 4) * 8;
+    const bool row0 = (lane & 15) == 0;
+    for (int s = 0; s < nseg; ++s) {
+      floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+      for (int j = 0; j < nk; ++j) {
+        wait_vm<kRing - 1>();
+        const u32x4 wf = myring[slot * 64 + lane];
+        u32x4 xf = *(const u32x4*)(abase + (k0 + j) * 32);
+        if (!row0) xf = u32x4{0u, 0u, 0u, 0u};
+        acc = mfma16(__builtin_bit_cast(bf16x8, xf), __builtin_bit_cast(bf16x8, wf), acc);
+        wait_lgkm0();
+        issue(slot);
+        slot = slot + 1 == kRing ? 0 : slot + 1;
+      }
+      if (lane < 16) red[(wv * kDecodeMaxSeg + s) * 16 + lane] = acc[0];
+    }
+    if (nk == 0)   // a wave without k steps contributes zeros
+      for (int s = lane; s < nseg * 16; s += 64) red[wv * kDecodeMaxSeg * 16 + s] = 0.f;
+  };
+
+  // Synchronising wave: grid barrier; every wave then reads the outcome.
+  unsigned nbar = 0;
+  auto barrier = [&]() -> bool {
+    if (syncw) {
+      const bool ok = grid_sync(a, ++nbar);
+      if (lane == 0) s_ok = ok;
+    }
+    __syncthreads();
+    return s_ok != 0;
+  };
+
+  // Prologue: r = x for the first layer's step 2; check that this workgroup
+  // runs on XCD blockIdx % 8, which makes each head's workgroups share one L2.
+  if (syncw) {
+    for (int i = lane; i < DH / 2; i += 64) rp[i] = a.rope[(size_t)a.pos * (DH / 2) + i];
+    for (int e = db0 * 16 + lane; e < (db0 + nseg3) * 16; e += 64) st_f32(r_r, e * 4, ld_f32(r_x, e * 4));
+    if (lane == 0 && (__builtin_amdgcn_s_getreg((31 << 11) | 20) & 0xf) != (unsigned)(gi & 7))
+      __hip_atomic_store(a.bar + kDecodeXccWord, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  bool run = barrier();
+  const bool xl = H % 8 == 0 &&
+                  __hip_atomic_load(a.bar + kDecodeXccWord, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0u;
+  unsigned nhbar = 0;
+
+  const float* gains = a.gains;
+  for (int l = 0; l < a.L && run; ++l) {
+    bf16* const lkc = a.kc + (size_t)l * a.kv_layer_elems;
+    bf16* const lvc = a.vc + (size_t)l * a.kv_layer_elems;
+    // ---------------- 1. QKV projection (head ah's rows, published to the head's workgroups)
+    stage_norm(r_x, gains + (size_t)l * 2 * d, d, a.KBd * 32, a.eps, act, wred);
+    __syncthreads();
+    if (!syncw) run_step(nseg0, nkd, k0d);
+    __syncthreads();
+    if (attn) {
+      if (syncw) {
+        for (int s0 = 0; s0 < nseg0; s0 += 4) {
+          const int s = s0 + (lane >> 4), t = lane & 15;
+          if (s < nseg0) {
+            const int m = s / nbm, rb = qb0 + s - m * nbm;
+            st_f32_x(r_qkv, (m * d + rb * 16 + t) * 4, sum_partials(red, s, t), xl);
+          }
+        }
+        const bool ok = head_sync(a, ah, (unsigned)nsl, ++nhbar);
+        if (lane == 0) s_ok = ok;
+      }
+      __syncthreads();
+      if (!s_ok) break;
+
+      // ---------------- 2. attention of head ah, times W_o's slice asl of head-ah columns
+      attn_head<DH>(ah, a.pos, d, a.kv_pad, asl == 0, xl, lkc, lvc, rp, r_qkv, qs, kn, vn, wred, sc, act);
+      if (!syncw) run_step(nseg_o, KH, 0);
+      __syncthreads();
+      if (syncw) {
+        for (int w = 0; w < kWaves; ++w) {
+          const int wb0 = w * nsb / kWaves, wn = (w + 1) * nsb / kWaves - wb0;
+          for (int s0 = 0; s0 < wn; s0 += 4) {
+            const int s = s0 + (lane >> 4), t = lane & 15;
+            if (s < wn)
+              __hip_atomic_fetch_add(a.r + (sb0 + wb0 + s) * 16 + t, red[(w * kDecodeMaxSeg + s) * 16 + t],
+                                     __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          }
+        }
+      }
+    }
+    if (!barrier()) break;
+
+    // ---------------- 3. gate/up projection + SwiGLU
+    stage_norm(r_r, gains + (size_t)l * 2 * d + d, d, a.KBd * 32, a.eps, act, wred);
+    __syncthreads();
+    if (!syncw) run_step(nseg2, nkd, k0d);
+    __syncthreads();
+    if (syncw) {
+      for (int s0 = 0; s0 < nseg2 / 2; s0 += 4) {
+        const int pr = s0 + (lane >> 4), t = lane & 15;
+        if (pr < nseg2 / 2) {
+          const float g = sum_partials(red, 2 * pr, t), u = sum_partials(red, 2 * pr + 1, t);
+          st_b16(r_act, ((gp0 + pr) * 16 + t) * 2, f2bf(g / (1.0f + __expf(-g)) * u));
+        }
+      }
+    }
+    if (!barrier()) break;
+
+    // ---------------- 4. down projection + residual; r = x for the next layer's step 2
+    stage_copy(r_act, F, a.KBf * 32, act);
+    __syncthreads();
+    if (!syncw) run_step(nseg3, nkf, k0f);
+    __syncthreads();
+    if (syncw) {
+      for (int s0 = 0; s0 < nseg3; s0 += 4) {
+        const int s = s0 + (lane >> 4), t = lane & 15;
+        if (s < nseg3) {
+          const int e = (db0 + s) * 16 + t;
+          const float xn = ld_f32(r_r, e * 4) + sum_partials(red, s, t);
+          st_f32(r_x, e * 4, xn);
+          st_f32(r_r, e * 4, xn);
+        }
+      }
+    }
+    if (!barrier()) break;
+  }
+  wait_vm<0>();   // direct-to-LDS loads must land before the workgroup ends
+}
+
+size_t decode_pass_lds_bytes(int act_bytes) { return (size_t)kRingBytes + act_bytes + kRedBytes; }
+
+int decode_pass_threads() { return kThreads; }
+
+int decode_pass_score_offset() { return kScoreOffset; }
+
+const void* decode_pass_kernel(int head_dim) {
+  if (head_dim == 128) return reinterpret_cast<const void*>(&k_decode_pass<128>);
+  if (head_dim == 64) return reinterpret_cast<const void*>(&k_decode_pass<64>);
+  return nullptr;
+}
+
+hipError_t launch_decode_pass(const DecodeArgs& a, int n_wg, hipStream_t s) {
+  const void* f = decode_pass_kernel(a.head_dim);
+  if (!f) return hipErrorInvalidValue;
+  DecodeArgs args = a;
+  void* params[] = {&args};
+  return hipLaunchCooperativeKernel(f, dim3(n_wg), dim3(kThreads), params,
+                                    (unsigned)decode_pass_lds_bytes(a.act_bytes), s);
+}
+
+}  // namespace gvc

@@ -212,49 +212,72 @@ __device__ __forceinline__ Top2 merge2(const Top2& a, const Top2& b) {
   return r;
 }
 
-__global__ __launch_bounds__(256) void k_logits_reduce(const float* __restrict__ logits, int V, int bin_lo,
-                                                       int full_vocab, int* __restrict__ tok_out,
-                                                       float* __restrict__ margin_out, int out_stride, int out_col,
-                                                       int rows_per_ep) {
-  __shared__ float s_f[256];
-  __shared__ Top2 s_t[256];
-  const int r = blockIdx.x;
-  const float* z = logits + (size_t)r * V;
+__device__ __forceinline__ Top2 shfl_top2(const Top2& t, int m) {
+  return Top2{__shfl_xor(t.v1, m), __shfl_xor(t.i1, m), __shfl_xor(t.v2, m), __shfl_xor(t.i2, m)};
+}
+
+// Running (max, sum of exp(z - max)) pair; a term at -inf contributes 0.
+__device__ __forceinline__ void lse_add(float& mx, float& sum, float v) {
+  if (v > mx) {
+    sum = sum * __expf(mx - v) + 1.f;
+    mx = v;
+  } else if (v != -INFINITY) {
+    sum += __expf(v - mx);
+  }
+}
+
+__device__ __forceinline__ void lse_merge(float& mx, float& sum, float mo, float so) {
+  const float m = fmaxf(mx, mo);
+  if (m == -INFINITY) return;
+  sum = (mx == -INFINITY ? 0.f : sum * __expf(mx - m)) + (mo == -INFINITY ? 0.f : so * __expf(mo - m));
+  mx = m;
+}
+
+constexpr int kReduceThreads = 1024;
+
+// One pass over the row: every thread keeps its own running maximum, sum of
+// exponentials and bin top-2 over a strided set of float4 columns; the
+// partial results are merged across the wave, then across the 16 waves.
+__global__ __launch_bounds__(kReduceThreads) void k_logits_reduce(const float* __restrict__ logits, int V,
+                                                                  int bin_lo, int full_vocab, int* __restrict__ tok_out,
+                                                                  float* __restrict__ margin_out, int out_stride,
+                                                                  int out_col, int rows_per_ep) {
+  __shared__ float s_m[kReduceThreads / 64], s_s[kReduceThreads / 64];
+  __shared__ Top2 s_t[kReduceThreads / 64];
+  const int r = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const float4* z4 = (const float4*)(logits + (size_t)r * V);
   const int lo = full_vocab ? 0 : bin_lo;
   const float NEG = -INFINITY;
-  float mx = NEG;
+  float mx = NEG, sum = 0.f;
   Top2 t = {NEG, 0x7fffffff, NEG, 0x7fffffff};
-  for (int i = lo + threadIdx.x; i < V; i += 256) {
-    const float v = z[i];
-    mx = fmaxf(mx, v);
-    if (i >= bin_lo) {
-      Top2 c = {v, i, NEG, 0x7fffffff};
-      t = merge2(t, c);
+  for (int c = tid; c < V / 4; c += kReduceThreads) {
+    const float4 q = z4[c];
+    const float v[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int i = c * 4 + j;
+      if (i >= lo) lse_add(mx, sum, v[j]);
+      if (i >= bin_lo) t = merge2(t, Top2{v[j], i, NEG, 0x7fffffff});
     }
   }
-  s_f[threadIdx.x] = mx;
-  s_t[threadIdx.x] = t;
+#pragma unroll
+  for (int m = 1; m < 64; m <<= 1) {
+    lse_merge(mx, sum, __shfl_xor(mx, m), __shfl_xor(sum, m));
+    t = merge2(t, shfl_top2(t, m));
+  }
+  if (lane == 0) {
+    s_m[wv] = mx;
+    s_s[wv] = sum;
+    s_t[wv] = t;
+  }
   __syncthreads();
-  for (int o = 128; o > 0; o >>= 1) {
-    if (threadIdx.x < o) {
-      s_f[threadIdx.x] = fmaxf(s_f[threadIdx.x], s_f[threadIdx.x + o]);
-      s_t[threadIdx.x] = merge2(s_t[threadIdx.x], s_t[threadIdx.x + o]);
+  if (tid == 0) {
+    float M = s_m[0], S = s_s[0];
+    Top2 best = s_t[0];
+    for (int w = 1; w < kReduceThreads / 64; ++w) {
+      lse_merge(M, S, s_m[w], s_s[w]);
+      best = merge2(best, s_t[w]);
     }
-    __syncthreads();
-  }
-  const float M = s_f[0];
-  const Top2 best = s_t[0];
-  __syncthreads();
-  float sum = 0.f;
-  for (int i = lo + threadIdx.x; i < V; i += 256) sum += __expf(z[i] - M);
-  s_f[threadIdx.x] = sum;
-  __syncthreads();
-  for (int o = 128; o > 0; o >>= 1) {
-    if (threadIdx.x < o) s_f[threadIdx.x] += s_f[threadIdx.x + o];
-    __syncthreads();
-  }
-  if (threadIdx.x == 0) {
-    const float S = s_f[0];
     const float m = (__expf(best.v1 - M) - __expf(best.v2 - M)) / S;
     const int o = (r / rows_per_ep) * out_stride + out_col + r % rows_per_ep;
     tok_out[o] = best.i1;
@@ -346,7 +369,7 @@ hipError_t launch_embed_tokens(const bf16* embed, const int* tokens, int tok_str
 
 hipError_t launch_logits_reduce(const float* logits, int rows, int V, int bin_lo, int full_vocab, int* tok_out,
                                 float* margin_out, int out_stride, int out_col, int rows_per_ep, hipStream_t s) {
-  hipLaunchKernelGGL(k_logits_reduce, dim3(rows), dim3(256), 0, s, logits, V, bin_lo, full_vocab, tok_out,
+  hipLaunchKernelGGL(k_logits_reduce, dim3(rows), dim3(kReduceThreads), 0, s, logits, V, bin_lo, full_vocab, tok_out,
                      margin_out, out_stride, out_col, rows_per_ep);
   return hipGetLastError();
 }

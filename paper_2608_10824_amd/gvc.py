@@ -15,7 +15,8 @@ REDUCE_MEAN, REDUCE_MIN = 0, 1
 STATE_H, STATE_K, STATE_V, STATE_HEAD_LOGITS, STATE_VALID, STATE_ROWS, STATE_MARGINS = range(7)
 
 (K_DECODE_QKV, K_DECODE_ATTN, K_DECODE_O, K_DECODE_GU, K_DECODE_DOWN, K_DECODE_HEAD, K_PREFILL_QKV,
- K_PREFILL_ATTN, K_PREFILL_O, K_PREFILL_GU, K_PREFILL_DOWN, K_PREFILL_HEAD, K_EMBED, K_NORM, K_SELECT) = range(15)
+ K_PREFILL_ATTN, K_PREFILL_O, K_PREFILL_GU, K_PREFILL_DOWN, K_PREFILL_HEAD, K_EMBED, K_NORM, K_SELECT,
+ K_DECODE_PASS) = range(16)
 
 EXPORTED = ("gvc_sizes", "gvc_init_cache", "gvc_select_static", "gvc_step_prefill", "gvc_decode_actions",
             "gvc_margin_gate", "gvc_invalidate", "gvc_read_state", "gvc_state_item_bytes", "gvc_profile_begin",

@@ -172,3 +172,36 @@ def test_largest_frame_selection():
     assert np.array_equal(mask[0].cpu().numpy().astype(bool), m)
     assert mask[0].sum(dim=1).cpu().tolist() == [420, 180]
     s.close()
+
+
+@pytest.mark.parametrize("cfg_fn", [synth.config_c1, synth.config_mid])
+def test_decode_pass_matches_per_step_launches(cfg_fn, monkeypatch):
+    """The single-launch decode pass (one episode) and the per-step launches
+    compute the same passes: with the same fed-back tokens their logits agree
+    to the bf16 tolerance, and the single-launch path is the one that ran."""
+    from paper_2608_10824_amd import gvc
+    cfg = cfg_fn()
+    w = synth.model_weights(cfg)
+    si = synth.step_inputs(cfg, cfg.n_patches // 2)
+    o = OracleVLA(cfg, w)
+    o.step_prefill(si["frame_prev"].numpy(), si["text_ids"].numpy())
+    tok_o, _, lg_o = o.decode_actions()
+    forced = torch.from_numpy(tok_o.astype(np.int32)).to(DEV)
+    got = {}
+    for mode in ("legacy", "single"):
+        if mode == "legacy":
+            monkeypatch.setenv("GVC_DECODE", "legacy")
+        else:
+            monkeypatch.delenv("GVC_DECODE", raising=False)
+        s = _session(cfg, w)
+        s.step_prefill(si["frame_prev"].to(DEV), si["text_ids"].to(DEV))
+        gvc.profile_begin(s.ctx, gvc.K_DECODE_PASS, 64)
+        _, _, lg = s.decode_actions(logits=True, forced_tokens=forced)
+        _, n = gvc.profile_end(s.ctx)
+        assert n == (0 if mode == "legacy" else cfg.n_decode - 1)
+        s.margin_gate()   # surfaces a barrier timeout of the single-launch path
+        got[mode] = lg.cpu().numpy()
+        s.close()
+    assert rel_err(got["single"], lg_o) <= TOL
+    assert rel_err(got["legacy"], lg_o) <= TOL
+    assert rel_err(got["single"], got["legacy"]) <= TOL
