@@ -223,14 +223,15 @@ namespace {
 // k range 4 ways (8 for long k ranges with few units).  Measured on the 7B
 // prompt pass: more concurrent weight streams beat reading the weights once
 // per 160 rows (two token groups sharing a k share were 10-50% slower), so
-// each token tile streams the weights itself.  GVC_FORCE_SPLITS (4 or 8)
-// overrides the wave count (testing).
+// each token tile streams the weights itself.  8 waves for long k ranges or
+// at most 128 units (7B output projection: 24.5 instead of 28 µs).
+// GVC_FORCE_SPLITS (4 or 8) overrides the wave count (testing).
 void tile_gemm(GemmArgs& a, int M, int force_splits) {
   a.M = M;
   a.mblocks = (M + 15) / 16;
   a.tgroups = 1;
   a.mtiles = (a.mblocks + kMaxNT - 1) / kMaxNT;
-  int KW = (a.n_pairs < 256 && a.KB > 200) ? 8 : 4;
+  int KW = (a.n_pairs < 256 && (a.KB > 200 || a.n_pairs <= 128)) ? 8 : 4;
   if (force_splits == 4 || force_splits == 8) KW = force_splits;
   a.splits = KW;
   a.kb_per_split = (a.KB + KW - 1) / KW;
