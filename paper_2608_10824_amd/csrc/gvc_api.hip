@@ -514,6 +514,12 @@ bool setup_persist(gvc_ctx* c) {
   a.L = p.L; a.d = d; a.F = F; a.H = p.H; a.head_dim = p.dh; a.KBd = p.KBd; a.KBf = p.KBf; a.kv_pad = p.kv_pad;
   a.act_bytes = act;
   a.eps = p.d.rms_eps;
+  // Weights are read once per pass: marked non-temporal they stop evicting
+  // the activations, barrier words and key/value lines from L2 (7B: 2.93
+  // instead of 3.09 ms per pass; warming the keys and values adds 1%).
+  // GVC_DECODE_FLAGS overrides the flags (measurement).
+  a.flags = kDecodeNtWeights | kDecodeWarmKv;
+  if (const char* e = getenv("GVC_DECODE_FLAGS")) a.flags = atoi(e) & (kDecodeNtWeights | kDecodeWarmKv);
   c->persist_wg = G;
   return true;
 }

@@ -133,7 +133,10 @@ struct DecodeArgs {
   long long timeout_ticks;     // barrier wait limit in wall-clock ticks (100 MHz)
   int L, d, F, H, head_dim, KBd, KBf, kv_pad, pos, act_bytes;
   float eps;
+  int flags;                   // kDecodeNtWeights | kDecodeWarmKv
 };
+constexpr int kDecodeNtWeights = 1;   // weight loads marked non-temporal
+constexpr int kDecodeWarmKv = 2;      // step 1 pulls the head's cached keys and values into L2
 
 // ------------------------------------------------------------------ launchers
 // All launchers enqueue on `s` and return hipGetLastError().

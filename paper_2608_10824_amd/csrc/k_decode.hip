@@ -9,7 +9,9 @@
 // its share of every matrix of every layer, in order, into a ring of 16
 // one-KiB fragments in LDS with direct global->LDS loads, and the ring keeps
 // running across the grid-wide barriers that separate the steps.  Only the
-// multiply waits for the activation vector.
+// multiply waits for the activation vector.  The weight loads are marked
+// non-temporal, so the streamed weights do not push the data the workgroups
+// exchange, or the keys and values, out of L2.
 //
 // Steps of a layer (one grid barrier after each):
 //  1. QKV projection of RMSNorm(x); the raw q, k, v are published.
@@ -371,6 +373,7 @@ __global__ __launch_bounds__(kThreads) void k_decode_pass(const DecodeArgs a) {
   __shared__ float qs[DH], kn[DH], vn[DH], wred[16];
   __shared__ float2 rp[DH / 2];
   __shared__ int s_ok;
+  __shared__ u32x4 sink[64];   // destination of the cache-warming loads
 
   const int tid = threadIdx.x, lane = tid & 63, wv = __builtin_amdgcn_readfirstlane(tid >> 6);
   const bool syncw = wv == kWaves;
@@ -434,6 +437,7 @@ __global__ __launch_bounds__(kThreads) void k_decode_pass(const DecodeArgs a) {
   const bf16x8* last = nullptr;
   int slot = 0;
   u32x4* myring = ring + wv * kRing * 64;
+  const bool nt_w = (a.flags & kDecodeNtWeights) != 0;
   const bool streams = !syncw && (nseg0 + nseg2) * nkd + nseg_o * KH + nseg3 * nkf > 0;
   const long long layer_stride = (long long)a.layer_stride;
   // moves to the next non-empty segment at or after (p_l, p_sg)
@@ -459,7 +463,10 @@ __global__ __launch_bounds__(kThreads) void k_decode_pass(const DecodeArgs a) {
         settle();
       }
     }
-    __builtin_amdgcn_global_load_lds(GP(ptr + lane), LP(myring + sl * 64), 16, 0, 0);
+    if (nt_w)
+      __builtin_amdgcn_global_load_lds(GP(ptr + lane), LP(myring + sl * 64), 16, 0, 2);
+    else
+      __builtin_amdgcn_global_load_lds(GP(ptr + lane), LP(myring + sl * 64), 16, 0, 0);
   };
   if (streams) {
     settle();
@@ -522,6 +529,18 @@ __global__ __launch_bounds__(kThreads) void k_decode_pass(const DecodeArgs a) {
     stage_norm(r_x, gains + (size_t)l * 2 * d, d, a.KBd * 32, a.eps, act, wred);
     __syncthreads();
     if (!syncw) run_step(nseg0, nkd, k0d);
+    if (syncw && attn && (a.flags & kDecodeWarmKv)) {
+      // share asl of head ah's cached keys (rows of DH) and values (dims of
+      // kv_pad), read once now so that step 2 finds them in this XCD's L2
+      const char* kb = reinterpret_cast<const char*>(lkc + (size_t)ah * a.kv_pad * DH);
+      const char* vb = reinterpret_cast<const char*>(lvc + (size_t)ah * DH * a.kv_pad);
+      const int r0 = asl * a.pos / nsl, r1 = (asl + 1) * a.pos / nsl;
+      for (int o = r0 * DH * 2 + lane * 16; o < r1 * DH * 2; o += 1024)
+        __builtin_amdgcn_global_load_lds(GP(kb + o), LP(sink), 16, 0, 0);
+      for (int dm = asl * DH / nsl; dm < (asl + 1) * DH / nsl; ++dm)
+        for (int o = lane * 16; o < a.pos * 2; o += 1024)
+          __builtin_amdgcn_global_load_lds(GP(vb + (size_t)dm * a.kv_pad * 2 + o), LP(sink), 16, 0, 0);
+    }
     __syncthreads();
     if (attn) {
       if (syncw) {
