@@ -102,6 +102,43 @@ __device__ __forceinline__ void st_b16(rsrc_t r, int off, bf16 v) {
 #define GP(p) ((const void __attribute__((address_space(1)))*)(p))
 #define LP(p) ((void __attribute__((address_space(3)))*)(p))
 
+// Cross-lane reductions on DPP row operations (a few cycles each) instead of
+// LDS permutes.  dpp_f<C>: v of the lane that DPP control C selects.
+template <int C>
+__device__ __forceinline__ float dpp_f(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), C, 0xF, 0xF, false));
+}
+constexpr int kDppXor1 = 0xB1;        // quad_perm [1, 0, 3, 2]
+constexpr int kDppXor2 = 0x4E;        // quad_perm [2, 3, 0, 1]
+constexpr int kDppHalfMirror = 0x141; // lane i of 8 <- lane 7 - i: the other quad, once quads agree
+constexpr int kDppMirror = 0x140;     // lane i of 16 <- lane 15 - i: the other half, once halves agree
+// Sum over aligned groups of N lanes (N = 1, 2, 4, 8, 16); every lane of a
+// group ends with the same value.
+template <int N>
+__device__ __forceinline__ float group_sum(float v) {
+  static_assert(N == 1 || N == 2 || N == 4 || N == 8 || N == 16, "group size");
+  if constexpr (N >= 2) v += dpp_f<kDppXor1>(v);
+  if constexpr (N >= 4) v += dpp_f<kDppXor2>(v);
+  if constexpr (N >= 8) v += dpp_f<kDppHalfMirror>(v);
+  if constexpr (N >= 16) v += dpp_f<kDppMirror>(v);
+  return v;
+}
+__device__ __forceinline__ float lane_f(float v, int l) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), l));
+}
+// Sum and maximum over the whole wave (all lanes active), wave-uniform.
+__device__ __forceinline__ float wave_sum(float v) {
+  v = group_sum<16>(v);
+  return (lane_f(v, 0) + lane_f(v, 16)) + (lane_f(v, 32) + lane_f(v, 48));
+}
+__device__ __forceinline__ float wave_max(float v) {
+  v = fmaxf(v, dpp_f<kDppXor1>(v));
+  v = fmaxf(v, dpp_f<kDppXor2>(v));
+  v = fmaxf(v, dpp_f<kDppHalfMirror>(v));
+  v = fmaxf(v, dpp_f<kDppMirror>(v));
+  return fmaxf(fmaxf(lane_f(v, 0), lane_f(v, 16)), fmaxf(lane_f(v, 32), lane_f(v, 48)));
+}
+
 // Grid barrier number k of this launch (k >= 1), run by the whole
 // synchronising wave.  Per-XCD group counters feed one global counter; the
 // targets grow with k, so the counters are zeroed once per launch sequence.
@@ -178,8 +215,7 @@ __device__ __forceinline__ void stage_norm(rsrc_t src, const float* __restrict__
         y[i] = float4{v.x * g.x, v.y * g.y, v.z * g.z, v.w * g.w};
       }
     }
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) ss += __shfl_xor(ss, o);
+ss = wave_sum(ss);
     if ((tid & 63) == 0) wred[tid >> 6] = ss;
   }
   __syncthreads();
@@ -231,7 +267,10 @@ __device__ __forceinline__ float sum_partials(const float* red, int s, int t) {
 // waves issue their first loads of the cached keys before the first block
 // barrier; meanwhile the synchronising wave applies RoPE to the new q and k
 // and, when `append`, writes the new key and value into the caches (for
-// later passes).  Position pos itself is read from LDS.
+// later passes).  Position pos itself is read from LDS.  A key (value)
+// register is reloaded with the next batch's key (value) as soon as it has
+// been used, and the first values are loaded right after the scores, so the
+// load round trips overlap the arithmetic and the block barriers.
 template <int DH>
 __device__ __forceinline__ void attn_head(int h, int pos, int d, int kv_pad, bool append, bool xl, bf16* lkc,
                                           bf16* lvc, const float2* rp, rsrc_t r_qkv, float* qs, float* kn, float* vn,
@@ -252,30 +291,48 @@ __device__ __forceinline__ void attn_head(int h, int pos, int d, int kv_pad, boo
   const int koff = sub * 16;
   const int dim = tid / CG, cg = tid % CG;             // value phase: dim, chunk group
   const int voff = dim * kv_pad * 2;
-  u16x8 kv[U];
+  u16x8 kv[U], vv[UV];
   if (!syncw) {
 #pragma unroll
     for (int u = 0; u < U; ++u) kv[u] = ld_plain_b128(r_k, koff + min(u * KPI + kg, last_cached) * DH * 2);
   } else {
-    for (int i = lane; i < half; i += 64) {
-      const float2 cs = rp[i];
-      const int qo = h * DH + i;
-      const float q0 = ld_f32_x(r_qkv, qo * 4, xl), q1 = ld_f32_x(r_qkv, (qo + half) * 4, xl);
-      const float k0 = ld_f32_x(r_qkv, (d + qo) * 4, xl), k1 = ld_f32_x(r_qkv, (d + qo + half) * 4, xl);
-      qs[i] = q0 * cs.x - q1 * cs.y;
-      qs[i + half] = q1 * cs.x + q0 * cs.y;
-      const bf16 ka = f2bf(k0 * cs.x - k1 * cs.y), kb = f2bf(k1 * cs.x + k0 * cs.y);
-      kn[i] = bf2f(ka);
-      kn[i + half] = bf2f(kb);
-      if (append) {
-        st_b16(r_k, (pos * DH + i) * 2, ka);
-        st_b16(r_k, (pos * DH + i + half) * 2, kb);
+    // every load first (one round trip), then RoPE and the appends
+    constexpr int NH = (half + 63) / 64, NV = (DH + 63) / 64;
+    float q0[NH], q1[NH], k0[NH], k1[NH], vr[NV];
+#pragma unroll
+    for (int n = 0; n < NH; ++n) {
+      const int qo = h * DH + min(lane + 64 * n, half - 1);
+      q0[n] = ld_f32_x(r_qkv, qo * 4, xl);
+      q1[n] = ld_f32_x(r_qkv, (qo + half) * 4, xl);
+      k0[n] = ld_f32_x(r_qkv, (d + qo) * 4, xl);
+      k1[n] = ld_f32_x(r_qkv, (d + qo + half) * 4, xl);
+    }
+#pragma unroll
+    for (int n = 0; n < NV; ++n) vr[n] = ld_f32_x(r_qkv, (2 * d + h * DH + min(lane + 64 * n, DH - 1)) * 4, xl);
+#pragma unroll
+    for (int n = 0; n < NH; ++n) {
+      const int i = lane + 64 * n;
+      if (i < half) {
+        const float2 cs = rp[i];
+        qs[i] = q0[n] * cs.x - q1[n] * cs.y;
+        qs[i + half] = q1[n] * cs.x + q0[n] * cs.y;
+        const bf16 ka = f2bf(k0[n] * cs.x - k1[n] * cs.y), kb = f2bf(k1[n] * cs.x + k0[n] * cs.y);
+        kn[i] = bf2f(ka);
+        kn[i + half] = bf2f(kb);
+        if (append) {
+          st_b16(r_k, (pos * DH + i) * 2, ka);
+          st_b16(r_k, (pos * DH + i + half) * 2, kb);
+        }
       }
     }
-    for (int i = lane; i < DH; i += 64) {
-      const bf16 v = f2bf(ld_f32_x(r_qkv, (2 * d + h * DH + i) * 4, xl));
-      vn[i] = bf2f(v);
-      if (append) st_b16(r_v, (i * kv_pad + pos) * 2, v);
+#pragma unroll
+    for (int n = 0; n < NV; ++n) {
+      const int i = lane + 64 * n;
+      if (i < DH) {
+        const bf16 v = f2bf(vr[n]);
+        vn[i] = bf2f(v);
+        if (append) st_b16(r_v, (i * kv_pad + pos) * 2, v);
+      }
     }
   }
   __syncthreads();
@@ -287,10 +344,7 @@ __device__ __forceinline__ void attn_head(int h, int pos, int d, int kv_pad, boo
     for (int i = 0; i < 8; ++i) { qv[i] = qs[sub * 8 + i]; kv_new[i] = kn[sub * 8 + i]; }
     const float scale = 1.0f / sqrtf((float)DH);
     for (int j0 = 0; j0 < n_keys; j0 += KPI * U) {
-      if (j0 > 0) {
-#pragma unroll
-        for (int u = 0; u < U; ++u) kv[u] = ld_plain_b128(r_k, koff + min(j0 + u * KPI + kg, last_cached) * DH * 2);
-      }
+      const bool more = j0 + KPI * U < n_keys;
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int j = j0 + u * KPI + kg;
@@ -302,8 +356,9 @@ __device__ __forceinline__ void attn_head(int h, int pos, int d, int kv_pad, boo
 #pragma unroll
           for (int i = 0; i < 8; ++i) s += qv[i] * bf2f(kv[u][i]);
         }
-#pragma unroll
-        for (int x = LPK / 2; x > 0; x >>= 1) s += __shfl_xor(s, x);
+        // the slot takes the next batch's key at once
+        if (more) kv[u] = ld_plain_b128(r_k, koff + min(j + KPI * U, last_cached) * DH * 2);
+s = group_sum<LPK>(s);
         s *= scale;
         if (j < n_keys) {
           if (sub == 0) sc[j] = s;
@@ -311,7 +366,10 @@ __device__ __forceinline__ void attn_head(int h, int pos, int d, int kv_pad, boo
         }
       }
     }
-    for (int x = 32; x > 0; x >>= 1) mx = fmaxf(mx, __shfl_xor(mx, x));
+    // the first values are in flight through the softmax
+#pragma unroll
+    for (int u = 0; u < UV; ++u) vv[u] = ld_plain_b128(r_v, voff + min(cg + CG * u, nchunk - 1) * 16);
+    mx = wave_max(mx);
     if (lane == 0) wred[wv] = mx;
   }
   __syncthreads();
@@ -325,7 +383,7 @@ __device__ __forceinline__ void attn_head(int h, int pos, int d, int kv_pad, boo
       sc[j] = p;
       sm += p;
     }
-    for (int x = 32; x > 0; x >>= 1) sm += __shfl_xor(sm, x);
+    sm = wave_sum(sm);
   }
   __syncthreads();
   if (!syncw) {
@@ -339,10 +397,8 @@ __device__ __forceinline__ void attn_head(int h, int pos, int d, int kv_pad, boo
     for (int w = 0; w < kWaves; ++w) tot += wred[8 + w];
     const float vnew = vn[dim];
     float acc = 0.f;
-    u16x8 vv[UV];
     for (int c0 = 0; c0 < nchunk; c0 += CG * UV) {
-#pragma unroll
-      for (int u = 0; u < UV; ++u) vv[u] = ld_plain_b128(r_v, voff + min(c0 + cg + CG * u, nchunk - 1) * 16);
+      const bool more = c0 + CG * UV < nchunk;
 #pragma unroll
       for (int u = 0; u < UV; ++u) {
         const int c = c0 + cg + CG * u;
@@ -352,10 +408,10 @@ __device__ __forceinline__ void attn_head(int h, int pos, int d, int kv_pad, boo
 #pragma unroll
           for (int e = 0; e < 8; ++e) acc += pp[e] * (c * 8 + e == pos ? vnew : bf2f(vv[u][e]));
         }
+        if (more) vv[u] = ld_plain_b128(r_v, voff + min(c + CG * UV, nchunk - 1) * 16);
       }
     }
-#pragma unroll
-    for (int x = CG / 2; x > 0; x >>= 1) acc += __shfl_xor(acc, x);
+acc = group_sum<CG>(acc);
     if (cg == 0) oact[dim] = f2bf(acc / tot);
   }
   __syncthreads();
