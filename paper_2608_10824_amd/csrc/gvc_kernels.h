@@ -44,6 +44,54 @@ __device__ __forceinline__ size_t frag_off(int m, int k, int KB) {
   return ((((size_t)(m >> 4) * KB + (k >> 5)) * 64 + ((k & 31) >> 3) * 16 + (m & 15)) << 3) + (k & 7);
 }
 
+// Cross-lane reductions on DPP row operations (a few cycles each) instead of
+// LDS permutes.  dpp_f<C>: v of the lane that DPP control C selects.
+template <int C>
+__device__ __forceinline__ float dpp_f(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), C, 0xF, 0xF, false));
+}
+constexpr int kDppXor1 = 0xB1;        // quad_perm [1, 0, 3, 2]
+constexpr int kDppXor2 = 0x4E;        // quad_perm [2, 3, 0, 1]
+constexpr int kDppHalfMirror = 0x141; // lane i of 8 <- lane 7 - i: the other quad, once quads agree
+constexpr int kDppMirror = 0x140;     // lane i of 16 <- lane 15 - i: the other half, once halves agree
+// Sum over aligned groups of N lanes (N = 1, 2, 4, 8, 16); every lane of a
+// group ends with the same value.
+template <int N>
+__device__ __forceinline__ float group_sum(float v) {
+  static_assert(N == 1 || N == 2 || N == 4 || N == 8 || N == 16, "group size");
+  if constexpr (N >= 2) v += dpp_f<kDppXor1>(v);
+  if constexpr (N >= 4) v += dpp_f<kDppXor2>(v);
+  if constexpr (N >= 8) v += dpp_f<kDppHalfMirror>(v);
+  if constexpr (N >= 16) v += dpp_f<kDppMirror>(v);
+  return v;
+}
+__device__ __forceinline__ float lane_f(float v, int l) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), l));
+}
+// Sum and maximum over the whole wave (all lanes active), wave-uniform.
+__device__ __forceinline__ float wave_sum(float v) {
+  v = group_sum<16>(v);
+  return (lane_f(v, 0) + lane_f(v, 16)) + (lane_f(v, 32) + lane_f(v, 48));
+}
+__device__ __forceinline__ float wave_max(float v) {
+  v = fmaxf(v, dpp_f<kDppXor1>(v));
+  v = fmaxf(v, dpp_f<kDppXor2>(v));
+  v = fmaxf(v, dpp_f<kDppHalfMirror>(v));
+  v = fmaxf(v, dpp_f<kDppMirror>(v));
+  return fmaxf(fmaxf(lane_f(v, 0), lane_f(v, 16)), fmaxf(lane_f(v, 32), lane_f(v, 48)));
+}
+
+// Maximum over aligned groups of N lanes (N = 2, 4, 8, 16), as group_sum.
+template <int N>
+__device__ __forceinline__ float group_max(float v) {
+  static_assert(N == 2 || N == 4 || N == 8 || N == 16, "group size");
+  v = fmaxf(v, dpp_f<kDppXor1>(v));
+  if constexpr (N >= 4) v = fmaxf(v, dpp_f<kDppXor2>(v));
+  if constexpr (N >= 8) v = fmaxf(v, dpp_f<kDppHalfMirror>(v));
+  if constexpr (N >= 16) v = fmaxf(v, dpp_f<kDppMirror>(v));
+  return v;
+}
+
 // ------------------------------------------------------------------ GEMM
 // Work units of a GEMM launch.  Pair maps give a workgroup two 16-row weight
 // blocks whose epilogue partners share lanes; single maps give it one block.

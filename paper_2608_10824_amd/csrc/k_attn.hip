@@ -59,28 +59,44 @@ __global__ __launch_bounds__(64) void k_attn_prefill(const bf16* __restrict__ q,
 #pragma unroll
   for (int i = 0; i < 4; ++i) { m_run[i] = -INFINITY; l_run[i] = 0.f; }
 
-  for (int j0 = 0; j0 <= max_pos; j0 += 32) {
-    floatx4 s0 = {0, 0, 0, 0}, s1 = {0, 0, 0, 0};
-    const bf16* k0 = kbase + (size_t)(j0 + col) * DH + grp * 8;
-    const bf16* k1 = k0 + 16 * DH;
+  // Key tile j0's fragments are loaded during tile j0 - 32 and its value
+  // fragments at the start of tile j0, so both round trips overlap the
+  // arithmetic (the last tile re-reads itself instead of reading past it).
+  bf16x8 kf0[NK], kf1[NK], vf[NO];
+  auto load_k = [&](int j, bf16x8 (&f0)[NK], bf16x8 (&f1)[NK]) {
+    const bf16* k0 = kbase + (size_t)(j + col) * DH + grp * 8;
 #pragma unroll
     for (int kk = 0; kk < NK; ++kk) {
-      s0 = mfma16(qf[kk], *(const bf16x8*)(k0 + kk * 32), s0);
-      s1 = mfma16(qf[kk], *(const bf16x8*)(k1 + kk * 32), s1);
+      f0[kk] = *(const bf16x8*)(k0 + kk * 32);
+      f1[kk] = *(const bf16x8*)(k0 + 16 * DH + kk * 32);
+    }
+  };
+  load_k(0, kf0, kf1);
+  for (int j0 = 0; j0 <= max_pos; j0 += 32) {
+    {
+      const bf16* vj = vbase + j0 + grp * 8;
+#pragma unroll
+      for (int c = 0; c < NO; ++c) vf[c] = *(const bf16x8*)(vj + (size_t)(c * 16 + col) * kv_pad);
+    }
+    bf16x8 nk0[NK], nk1[NK];
+    load_k(j0 + 32 <= max_pos ? j0 + 32 : j0, nk0, nk1);
+    floatx4 s0 = {0, 0, 0, 0}, s1 = {0, 0, 0, 0};
+#pragma unroll
+    for (int kk = 0; kk < NK; ++kk) {
+      s0 = mfma16(qf[kk], kf0[kk], s0);
+      s1 = mfma16(qf[kk], kf1[kk], s1);
     }
     float p0[4], p1[4], alpha[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const float a0 = (j0 + col <= qpos[i]) ? s0[i] * scale : -INFINITY;
       const float a1 = (j0 + 16 + col <= qpos[i]) ? s1[i] * scale : -INFINITY;
-      float mx = fmaxf(a0, a1);
-      for (int x = 1; x < 16; x <<= 1) mx = fmaxf(mx, __shfl_xor(mx, x));
+      const float mx = group_max<16>(fmaxf(a0, a1));   // over the row's 16 lanes (one DPP row)
       const float mn = fmaxf(m_run[i], mx);
       alpha[i] = __expf(m_run[i] - mn);
       p0[i] = __expf(a0 - mn);
       p1[i] = __expf(a1 - mn);
-      float sm = p0[i] + p1[i];
-      for (int x = 1; x < 16; x <<= 1) sm += __shfl_xor(sm, x);
+      const float sm = group_sum<16>(p0[i] + p1[i]);
       l_run[i] = l_run[i] * alpha[i] + sm;
       m_run[i] = mn;
     }
@@ -97,11 +113,12 @@ __global__ __launch_bounds__(64) void k_attn_prefill(const bf16* __restrict__ q,
     __syncthreads();
     const bf16x8 pa = *(const bf16x8*)(ps + col * 32 + grp * 8);
     __syncthreads();
-    const bf16* vj = vbase + j0 + grp * 8;
 #pragma unroll
-    for (int c = 0; c < NO; ++c) {
-      const bf16x8 vb = *(const bf16x8*)(vj + (size_t)(c * 16 + col) * kv_pad);
-      acc[c] = mfma16(pa, vb, acc[c]);
+    for (int c = 0; c < NO; ++c) acc[c] = mfma16(pa, vf[c], acc[c]);
+#pragma unroll
+    for (int kk = 0; kk < NK; ++kk) {
+      kf0[kk] = nk0[kk];
+      kf1[kk] = nk1[kk];
     }
   }
   // normalise and store (frag layout for the output projection)
