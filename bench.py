@@ -38,6 +38,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-c3", action="store_true", help="skip the C3 episode (recompute rate)")
     return ap.parse_args()
 
 
@@ -85,6 +86,48 @@ def cpu_baseline(cfg, w_cpu, si, n_static, min_s=10.0, max_reps=20):
                       "(%.1f s of CPU work); per-layer time scaled to 32 layers"
                       % (int(o.recomputed[0, 0]), reps, time.perf_counter() - t_all),
             "seconds_per_step": t_step}
+
+
+def c3_episode(dev):
+    """The 50-frame moving-rectangle episode at the 7B shape with the gate
+    applied (Alg. 1): per-layer reuse 80% -> 20%, tau = 249/250, theta = 0.1.
+    Reports how often the gate fired (the recompute rate over steps 1..49;
+    step 0 has no cache), the mean recomputed rows per layer, and the time
+    per control step."""
+    import torch
+    import synth
+    from paper_2608_10824_amd import gvc
+    from paper_2608_10824_amd.session import Session
+    cfg = synth.config_c3()
+    w = synth.model_weights(cfg, device=dev)
+    s = Session(cfg, w, device=dev)
+    torch.cuda.synchronize()
+    del w
+    torch.cuda.empty_cache()
+    frames = synth.c3_episode_frames(cfg).to(dev)
+    ids = synth.text_ids(cfg).to(dev)
+    s.step_prefill(frames[0:1], ids)
+    s.decode_actions()
+    n = frames.shape[0]
+    fired, rows = [], []
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for t in range(1, n):
+        _, fire = s.margin_gate()
+        fired.append(bool(fire[0]))
+        mask, _ = s.select_static(frames[t:t + 1], frames[t - 1:t])
+        s.step_prefill(frames[t:t + 1], ids, None, mask)
+        s.decode_actions()
+        rows.append(s.read(gvc.STATE_ROWS).cpu().tolist())
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    s.close()
+    L = cfg.n_layers
+    return {"frames": n, "gated_steps": n - 1, "fired": sum(fired), "recompute_rate": sum(fired) / (n - 1),
+            "mean_recomputed_rows_per_layer": sum(sum(r) for r in rows) / (len(rows) * L),
+            "prompt_len": cfg.prompt_len, "ms_per_step": dt * 1e3 / (n - 1),
+            "reuse_permille": "%d -> %d over the layers" % (cfg.permille()[0], cfg.permille()[-1]),
+            "tau": "%d/%d" % cfg.tau, "theta": cfg.theta}
 
 
 def stored_traffic(kernel_sources):
@@ -251,6 +294,11 @@ def main():
         out["cpu_baseline"] = cb
         note("cpu baseline done")
     s.close()
+    del s
+    torch.cuda.empty_cache()
+    if not args.no_c3:
+        out["c3"] = c3_episode(dev)
+        note("C3 episode done: recompute rate %.3f" % out["c3"]["recompute_rate"])
     print(json.dumps(out))
     return 0
 
