@@ -279,6 +279,7 @@ def main():
         "prefill_tflops": prefill_flops / (prefill_ms / 1e3) / 1e12,
         "prefill_mfma_util_pct": 100.0 * prefill_flops / (prefill_ms / 1e3) / 1e12 / BF16_PEAK_TFLOPS,
         "prefill_hbm_gbs": prefill_bytes / (prefill_ms / 1e3) / 1e9,
+        "prefill_hbm_frac": prefill_bytes / (prefill_ms / 1e3) / 1e9 / HBM_PEAK_GBS,
         "decode_ms": decode_ms,
         "decode_gbs": decode_bytes / (decode_ms / 1e3) / 1e9,
         "decode_hbm_frac": decode_bytes / (decode_ms / 1e3) / 1e9 / HBM_PEAK_GBS,
