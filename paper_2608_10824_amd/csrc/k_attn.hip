@@ -6,7 +6,8 @@
 // the same per-layer cache, so the kernel is an ordinary causal attention
 // whose queries are an arbitrary, position-sorted subset of the prompt.
 //
-// Prefill: one wave per (episode, head, 16 query rows).  S = Q K^T and O += P V
+// Prefill: one workgroup per (episode, head, 16 query rows), its waves
+// splitting the key tiles.  S = Q K^T and O += P V
 // run on MFMA v_mfma_f32_16x16x32_bf16 over key tiles of 32 with an fp32
 // online softmax; P is re-laid out through a 1 KiB LDS tile into the A
 // operand order; V is stored transposed so the B operand of P V is 16
@@ -16,20 +17,28 @@
 
 namespace gvc {
 
+// kAttnWaves waves per (episode, head, 16 query rows) split the key tiles
+// round robin; each keeps its own online softmax (running max, sum and
+// output), and the partial results are merged through LDS at the end.
+constexpr int kAttnWaves = 4;
+
 template <int DH>
-__global__ __launch_bounds__(64) void k_attn_prefill(const bf16* __restrict__ q, const bf16* __restrict__ kc,
-                                                     const bf16* __restrict__ vc, const int* __restrict__ rows_pos,
-                                                     const int* __restrict__ ep_counts,
-                                                     const int* __restrict__ ep_offsets, int H, int kv_pad,
-                                                     bf16* __restrict__ o, int KB) {
+__global__ __launch_bounds__(kAttnWaves * 64) void k_attn_prefill(
+    const bf16* __restrict__ q, const bf16* __restrict__ kc, const bf16* __restrict__ vc,
+    const int* __restrict__ rows_pos, const int* __restrict__ ep_counts, const int* __restrict__ ep_offsets, int H,
+    int kv_pad, bf16* __restrict__ o, int KB) {
   constexpr int NK = DH / 32;   // k-steps of QK^T
   constexpr int NO = DH / 16;   // output column blocks
-  __shared__ bf16 ps[16 * 32];
+  static_assert(NO % kAttnWaves == 0, "output blocks per merging wave");
+  __shared__ bf16 ps_all[kAttnWaves][16 * 32];
+  __shared__ floatx4 m_acc[kAttnWaves][NO][64];
+  __shared__ float m_ml[kAttnWaves][8][64];
   const int tile = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
   const int cnt = ep_counts[b];
   if (tile * 16 >= cnt) return;
   const int off = ep_offsets[b];
-  const int lane = threadIdx.x;
+  const int lane = threadIdx.x & 63, wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  bf16* ps = ps_all[wv];
   const int col = lane & 15, grp = lane >> 4;
   const int d = H * DH;
   const int last = min(cnt, tile * 16 + 16) - 1;     // last valid row of the tile
@@ -59,9 +68,13 @@ __global__ __launch_bounds__(64) void k_attn_prefill(const bf16* __restrict__ q,
 #pragma unroll
   for (int i = 0; i < 4; ++i) { m_run[i] = -INFINITY; l_run[i] = 0.f; }
 
-  // Key tile j0's fragments are loaded during tile j0 - 32 and its value
-  // fragments at the start of tile j0, so both round trips overlap the
+  // This wave's key tiles: j0 = 32 * (wv + kAttnWaves * n) <= max_pos.  Key
+  // tile j0's fragments are loaded during the wave's previous tile and its
+  // value fragments at the start of tile j0, so both round trips overlap the
   // arithmetic (the last tile re-reads itself instead of reading past it).
+  // A row may see no key at all in a wave's tiles: its running max stays
+  // -inf and the update keeps its sum and output at zero.
+  constexpr int kStride = 32 * kAttnWaves;
   bf16x8 kf0[NK], kf1[NK], vf[NO];
   auto load_k = [&](int j, bf16x8 (&f0)[NK], bf16x8 (&f1)[NK]) {
     const bf16* k0 = kbase + (size_t)(j + col) * DH + grp * 8;
@@ -71,15 +84,16 @@ __global__ __launch_bounds__(64) void k_attn_prefill(const bf16* __restrict__ q,
       f1[kk] = *(const bf16x8*)(k0 + 16 * DH + kk * 32);
     }
   };
-  load_k(0, kf0, kf1);
-  for (int j0 = 0; j0 <= max_pos; j0 += 32) {
+  const int jstart = 32 * wv;
+  if (jstart <= max_pos) load_k(jstart, kf0, kf1);
+  for (int j0 = jstart; j0 <= max_pos; j0 += kStride) {
     {
       const bf16* vj = vbase + j0 + grp * 8;
 #pragma unroll
       for (int c = 0; c < NO; ++c) vf[c] = *(const bf16x8*)(vj + (size_t)(c * 16 + col) * kv_pad);
     }
     bf16x8 nk0[NK], nk1[NK];
-    load_k(j0 + 32 <= max_pos ? j0 + 32 : j0, nk0, nk1);
+    load_k(j0 + kStride <= max_pos ? j0 + kStride : j0, nk0, nk1);
     floatx4 s0 = {0, 0, 0, 0}, s1 = {0, 0, 0, 0};
 #pragma unroll
     for (int kk = 0; kk < NK; ++kk) {
@@ -93,9 +107,10 @@ __global__ __launch_bounds__(64) void k_attn_prefill(const bf16* __restrict__ q,
       const float a1 = (j0 + 16 + col <= qpos[i]) ? s1[i] * scale : -INFINITY;
       const float mx = group_max<16>(fmaxf(a0, a1));   // over the row's 16 lanes (one DPP row)
       const float mn = fmaxf(m_run[i], mx);
-      alpha[i] = __expf(m_run[i] - mn);
-      p0[i] = __expf(a0 - mn);
-      p1[i] = __expf(a1 - mn);
+      const float mb = mn == -INFINITY ? 0.f : mn;      // no key yet: everything stays zero
+      alpha[i] = __expf(m_run[i] - mb);
+      p0[i] = __expf(a0 - mb);
+      p1[i] = __expf(a1 - mb);
       const float sm = group_sum<16>(p0[i] + p1[i]);
       l_run[i] = l_run[i] * alpha[i] + sm;
       m_run[i] = mn;
@@ -104,15 +119,14 @@ __global__ __launch_bounds__(64) void k_attn_prefill(const bf16* __restrict__ q,
     for (int c = 0; c < NO; ++c)
 #pragma unroll
       for (int i = 0; i < 4; ++i) acc[c][i] *= alpha[i];
-    // P (C layout: row grp*4+i, key col / 16+col) -> LDS [16][32] -> A layout
+    // P (C layout: row grp*4+i, key col / 16+col) -> this wave's LDS tile
+    // [16][32] -> A layout (a wave's LDS accesses complete in order)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       ps[(grp * 4 + i) * 32 + col] = f2bf(p0[i]);
       ps[(grp * 4 + i) * 32 + 16 + col] = f2bf(p1[i]);
     }
-    __syncthreads();
     const bf16x8 pa = *(const bf16x8*)(ps + col * 32 + grp * 8);
-    __syncthreads();
 #pragma unroll
     for (int c = 0; c < NO; ++c) acc[c] = mfma16(pa, vf[c], acc[c]);
 #pragma unroll
@@ -121,15 +135,47 @@ __global__ __launch_bounds__(64) void k_attn_prefill(const bf16* __restrict__ q,
       kf1[kk] = nk1[kk];
     }
   }
-  // normalise and store (frag layout for the output projection)
+  // merge the waves' partial softmax results; wave w finishes output blocks
+  // [w NO / kAttnWaves, (w + 1) NO / kAttnWaves) for all 16 rows
+#pragma unroll
+  for (int c = 0; c < NO; ++c) m_acc[wv][c][lane] = acc[c];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    const int r = tile * 16 + grp * 4 + i;
-    if (r >= cnt) continue;
-    const int m = off + r;
-    const float inv = 1.0f / l_run[i];
+    m_ml[wv][i][lane] = m_run[i];
+    m_ml[wv][4 + i][lane] = l_run[i];
+  }
+  __syncthreads();
+  float lt[4], sw[kAttnWaves][4];
 #pragma unroll
-    for (int c = 0; c < NO; ++c) o[frag_off(m, h * DH + c * 16 + col, KB)] = f2bf(acc[c][i] * inv);
+  for (int i = 0; i < 4; ++i) {
+    float m = m_ml[0][i][lane];
+#pragma unroll
+    for (int w = 1; w < kAttnWaves; ++w) m = fmaxf(m, m_ml[w][i][lane]);   // finite: wave 0 sees key 0
+    float l = 0.f;
+#pragma unroll
+    for (int w = 0; w < kAttnWaves; ++w) {
+      sw[w][i] = __expf(m_ml[w][i][lane] - m);
+      l += m_ml[w][4 + i][lane] * sw[w][i];
+    }
+    lt[i] = l;
+  }
+  constexpr int CW = NO / kAttnWaves;
+#pragma unroll
+  for (int cc = 0; cc < CW; ++cc) {
+    const int c = wv * CW + cc;
+    floatx4 v = {0, 0, 0, 0};
+#pragma unroll
+    for (int w = 0; w < kAttnWaves; ++w) {
+      const floatx4 aw = m_acc[w][c][lane];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) v[i] += aw[i] * sw[w][i];
+    }
+    // normalise and store (frag layout for the output projection)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = tile * 16 + grp * 4 + i;
+      if (r < cnt) o[frag_off(off + r, h * DH + c * 16 + col, KB)] = f2bf(v[i] / lt[i]);
+    }
   }
 }
 
@@ -288,11 +334,11 @@ hipError_t launch_attn_prefill(const bf16* q, const bf16* kc, const bf16* vc, co
                                int max_tiles, bf16* o, int KB, hipStream_t s) {
   dim3 grid(max_tiles, H, B);
   if (head_dim == 128)
-    hipLaunchKernelGGL(k_attn_prefill<128>, grid, dim3(64), 0, s, q, kc, vc, rows_pos, ep_counts, ep_offsets, H,
-                       kv_pad, o, KB);
+    hipLaunchKernelGGL(k_attn_prefill<128>, grid, dim3(kAttnWaves * 64), 0, s, q, kc, vc, rows_pos, ep_counts,
+                       ep_offsets, H, kv_pad, o, KB);
   else if (head_dim == 64)
-    hipLaunchKernelGGL(k_attn_prefill<64>, grid, dim3(64), 0, s, q, kc, vc, rows_pos, ep_counts, ep_offsets, H,
-                       kv_pad, o, KB);
+    hipLaunchKernelGGL(k_attn_prefill<64>, grid, dim3(kAttnWaves * 64), 0, s, q, kc, vc, rows_pos, ep_counts,
+                       ep_offsets, H, kv_pad, o, KB);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();
