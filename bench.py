@@ -104,6 +104,7 @@ def c3_episode(dev):
     torch.cuda.synchronize()
     del w
     torch.cuda.empty_cache()
+    note("C3 weights generated")
     frames = synth.c3_episode_frames(cfg).to(dev)
     ids = synth.text_ids(cfg).to(dev)
     s.step_prefill(frames[0:1], ids)
@@ -119,6 +120,8 @@ def c3_episode(dev):
         s.step_prefill(frames[t:t + 1], ids, None, mask)
         s.decode_actions()
         rows.append(s.read(gvc.STATE_ROWS).cpu().tolist())
+        if t % 10 == 0:
+            note("C3 frame %d of %d" % (t, n - 1))
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
     s.close()
