@@ -87,12 +87,16 @@ def layer_reuse_masks(n_patches: int, ranked: list, permille) -> np.ndarray:
     return masks
 
 
-def select_static(frame_t: np.ndarray, frame_prev: np.ndarray, p: int, tau, permille):
-    """One episode: returns (masks [L][N] bool, n_static, static [N] bool, ranked)."""
+def select_static(frame_t: np.ndarray, frame_prev: np.ndarray, p: int, tau, permille, exclude=None):
+    """One episode: returns (masks [L][N] bool, n_static, static [N] bool, ranked).
+    exclude [N] bool (Stage 2's task-relevant patches) leaves the static set
+    before the ranking."""
     u = patchify(frame_t, p)
     v = patchify(frame_prev, p)
     dot, na, nb = patch_stats(u, v)
     num, den = tau
     static = np.array([is_static(dot[n], na[n], nb[n], num, den) for n in range(len(dot))])
+    if exclude is not None:
+        static = static & ~np.asarray(exclude, dtype=bool)
     ranked = rank_static(static, dot, na, nb)
     return layer_reuse_masks(len(dot), ranked, permille), len(ranked), static, ranked

@@ -28,6 +28,7 @@ import numpy as np
 
 from .patches import select_static as _select_one
 from .llama import layer_rows, head_row, rmsnorm
+from .relevance import text_vision_attention, relevant_patches
 from .margin import position_margin, reduce_margin, gate_fires
 
 
@@ -74,10 +75,24 @@ class OracleVLA:
         self.margins = None
         self.tokens = None
         self.recomputed = None     # [B][L] rows recomputed by the last prefill
+        self.tv = None             # [B][L][H][N] Stage 2 attention of the last prefill (task_topk > 0)
 
     # ---------------------------------------------------------- Stage 1 + 3
-    def select_static(self, frame_t, frame_prev, tau=None, permille=None):
-        """Per episode: reuse masks [B][L][N] and |S| [B]."""
+    def relevant(self, b, scores=None):
+        """Stage 2: episode b's task-relevant patches [N] bool from the last
+        prefill's attention (or from given per-patch scores), or None."""
+        cfg = self.cfg
+        if cfg.task_topk <= 0 or cfg.n_text < 2:
+            return None
+        if scores is None:
+            if self.tv is None:
+                return None
+            scores = self.tv[b].sum(axis=(0, 1))
+        return relevant_patches(np.asarray(scores, dtype=np.float64), cfg.task_topk)
+
+    def select_static(self, frame_t, frame_prev, tau=None, permille=None, scores=None):
+        """Per episode: reuse masks [B][L][N] and |S| [B] (Stages 1 and 2).
+        scores [B][N], if given, replace the oracle's own Stage 2 scores."""
         cfg = self.cfg
         tau = tau or cfg.tau
         permille = permille or cfg.permille()
@@ -85,7 +100,8 @@ class OracleVLA:
         masks = np.zeros((cfg.batch, cfg.n_layers, cfg.n_patches), dtype=bool)
         n_static = np.zeros(cfg.batch, dtype=np.int64)
         for b in range(cfg.batch):
-            masks[b], n_static[b], _, _ = _select_one(ft[b], fp[b], cfg.patch, tau, permille)
+            excl = self.relevant(b, None if scores is None else scores[b])
+            masks[b], n_static[b], _, _ = _select_one(ft[b], fp[b], cfg.patch, tau, permille, excl)
         return masks, n_static
 
     # ---------------------------------------------------------- prompt pass
@@ -115,6 +131,9 @@ class OracleVLA:
         P, L = lay.P, cfg.n_layers
         self.head_logits = np.zeros((cfg.batch, len(lay.head_pos), cfg.vocab))
         self.recomputed = np.zeros((cfg.batch, L), dtype=np.int64)
+        stage2 = cfg.task_topk > 0 and cfg.n_text >= 2
+        if stage2:
+            self.tv = np.zeros((cfg.batch, L, cfg.n_heads, cfg.n_patches))
         for b in range(cfg.batch):
             use_mask = masks is not None and self.valid[b]
             for l in range(L):
@@ -127,6 +146,10 @@ class OracleVLA:
                         self.H[0, b, p] = self.embed_row(b, p, frame_t, text_ids, extra_rows)
                 out = layer_rows(self.w["layers"][l], self.H[l, b], rows, rows,
                                  self.K[l, b], self.V[l, b], cfg.n_heads, cfg.rms_eps, cfg.rope_theta)
+                if stage2:
+                    self.tv[b, l] = text_vision_attention(self.w["layers"][l], self.H[l, b], self.K[l, b],
+                                                          cfg.n_patches, cfg.n_text, cfg.n_heads, cfg.rms_eps,
+                                                          cfg.rope_theta)
                 self.H[l + 1, b, rows] = out
                 self.recomputed[b, l] = len(rows)
             for i, p in enumerate(lay.head_pos):

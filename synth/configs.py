@@ -40,6 +40,7 @@ class VLAConfig:
     # at s = -3.6, 23/49 at -3.65).
     bin_scale_log2: float = -3.625
     norm_full_vocab: bool = True    # softmax normaliser over the full vocabulary
+    task_topk: int = 0          # Stage 2: patches with the most instruction attention leave S (0: off)
 
     @property
     def head_dim(self) -> int:
