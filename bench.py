@@ -39,6 +39,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-c3", action="store_true", help="skip the C3 episode (recompute rate)")
+    ap.add_argument("--no-stage2", action="store_true", help="skip the Stage 2 (top-k = 120) steps")
     return ap.parse_args()
 
 
@@ -133,6 +134,49 @@ def c3_episode(dev):
             "tau": "%d/%d" % cfg.tau, "theta": cfg.theta}
 
 
+def stage2_steps(cfg, w, si, dev, steps, warmup):
+    """The C2 workload with Stage 2 on (the paper's top-k = 120): Stage 1's
+    128 static patches minus those among the 120 that drew the most
+    instruction attention in the previous pass.  Reports the time per
+    control step, the patches left static, the rows recomputed per layer and
+    the signal kernel's time per layer."""
+    import torch
+    from paper_2608_10824_amd import gvc
+    from paper_2608_10824_amd.session import Session
+    cfg2 = cfg.with_(task_topk=120)
+    s = Session(cfg2, w, device=dev)
+    torch.cuda.synchronize()
+    fp, ft = si["frame_prev"].to(dev), si["frame_t"].to(dev)
+    ids = si["text_ids"].to(dev)
+    s.step_prefill(fp, ids)
+    s.decode_actions()
+
+    def step():
+        s.margin_gate(force=[0])
+        mask, _ = s.select_static(ft, fp)
+        s.step_prefill(ft, ids, None, mask)
+        s.decode_actions()
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    n_static = int(s.n_static[0].item())
+    rows = s.read(gvc.STATE_ROWS).cpu().tolist()
+    gvc.profile_begin(s.ctx, gvc.K_STAGE2, cfg.n_layers * 2 + 8)
+    step()
+    torch.cuda.synchronize()
+    sig_ms, sig_n = gvc.profile_end(s.ctx)
+    s.close()
+    return {"task_topk": 120, "ms_per_step": dt * 1e3 / steps, "steps": steps, "static_patches": n_static,
+            "recomputed_rows_per_layer": rows[0], "signal_us_per_layer": sig_ms * 1e3 / max(sig_n, 1),
+            "signal_launches_per_step": sig_n}
+
+
 def stored_traffic(kernel_sources):
     """HBM bytes per launch of the dominant kernel from the committed rocprofv3
     counter summary, or None when the kernel sources changed since."""
@@ -174,6 +218,7 @@ def main():
     w = synth.model_weights(cfg, device=dev)
     si = synth.step_inputs(cfg, n_static)
     note("weights and inputs generated")
+    w_stage2 = w if not args.no_stage2 else None
     w_cpu = None
     if not args.no_cpu_baseline:
         w_cpu = {k: v.cpu() for k, v in w.items() if k != "layers"}
@@ -300,6 +345,11 @@ def main():
     s.close()
     del s
     torch.cuda.empty_cache()
+    if w_stage2 is not None:
+        out["stage2"] = stage2_steps(cfg, w_stage2, si, dev, min(args.steps, 10), 2)
+        note("Stage 2 steps done: %d static patches left" % out["stage2"]["static_patches"])
+        del w_stage2
+        torch.cuda.empty_cache()
     if not args.no_c3:
         out["c3"] = c3_episode(dev)
         note("C3 episode done: recompute rate %.3f" % out["c3"]["recompute_rate"])

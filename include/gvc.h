@@ -68,7 +68,9 @@ enum gvc_state_item {
   GVC_STATE_HEAD_LOGITS = 3, /* fp32 [B][n_head_rows][V] logits of the last prompt pass */
   GVC_STATE_VALID = 4,   /* int32 [B] cache-valid flags */
   GVC_STATE_ROWS = 5,    /* int32 [L]: rows recomputed per layer by the last prompt pass */
-  GVC_STATE_MARGINS = 6  /* fp32 [B][D] per-position margins of the last decode */
+  GVC_STATE_MARGINS = 6, /* fp32 [B][D] per-position margins of the last decode */
+  GVC_STATE_TV = 7       /* fp32 [B][L][n_heads][N] Stage 2 attention of the last prompt pass
+                            (desc.task_topk > 0; the layer argument is ignored) */
 };
 
 /* Model and workload shape.  Llama-2 block (Sec. V-A backbone): pre-norm
@@ -94,6 +96,11 @@ typedef struct gvc_desc {
   int32_t norm_full_vocab;/* 1: softmax normaliser over all V ids; 0: over the bins */
   float rms_eps;          /* RMSNorm epsilon (1e-5 for Llama-2) */
   float rope_theta;       /* rotary base (10000 for Llama-2) */
+  int32_t task_topk;      /* Stage 2 (Sec. III-B): 0 = off; else each prompt pass records, per layer
+                             and head, the softmax probability that the instruction tokens after the
+                             image (1 <= n_text - 1 <= 32) put on each visual key, and the next
+                             gvc_select_static takes the task_topk patches of highest total out of
+                             the static set.  0 <= task_topk <= N; N + n_text < 640. */
 } gvc_desc;
 
 /* bf16 weights of one decoder layer, canonical [out_features][in_features]. */
@@ -139,16 +146,19 @@ int32_t gvc_init_cache(const gvc_desc* desc, const gvc_weights* weights,
                        void* workspace, size_t workspace_bytes,
                        void* stream, gvc_ctx** out);
 
-/* Stage 1 + applied Stage 3 (Sec. III-B).  frame_t, frame_prev: dev uint8
+/* Stage 1 + Stage 2 + applied Stage 3 (Sec. III-B).  frame_t, frame_prev: dev uint8
  * [B][n_views][img][img][3].  A patch (p x p x 3 values, H,W,C order) is static
  * iff its cosine with the same patch of frame_prev exceeds tau_num/tau_den,
  * decided exactly in integer arithmetic (both patches all-zero: static;
- * exactly one all-zero: not static).  Static patches are ranked by cosine,
+ * exactly one all-zero: not static).  With desc.task_topk > 0, once a prompt
+ * pass has run, the task_topk patches whose total instruction attention in
+ * that pass is highest (fp32 sums in a fixed order, ties to the lower index)
+ * are not static (Stage 2).  Static patches are ranked by cosine,
  * highest first, ties to the lower index; layer l reuses the first
  * floor(reuse_permille[l] * |S| / 1000) of them.
  * reuse_permille: host int32 [L] in [0, 1000], or NULL for 1000 everywhere.
  * reuse_mask: dev uint8 [B][L][N] out (1 = reuse at that layer).
- * n_static: dev int32 [B] out (|S|), or NULL.
+ * n_static: dev int32 [B] out (|S|, after Stage 2), or NULL.
  * Errors: GVC_EINVAL (null frame/mask, 0 < tau_num <= tau_den violated,
  * permille out of range). */
 int32_t gvc_select_static(gvc_ctx* ctx, const uint8_t* frame_t, const uint8_t* frame_prev,
@@ -211,7 +221,7 @@ enum gvc_kernel_class {
   GVC_K_DECODE_DOWN = 4, GVC_K_DECODE_HEAD = 5,
   GVC_K_PREFILL_QKV = 6, GVC_K_PREFILL_ATTN = 7, GVC_K_PREFILL_O = 8, GVC_K_PREFILL_GU = 9,
   GVC_K_PREFILL_DOWN = 10, GVC_K_PREFILL_HEAD = 11, GVC_K_EMBED = 12, GVC_K_NORM = 13,
-  GVC_K_SELECT = 14, GVC_K_DECODE_PASS = 15, GVC_K_COUNT = 16
+  GVC_K_SELECT = 14, GVC_K_DECODE_PASS = 15, GVC_K_STAGE2 = 16, GVC_K_COUNT = 17
 };
 
 /* Starts timing every launch of kernel class `cls` (enum gvc_kernel_class):

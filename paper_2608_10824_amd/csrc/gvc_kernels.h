@@ -195,8 +195,11 @@ hipError_t launch_fill_u32(uint32_t* p, uint32_t v, size_t n, hipStream_t s);
 
 hipError_t launch_patch_stats(const uint8_t* ft, const uint8_t* fp, int B, int views, int img, int patch,
                               int* stats, hipStream_t s);
+// Stage 1 (+ Stage 2 when tv != nullptr: per patch the sum over LH columns of
+// tv [B][LH][N], in order; the topk highest, ties to the lower index, are not static).
 hipError_t launch_rank_mask(const int* stats, int B, int N, int L, long long tau_num, long long tau_den,
-                            const int* permille_dev, uint8_t* mask, int* n_static, hipStream_t s);
+                            const int* permille_dev, uint8_t* mask, int* n_static, const float* tv, int LH,
+                            int topk, hipStream_t s);
 
 hipError_t launch_build_rows(const uint8_t* mask, const int* valid, int B, int L, int N, int P,
                              int* rows, int* counts, int* ep_counts, int* ep_offsets, hipStream_t s);
@@ -205,6 +208,12 @@ hipError_t launch_im2row(const uint8_t* frame, int views, int img, int patch, co
 hipError_t launch_rmsnorm(const float* src, const int* idx, int M, int d, const float* gain, float eps,
                           bf16* x, int KB, hipStream_t s);
 hipError_t launch_gemm(const GemmArgs& a, int epi, int NT, hipStream_t s);
+// Stage 2 signal of one layer: tv[b * tv_bstride + h * N + n] = sum over the
+// T1 instruction rows after the image of their softmax probability on visual
+// key n (1 <= T1 <= 32, N + T1 < 640).
+hipError_t launch_text_vis(const bf16* q, const bf16* kc, const int* ep_counts, const int* ep_offsets, int B, int H,
+                           int head_dim, int kv_pad, int N, int P, int T1, float* tv, size_t tv_bstride,
+                           hipStream_t s);
 hipError_t launch_attn_prefill(const bf16* q, const bf16* kc, const bf16* vc, const int* rows_pos,
                                const int* ep_counts, const int* ep_offsets, int B, int H, int head_dim,
                                int kv_pad, int max_tiles, bf16* o, int KB, hipStream_t s);

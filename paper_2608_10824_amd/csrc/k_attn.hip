@@ -179,6 +179,134 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn_prefill(
   }
 }
 
+// Stage 2 signal (Sec. III-B: static patches that draw the instruction's
+// attention are recomputed): for head h of episode b, the exact softmax of
+// each instruction token after the image (positions N+1 .. N+T1, the T1 <= 32
+// text rows that follow the visual block in the position-sorted row list)
+// over the keys up to its position, and per visual key n the sum of those
+// probabilities over the rows, written to tv[n].  Scores on MFMA as in
+// k_attn_prefill (16-row tiles, key tiles of 32 over the 4 waves, kept in
+// registers); three passes: row maxima, row sums, column sums in a fixed
+// order (deterministic).
+constexpr int kTvWaves = 4, kTvTiles = 5;   // key tiles per wave: keys < 4 * 5 * 32 = 640
+
+template <int DH>
+__global__ __launch_bounds__(kTvWaves * 64) void k_text_vis(const bf16* __restrict__ q, const bf16* __restrict__ kc,
+                                                           const int* __restrict__ ep_counts,
+                                                           const int* __restrict__ ep_offsets, int H, int kv_pad,
+                                                           int N, int P, int T1, float* __restrict__ tv,
+                                                           size_t tv_bstride) {
+  constexpr int NK = DH / 32;
+  __shared__ float red[kTvWaves][32];
+  __shared__ float mrow[32], lrow[32];
+  const int h = blockIdx.x, b = blockIdx.y;
+  const int lane = threadIdx.x & 63, wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int col = lane & 15, grp = lane >> 4;
+  const int cnt = ep_counts[b], off = ep_offsets[b];
+  const int first = cnt - (P - N - 1);   // list index of position N + 1
+  const int d = H * DH;
+  const int nkeys = N + T1 + 1, ntile = (nkeys + 31) / 32;
+  const float scale = 1.0f / sqrtf((float)DH);
+  bf16x8 qf[2][NK];
+#pragma unroll
+  for (int rt = 0; rt < 2; ++rt) {
+    const int r = min(rt * 16 + col, T1 - 1);
+    const bf16* qr = q + (size_t)(off + first + r) * d + h * DH + grp * 8;
+#pragma unroll
+    for (int kk = 0; kk < NK; ++kk) qf[rt][kk] = *(const bf16x8*)(qr + kk * 32);
+  }
+  const bf16* kbase = kc + (size_t)(b * H + h) * kv_pad * DH;
+  floatx4 sc[kTvTiles][2][2];   // [tile of this wave][row tile][key half]
+#pragma unroll
+  for (int m = 0; m < kTvTiles; ++m) {
+    const int t = wv + kTvWaves * m;
+#pragma unroll
+    for (int rt = 0; rt < 2; ++rt) sc[m][rt][0] = sc[m][rt][1] = floatx4{0, 0, 0, 0};
+    if (t < ntile) {
+      const bf16* k0 = kbase + (size_t)(32 * t + col) * DH + grp * 8;
+#pragma unroll
+      for (int kk = 0; kk < NK; ++kk) {
+        const bf16x8 kf0 = *(const bf16x8*)(k0 + kk * 32), kf1 = *(const bf16x8*)(k0 + 16 * DH + kk * 32);
+#pragma unroll
+        for (int rt = 0; rt < 2; ++rt) {
+          sc[m][rt][0] = mfma16(qf[rt][kk], kf0, sc[m][rt][0]);
+          sc[m][rt][1] = mfma16(qf[rt][kk], kf1, sc[m][rt][1]);
+        }
+      }
+    }
+  }
+  // row r = rt * 16 + grp * 4 + i sees key j when r < T1 and j <= N + 1 + r
+  auto seen = [&](int m, int rt, int hf, int i) {
+    const int t = wv + kTvWaves * m, r = rt * 16 + grp * 4 + i, j = 32 * t + 16 * hf + col;
+    return t < ntile && r < T1 && j <= N + 1 + r;
+  };
+  // pass 1: row maxima
+#pragma unroll
+  for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      float mx = -INFINITY;
+#pragma unroll
+      for (int m = 0; m < kTvTiles; ++m)
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf)
+          if (seen(m, rt, hf, i)) mx = fmaxf(mx, sc[m][rt][hf][i] * scale);
+      mx = group_max<16>(mx);
+      if (col == 0) red[wv][rt * 16 + grp * 4 + i] = mx;
+    }
+  __syncthreads();
+  if (threadIdx.x < 32) {
+    float mx = red[0][threadIdx.x];
+#pragma unroll
+    for (int w = 1; w < kTvWaves; ++w) mx = fmaxf(mx, red[w][threadIdx.x]);
+    mrow[threadIdx.x] = mx;
+  }
+  __syncthreads();
+  // pass 2: row sums
+#pragma unroll
+  for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = rt * 16 + grp * 4 + i;
+      const float mr = mrow[min(r, 31)];
+      float sm = 0.f;
+#pragma unroll
+      for (int m = 0; m < kTvTiles; ++m)
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf)
+          if (seen(m, rt, hf, i)) sm += __expf(sc[m][rt][hf][i] * scale - mr);
+      sm = group_sum<16>(sm);
+      if (col == 0) red[wv][r] = sm;
+    }
+  __syncthreads();
+  if (threadIdx.x < 32) {
+    float sm = 0.f;
+#pragma unroll
+    for (int w = 0; w < kTvWaves; ++w) sm += red[w][threadIdx.x];
+    lrow[threadIdx.x] = sm;
+  }
+  __syncthreads();
+  // pass 3: per visual key (1 <= j <= N) the sum of the rows' probabilities
+  float* out = tv + (size_t)b * tv_bstride + (size_t)h * N;
+#pragma unroll
+  for (int m = 0; m < kTvTiles; ++m)
+#pragma unroll
+    for (int hf = 0; hf < 2; ++hf) {
+      const int t = wv + kTvWaves * m, j = 32 * t + 16 * hf + col;
+      float cs = 0.f;
+#pragma unroll
+      for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int r = rt * 16 + grp * 4 + i;
+          if (seen(m, rt, hf, i)) cs += __expf(sc[m][rt][hf][i] * scale - mrow[r]) / lrow[r];
+        }
+      cs += __shfl_xor(cs, 16);
+      cs += __shfl_xor(cs, 32);
+      if (grp == 0 && t < ntile && j >= 1 && j <= N) out[j - 1] = cs;
+    }
+}
+
 // Single-query attention of a decode pass at position pos.  One workgroup
 // per (head, episode, value slice): q and the new key arrive un-rotated in
 // fp32; every workgroup rotates them (RoPE, pairing dim i with i + DH/2), the
@@ -339,6 +467,22 @@ hipError_t launch_attn_prefill(const bf16* q, const bf16* kc, const bf16* vc, co
   else if (head_dim == 64)
     hipLaunchKernelGGL(k_attn_prefill<64>, grid, dim3(kAttnWaves * 64), 0, s, q, kc, vc, rows_pos, ep_counts,
                        ep_offsets, H, kv_pad, o, KB);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+hipError_t launch_text_vis(const bf16* q, const bf16* kc, const int* ep_counts, const int* ep_offsets, int B, int H,
+                           int head_dim, int kv_pad, int N, int P, int T1, float* tv, size_t tv_bstride,
+                           hipStream_t s) {
+  if (T1 < 1 || T1 > 32 || N + T1 + 1 > kTvWaves * kTvTiles * 32) return hipErrorInvalidValue;
+  const dim3 grid(H, B);
+  if (head_dim == 128)
+    hipLaunchKernelGGL(k_text_vis<128>, grid, dim3(kTvWaves * 64), 0, s, q, kc, ep_counts, ep_offsets, H, kv_pad, N,
+                       P, T1, tv, tv_bstride);
+  else if (head_dim == 64)
+    hipLaunchKernelGGL(k_text_vis<64>, grid, dim3(kTvWaves * 64), 0, s, q, kc, ep_counts, ep_offsets, H, kv_pad, N,
+                       P, T1, tv, tv_bstride);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();

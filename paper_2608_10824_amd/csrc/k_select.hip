@@ -43,15 +43,25 @@ typedef unsigned __int128 u128;
 struct Permille { int q[128]; };
 
 // One workgroup per episode: static flags, exact ranks, |S|, per-layer masks.
+// With tv (Stage 2), the topk patches of highest score (sum of the LH
+// columns of tv, in order; ties to the lower index) are not static.
 __global__ __launch_bounds__(512) void k_rank_mask(const int* __restrict__ stats, int N, int L, long long tau_num,
                                                    long long tau_den, Permille pm, uint8_t* __restrict__ mask,
-                                                   int* __restrict__ n_static) {
-  extern __shared__ unsigned long long sh[];   // [N] cos^2 numerator, [N] denominator (0 = not static)
+                                                   int* __restrict__ n_static, const float* __restrict__ tv, int LH,
+                                                   int topk) {
+  extern __shared__ unsigned long long sh[];   // [N] cos^2 numerator, [N] denominator (0 = not static), [N] score
   unsigned long long* knum = sh;
   unsigned long long* kden = sh + N;
+  float* score = reinterpret_cast<float*>(sh + 2 * N);
   __shared__ int s_count;
   const int b = blockIdx.x;
   if (threadIdx.x == 0) s_count = 0;
+  if (tv)
+    for (int n = threadIdx.x; n < N; n += blockDim.x) {
+      float sc = 0.f;
+      for (int c = 0; c < LH; ++c) sc += tv[((size_t)b * LH + c) * N + n];
+      score[n] = sc;
+    }
   __syncthreads();
   const unsigned long long num2 = (unsigned long long)(tau_num * tau_num);
   const unsigned long long den2 = (unsigned long long)(tau_den * tau_den);
@@ -65,6 +75,12 @@ __global__ __launch_bounds__(512) void k_rank_mask(const int* __restrict__ stats
       const unsigned long long d2 = (unsigned long long)dot * (unsigned long long)dot;
       const unsigned long long nn = (unsigned long long)na * (unsigned long long)nb;
       if ((u128)d2 * den2 > (u128)nn * num2) { kn = d2; kd = nn; }
+    }
+    if (kd && tv) {   // Stage 2: a task-relevant patch is recomputed
+      const float sn = score[n];
+      int above = 0;
+      for (int j = 0; j < N; ++j) above += score[j] > sn || (score[j] == sn && j < n);
+      if (above < topk) kd = 0;
     }
     knum[n] = kn; kden[n] = kd;
     if (kd) atomicAdd(&s_count, 1);
@@ -99,11 +115,13 @@ hipError_t launch_patch_stats(const uint8_t* ft, const uint8_t* fp, int B, int v
 }
 
 hipError_t launch_rank_mask(const int* stats, int B, int N, int L, long long tau_num, long long tau_den,
-                            const int* permille_host, uint8_t* mask, int* n_static, hipStream_t s) {
+                            const int* permille_host, uint8_t* mask, int* n_static, const float* tv, int LH,
+                            int topk, hipStream_t s) {
   Permille pm;
   for (int l = 0; l < 128; ++l) pm.q[l] = l < L ? permille_host[l] : 0;
-  const size_t shm = (size_t)N * 2 * sizeof(unsigned long long);
-  hipLaunchKernelGGL(k_rank_mask, dim3(B), dim3(512), shm, s, stats, N, L, tau_num, tau_den, pm, mask, n_static);
+  const size_t shm = (size_t)N * 2 * sizeof(unsigned long long) + (size_t)N * sizeof(float);
+  hipLaunchKernelGGL(k_rank_mask, dim3(B), dim3(512), shm, s, stats, N, L, tau_num, tau_den, pm, mask, n_static, tv,
+                     LH, topk);
   return hipGetLastError();
 }
 

@@ -15,7 +15,8 @@ def desc_from(cfg) -> gvc.Desc:
                     ffn=cfg.ffn, vocab=cfg.vocab, n_bins=cfg.n_bins, img=cfg.img, patch=cfg.patch,
                     n_views=cfg.n_views, n_text=cfg.n_text, n_proprio=cfg.n_proprio, n_action_q=cfg.n_action_q,
                     n_decode=cfg.n_decode, parallel_decode=int(cfg.parallel_decode),
-                    norm_full_vocab=int(cfg.norm_full_vocab), rms_eps=cfg.rms_eps, rope_theta=cfg.rope_theta)
+                    norm_full_vocab=int(cfg.norm_full_vocab), rms_eps=cfg.rms_eps, rope_theta=cfg.rope_theta,
+                    task_topk=cfg.task_topk)
 
 
 def _ptr(t):
@@ -115,4 +116,6 @@ class Session:
             return buf.view(torch.int32)
         if item == gvc.STATE_MARGINS:
             return buf.view(torch.float32).view(B, cfg.n_decode)
+        if item == gvc.STATE_TV:
+            return buf.view(torch.float32).view(B, cfg.n_layers, H, cfg.n_patches)
         return buf
