@@ -28,7 +28,7 @@ import numpy as np
 
 from .patches import select_static as _select_one
 from .llama import layer_rows, head_row, rmsnorm
-from .relevance import text_vision_attention, relevant_patches
+from .relevance import text_vision_attention, text_attention_entropy, entropy_permille, relevant_patches
 from .margin import position_margin, reduce_margin, gate_fires
 
 
@@ -76,6 +76,7 @@ class OracleVLA:
         self.tokens = None
         self.recomputed = None     # [B][L] rows recomputed by the last prefill
         self.tv = None             # [B][L][H][N] Stage 2 attention of the last prefill (task_topk > 0)
+        self.ent = None            # [B][L][H] Stage 3 entropy sums of the last prefill (entropy_reuse)
 
     # ---------------------------------------------------------- Stage 1 + 3
     def relevant(self, b, scores=None):
@@ -90,18 +91,28 @@ class OracleVLA:
             scores = self.tv[b].sum(axis=(0, 1))
         return relevant_patches(np.asarray(scores, dtype=np.float64), cfg.task_topk)
 
-    def select_static(self, frame_t, frame_prev, tau=None, permille=None, scores=None):
-        """Per episode: reuse masks [B][L][N] and |S| [B] (Stages 1 and 2).
-        scores [B][N], if given, replace the oracle's own Stage 2 scores."""
+    def layer_permille(self, b):
+        """Stage 3: episode b's per-layer proportions from the last prefill's
+        attention entropy, or None (fixed proportions)."""
+        cfg = self.cfg
+        if not cfg.entropy_reuse or cfg.n_text < 2 or self.ent is None:
+            return None
+        return entropy_permille(self.ent[b], cfg.n_text - 1)
+
+    def select_static(self, frame_t, frame_prev, tau=None, permille=None, scores=None, layer_q=None):
+        """Per episode: reuse masks [B][L][N] and |S| [B] (Stages 1-3).
+        scores [B][N] / layer_q [B][L], if given, replace the oracle's own
+        Stage 2 scores / Stage 3 proportions."""
         cfg = self.cfg
         tau = tau or cfg.tau
-        permille = permille or cfg.permille()
         ft, fp = np.asarray(frame_t), np.asarray(frame_prev)
         masks = np.zeros((cfg.batch, cfg.n_layers, cfg.n_patches), dtype=bool)
         n_static = np.zeros(cfg.batch, dtype=np.int64)
         for b in range(cfg.batch):
             excl = self.relevant(b, None if scores is None else scores[b])
-            masks[b], n_static[b], _, _ = _select_one(ft[b], fp[b], cfg.patch, tau, permille, excl)
+            q = list(layer_q[b]) if layer_q is not None else self.layer_permille(b)
+            q = q or permille or cfg.permille()
+            masks[b], n_static[b], _, _ = _select_one(ft[b], fp[b], cfg.patch, tau, q, excl)
         return masks, n_static
 
     # ---------------------------------------------------------- prompt pass
@@ -132,8 +143,11 @@ class OracleVLA:
         self.head_logits = np.zeros((cfg.batch, len(lay.head_pos), cfg.vocab))
         self.recomputed = np.zeros((cfg.batch, L), dtype=np.int64)
         stage2 = cfg.task_topk > 0 and cfg.n_text >= 2
+        stage3 = cfg.entropy_reuse and cfg.n_text >= 2
         if stage2:
             self.tv = np.zeros((cfg.batch, L, cfg.n_heads, cfg.n_patches))
+        if stage3:
+            self.ent = np.zeros((cfg.batch, L, cfg.n_heads))
         for b in range(cfg.batch):
             use_mask = masks is not None and self.valid[b]
             for l in range(L):
@@ -150,6 +164,10 @@ class OracleVLA:
                     self.tv[b, l] = text_vision_attention(self.w["layers"][l], self.H[l, b], self.K[l, b],
                                                           cfg.n_patches, cfg.n_text, cfg.n_heads, cfg.rms_eps,
                                                           cfg.rope_theta)
+                if stage3:
+                    self.ent[b, l] = text_attention_entropy(self.w["layers"][l], self.H[l, b], self.K[l, b],
+                                                            cfg.n_patches, cfg.n_text, cfg.n_heads, cfg.rms_eps,
+                                                            cfg.rope_theta)
                 self.H[l + 1, b, rows] = out
                 self.recomputed[b, l] = len(rows)
             for i, p in enumerate(lay.head_pos):

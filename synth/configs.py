@@ -41,6 +41,7 @@ class VLAConfig:
     bin_scale_log2: float = -3.625
     norm_full_vocab: bool = True    # softmax normaliser over the full vocabulary
     task_topk: int = 0          # Stage 2: patches with the most instruction attention leave S (0: off)
+    entropy_reuse: bool = False # Stage 3: per-layer proportions from the instruction tokens' attention entropy
 
     @property
     def head_dim(self) -> int:
