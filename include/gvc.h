@@ -69,8 +69,13 @@ enum gvc_state_item {
   GVC_STATE_VALID = 4,   /* int32 [B] cache-valid flags */
   GVC_STATE_ROWS = 5,    /* int32 [L]: rows recomputed per layer by the last prompt pass */
   GVC_STATE_MARGINS = 6, /* fp32 [B][D] per-position margins of the last decode */
-  GVC_STATE_TV = 7       /* fp32 [B][L][n_heads][N] Stage 2 attention of the last prompt pass
+  GVC_STATE_TV = 7,      /* fp32 [B][L][n_heads][N] Stage 2 attention of the last prompt pass
                             (desc.task_topk > 0; the layer argument is ignored) */
+  GVC_STATE_ENTROPY = 8, /* fp32 [B][L][n_heads] Stage 3 signal of the last prompt pass: per head,
+                            the sum over the instruction tokens after the image of their attention
+                            entropy divided by log(keys seen) (desc.entropy_reuse; layer ignored) */
+  GVC_STATE_LAYER_Q = 9  /* int32 [B][L] per-layer reuse proportions (per mille) the last
+                            gvc_select_static applied (desc.entropy_reuse; layer ignored) */
 };
 
 /* Model and workload shape.  Llama-2 block (Sec. V-A backbone): pre-norm
@@ -101,6 +106,13 @@ typedef struct gvc_desc {
                              image (1 <= n_text - 1 <= 32) put on each visual key, and the next
                              gvc_select_static takes the task_topk patches of highest total out of
                              the static set.  0 <= task_topk <= N; N + n_text < 640. */
+  int32_t entropy_reuse;  /* Stage 3 (Sec. III-B): 0 = the caller's fixed proportions; 1 = each
+                             prompt pass also records the normalized attention entropy E_l of those
+                             instruction tokens (mean over heads and tokens of the entropy over the
+                             keys up to the token, divided by log of their count), and the next
+                             gvc_select_static reuses q_l = floor(1000 s_l) per mille in layer l,
+                             s_0 = u_0, s_l = s_{l-1} + (u_l - s_{l-1}) / 2, u_l = 1 - E_l, clamped to
+                             [0, 1]: low-entropy layers reuse more.  Same limits as Stage 2. */
 } gvc_desc;
 
 /* bf16 weights of one decoder layer, canonical [out_features][in_features]. */
@@ -155,7 +167,10 @@ int32_t gvc_init_cache(const gvc_desc* desc, const gvc_weights* weights,
  * that pass is highest (fp32 sums in a fixed order, ties to the lower index)
  * are not static (Stage 2).  Static patches are ranked by cosine,
  * highest first, ties to the lower index; layer l reuses the first
- * floor(reuse_permille[l] * |S| / 1000) of them.
+ * floor(q_l * |S| / 1000) of them, q_l = reuse_permille[l], or with
+ * desc.entropy_reuse, once a prompt pass has run, the per-episode q_l of its
+ * attention entropy (Stage 3, computed on the GPU in fp32; readable as
+ * GVC_STATE_LAYER_Q; reuse_permille is then still validated but not used).
  * reuse_permille: host int32 [L] in [0, 1000], or NULL for 1000 everywhere.
  * reuse_mask: dev uint8 [B][L][N] out (1 = reuse at that layer).
  * n_static: dev int32 [B] out (|S|, after Stage 2), or NULL.

@@ -54,8 +54,10 @@ struct Plan {
   Packed patch, lm;
   size_t embed_off, gains_off, final_gain_off, weight_bytes;
   // state
-  size_t H_off, K_off, V_off, valid_off, margins_off, head_logits_off, rowcount_off, tv_off, state_bytes;
+  size_t H_off, K_off, V_off, valid_off, margins_off, head_logits_off, rowcount_off, tv_off, ent_off, lq_off,
+      state_bytes;
   bool stage2;   // task_topk > 0 and at least one instruction token after the image
+  bool stage3;   // entropy_reuse and at least one instruction token after the image
   size_t layer_kv_elems;
   // workspace
   size_t rows_off, counts_off, epc_off, epo_off, stats_off, x_off, q_off, o_off, r_off, act_off, xdec_off, xf_off,
@@ -102,9 +104,11 @@ int32_t make_plan(const gvc_desc* dsc, Plan& p) {
   p.kv_pad = (p.kv_len + 31) / 32 * 32;
   if (p.kv_pad > 8192) return fail(GVC_EINVAL, "sequence too long");
   if (d.task_topk < 0 || d.task_topk > p.N) return fail(GVC_EINVAL, "task_topk must lie in [0, N]");
+  if (d.entropy_reuse != 0 && d.entropy_reuse != 1) return fail(GVC_EINVAL, "entropy_reuse must be 0 or 1");
   p.stage2 = d.task_topk > 0 && d.n_text >= 2;
-  if (p.stage2 && (d.n_text - 1 > 32 || p.N + d.n_text >= 640 || (dh != 64 && dh != 128)))
-    return fail(GVC_EINVAL, "Stage 2 needs n_text - 1 <= 32 and N + n_text < 640");
+  p.stage3 = d.entropy_reuse && d.n_text >= 2;
+  if ((p.stage2 || p.stage3) && (d.n_text - 1 > 32 || p.N + d.n_text >= 640 || (dh != 64 && dh != 128)))
+    return fail(GVC_EINVAL, "Stages 2 and 3 need n_text - 1 <= 32 and N + n_text < 640");
   p.head_rows = d.parallel_decode ? d.n_action_q : 1;
   p.patch_dim = d.patch * d.patch * 3;
   p.bin_lo = d.vocab - d.n_bins;
@@ -142,6 +146,8 @@ int32_t make_plan(const gvc_desc* dsc, Plan& p) {
   p.head_logits_off = s.take((size_t)p.B * p.head_rows * p.V * 4);
   p.rowcount_off = s.take((size_t)p.L * 4);
   p.tv_off = s.take(p.stage2 ? (size_t)p.B * p.L * p.H * p.N * 4 : 0);
+  p.ent_off = s.take(p.stage3 ? (size_t)p.B * p.L * p.H * 4 : 0);
+  p.lq_off = s.take(p.stage3 ? (size_t)p.B * p.L * 4 : 0);
   p.state_bytes = s.off;
 
   Bump k;
@@ -192,7 +198,7 @@ struct gvc_ctx {
   int persist_wg = 0;
   DecodeArgs dargs{};
   bool persist_ran = false;       // a launch sequence ran since the last check of the abort word
-  bool tv_ready = false;          // a prompt pass has written the Stage 2 signal
+  bool tv_ready = false;          // a prompt pass has written the Stage 2 / Stage 3 signals
   uint32_t abort_word = 0;        // host copy, read by margin_gate
   // launch timing of one kernel class (gvc_profile_begin / _end)
   int prof_cls = -1;
@@ -316,10 +322,12 @@ int32_t run_layer(gvc_ctx* c, int l, const RowMap& rows, int M, float* src, floa
     HIP_TRY(launch_attn_prefill(Q, c->Kc(l), c->Vc(l), rows.pos, epc, epo, p.B, p.H, p.dh, p.kv_pad, max_tiles, O,
                                 p.KBd, c->stream));
   }
-  if (p.stage2) {   // Stage 2 signal of this layer, for the next step's selection
+  if (p.stage2 || p.stage3) {   // Stage 2 / 3 signals of this layer, for the next step's selection
     ProfScope ps(c, GVC_K_STAGE2);
-    HIP_TRY(launch_text_vis(Q, c->Kc(l), epc, epo, p.B, p.H, p.dh, p.kv_pad, p.N, p.P, p.d.n_text - 1,
-                            c->S<float>(p.tv_off) + (size_t)l * p.H * p.N, (size_t)p.L * p.H * p.N, c->stream));
+    float* tv = p.stage2 ? c->S<float>(p.tv_off) + (size_t)l * p.H * p.N : nullptr;
+    float* ent = p.stage3 ? c->S<float>(p.ent_off) + (size_t)l * p.H : nullptr;
+    HIP_TRY(launch_text_vis(Q, c->Kc(l), epc, epo, p.B, p.H, p.dh, p.kv_pad, p.N, p.P, p.d.n_text - 1, tv,
+                            (size_t)p.L * p.H * p.N, ent, (size_t)p.L * p.H, c->stream));
   }
   {
     GemmArgs a = base_args(c);
@@ -641,8 +649,10 @@ int32_t gvc_select_static(gvc_ctx* c, const uint8_t* frame_t, const uint8_t* fra
   ProfScope ps(c, GVC_K_SELECT);
   HIP_TRY(launch_patch_stats(frame_t, frame_prev, p.B, p.d.n_views, p.d.img, p.d.patch, stats, c->stream));
   const float* tv = p.stage2 && c->tv_ready ? c->S<float>(p.tv_off) : nullptr;
+  const float* ent = p.stage3 && c->tv_ready ? c->S<float>(p.ent_off) : nullptr;
   HIP_TRY(launch_rank_mask(stats, p.B, p.N, p.L, tau_num, tau_den, q.data(), reuse_mask, n_static, tv, p.L * p.H,
-                           p.d.task_topk, c->stream));
+                           p.d.task_topk, ent, p.H, p.d.n_text - 1, ent ? c->S<int>(p.lq_off) : nullptr,
+                           c->stream));
   return GVC_OK;
 }
 
@@ -683,7 +693,7 @@ int32_t gvc_step_prefill(gvc_ctx* c, const uint8_t* frame_t, const int32_t* text
                           epo + l * p.B);
     if (r) return r;
   }
-  if (p.stage2) c->tv_ready = true;
+  if (p.stage2 || p.stage3) c->tv_ready = true;
   int32_t r = run_head(c, c->head_rows(), c->H(p.L), p.B * p.head_rows, c->S<float>(p.head_logits_off),
                        GVC_K_PREFILL_HEAD);
   if (r) return r;
@@ -822,6 +832,8 @@ size_t gvc_state_item_bytes(const gvc_ctx* c, int32_t item) {
     case GVC_STATE_ROWS: return (size_t)p.L * 4;
     case GVC_STATE_MARGINS: return (size_t)p.B * p.D * 4;
     case GVC_STATE_TV: return p.stage2 ? (size_t)p.B * p.L * p.H * p.N * 4 : 0;
+    case GVC_STATE_ENTROPY: return p.stage3 ? (size_t)p.B * p.L * p.H * 4 : 0;
+    case GVC_STATE_LAYER_Q: return p.stage3 ? (size_t)p.B * p.L * 4 : 0;
     default: return 0;
   }
 }
@@ -848,6 +860,8 @@ int32_t gvc_read_state(gvc_ctx* c, int32_t item, int32_t layer, void* dst, size_
     case GVC_STATE_ROWS: src = c->S<int>(p.rowcount_off); break;
     case GVC_STATE_MARGINS: src = c->S<float>(p.margins_off); break;
     case GVC_STATE_TV: src = c->S<float>(p.tv_off); break;
+    case GVC_STATE_ENTROPY: src = c->S<float>(p.ent_off); break;
+    case GVC_STATE_LAYER_Q: src = c->S<int>(p.lq_off); break;
   }
   HIP_TRY(hipMemcpyAsync(dst, src, n, hipMemcpyDeviceToDevice, c->stream));
   HIP_TRY(hipStreamSynchronize(c->stream));

@@ -198,8 +198,8 @@ hipError_t launch_patch_stats(const uint8_t* ft, const uint8_t* fp, int B, int v
 // Stage 1 (+ Stage 2 when tv != nullptr: per patch the sum over LH columns of
 // tv [B][LH][N], in order; the topk highest, ties to the lower index, are not static).
 hipError_t launch_rank_mask(const int* stats, int B, int N, int L, long long tau_num, long long tau_den,
-                            const int* permille_dev, uint8_t* mask, int* n_static, const float* tv, int LH,
-                            int topk, hipStream_t s);
+                            const int* permille_host, uint8_t* mask, int* n_static, const float* tv, int LH,
+                            int topk, const float* ent, int H, int n_instr, int* q_out, hipStream_t s);
 
 hipError_t launch_build_rows(const uint8_t* mask, const int* valid, int B, int L, int N, int P,
                              int* rows, int* counts, int* ep_counts, int* ep_offsets, hipStream_t s);
@@ -213,7 +213,7 @@ hipError_t launch_gemm(const GemmArgs& a, int epi, int NT, hipStream_t s);
 // key n (1 <= T1 <= 32, N + T1 < 640).
 hipError_t launch_text_vis(const bf16* q, const bf16* kc, const int* ep_counts, const int* ep_offsets, int B, int H,
                            int head_dim, int kv_pad, int N, int P, int T1, float* tv, size_t tv_bstride,
-                           hipStream_t s);
+                           float* ent, size_t ent_bstride, hipStream_t s);
 hipError_t launch_attn_prefill(const bf16* q, const bf16* kc, const bf16* vc, const int* rows_pos,
                                const int* ep_counts, const int* ep_offsets, int B, int H, int head_dim,
                                int kv_pad, int max_tiles, bf16* o, int KB, hipStream_t s);

@@ -187,7 +187,11 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn_prefill(
 // probabilities over the rows, written to tv[n].  Scores on MFMA as in
 // k_attn_prefill (16-row tiles, key tiles of 32 over the 4 waves, kept in
 // registers); three passes: row maxima, row sums, column sums in a fixed
-// order (deterministic).
+// order (deterministic).  Either output may be null.  ent (Stage 3): per
+// head, the sum over the rows (in order) of each row's entropy divided by
+// log of its key count, the entropy taken as log Z - (sum_j e_j x_j) / Z
+// with x_j the max-shifted score, e_j = exp(x_j) and Z = sum_j e_j (the row
+// sums of pass 2).
 constexpr int kTvWaves = 4, kTvTiles = 5;   // key tiles per wave: keys < 4 * 5 * 32 = 640
 
 template <int DH>
@@ -195,10 +199,11 @@ __global__ __launch_bounds__(kTvWaves * 64) void k_text_vis(const bf16* __restri
                                                            const int* __restrict__ ep_counts,
                                                            const int* __restrict__ ep_offsets, int H, int kv_pad,
                                                            int N, int P, int T1, float* __restrict__ tv,
-                                                           size_t tv_bstride) {
+                                                           size_t tv_bstride, float* __restrict__ ent,
+                                                           size_t ent_bstride) {
   constexpr int NK = DH / 32;
-  __shared__ float red[kTvWaves][32];
-  __shared__ float mrow[32], lrow[32];
+  __shared__ float red[kTvWaves][32], redx[kTvWaves][32];
+  __shared__ float mrow[32], lrow[32], hrow[32];
   const int h = blockIdx.x, b = blockIdx.y;
   const int lane = threadIdx.x & 63, wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int col = lane & 15, grp = lane >> 4;
@@ -269,23 +274,42 @@ __global__ __launch_bounds__(kTvWaves * 64) void k_text_vis(const bf16* __restri
     for (int i = 0; i < 4; ++i) {
       const int r = rt * 16 + grp * 4 + i;
       const float mr = mrow[min(r, 31)];
-      float sm = 0.f;
+      float sm = 0.f, sx = 0.f;
 #pragma unroll
       for (int m = 0; m < kTvTiles; ++m)
 #pragma unroll
         for (int hf = 0; hf < 2; ++hf)
-          if (seen(m, rt, hf, i)) sm += __expf(sc[m][rt][hf][i] * scale - mr);
+          if (seen(m, rt, hf, i)) {
+            const float x = sc[m][rt][hf][i] * scale - mr, e = __expf(x);
+            sm += e;
+            sx += e * x;
+          }
       sm = group_sum<16>(sm);
       if (col == 0) red[wv][r] = sm;
+      if (ent) {
+        sx = group_sum<16>(sx);
+        if (col == 0) redx[wv][r] = sx;
+      }
     }
   __syncthreads();
   if (threadIdx.x < 32) {
-    float sm = 0.f;
+    float sm = 0.f, sx = 0.f;
 #pragma unroll
-    for (int w = 0; w < kTvWaves; ++w) sm += red[w][threadIdx.x];
+    for (int w = 0; w < kTvWaves; ++w) {
+      sm += red[w][threadIdx.x];
+      sx += ent ? redx[w][threadIdx.x] : 0.f;
+    }
     lrow[threadIdx.x] = sm;
+    const int r = threadIdx.x;
+    hrow[r] = r < T1 ? (__logf(sm) - sx / sm) / __logf((float)(N + 2 + r)) : 0.f;
   }
   __syncthreads();
+  if (ent && threadIdx.x == 0) {
+    float e = 0.f;
+    for (int r = 0; r < T1; ++r) e += hrow[r];
+    ent[(size_t)b * ent_bstride + h] = e;
+  }
+  if (!tv) return;
   // pass 3: per visual key (1 <= j <= N) the sum of the rows' probabilities
   float* out = tv + (size_t)b * tv_bstride + (size_t)h * N;
 #pragma unroll
@@ -474,15 +498,15 @@ hipError_t launch_attn_prefill(const bf16* q, const bf16* kc, const bf16* vc, co
 
 hipError_t launch_text_vis(const bf16* q, const bf16* kc, const int* ep_counts, const int* ep_offsets, int B, int H,
                            int head_dim, int kv_pad, int N, int P, int T1, float* tv, size_t tv_bstride,
-                           hipStream_t s) {
-  if (T1 < 1 || T1 > 32 || N + T1 + 1 > kTvWaves * kTvTiles * 32) return hipErrorInvalidValue;
+                           float* ent, size_t ent_bstride, hipStream_t s) {
+  if (T1 < 1 || T1 > 32 || N + T1 + 1 > kTvWaves * kTvTiles * 32 || (!tv && !ent)) return hipErrorInvalidValue;
   const dim3 grid(H, B);
   if (head_dim == 128)
     hipLaunchKernelGGL(k_text_vis<128>, grid, dim3(kTvWaves * 64), 0, s, q, kc, ep_counts, ep_offsets, H, kv_pad, N,
-                       P, T1, tv, tv_bstride);
+                       P, T1, tv, tv_bstride, ent, ent_bstride);
   else if (head_dim == 64)
     hipLaunchKernelGGL(k_text_vis<64>, grid, dim3(kTvWaves * 64), 0, s, q, kc, ep_counts, ep_offsets, H, kv_pad, N,
-                       P, T1, tv, tv_bstride);
+                       P, T1, tv, tv_bstride, ent, ent_bstride);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();

@@ -45,17 +45,39 @@ struct Permille { int q[128]; };
 // One workgroup per episode: static flags, exact ranks, |S|, per-layer masks.
 // With tv (Stage 2), the topk patches of highest score (sum of the LH
 // columns of tv, in order; ties to the lower index) are not static.
+// With ent (Stage 3, [B][L][H] per-head entropy sums over n_instr tokens),
+// the per-layer proportions come from the episode's entropy: E_l = (sum over
+// heads in order) / (H n_instr), u_l = 1 - E_l, s_0 = u_0,
+// s_l = s_{l-1} + (u_l - s_{l-1}) * 0.5, q_l = floor(1000 clamp(s_l, 0, 1)),
+// in fp32 and written to q_out [B][L]; otherwise they are pm.
 __global__ __launch_bounds__(512) void k_rank_mask(const int* __restrict__ stats, int N, int L, long long tau_num,
                                                    long long tau_den, Permille pm, uint8_t* __restrict__ mask,
                                                    int* __restrict__ n_static, const float* __restrict__ tv, int LH,
-                                                   int topk) {
+                                                   int topk, const float* __restrict__ ent, int H, int n_instr,
+                                                   int* __restrict__ q_out) {
   extern __shared__ unsigned long long sh[];   // [N] cos^2 numerator, [N] denominator (0 = not static), [N] score
   unsigned long long* knum = sh;
   unsigned long long* kden = sh + N;
   float* score = reinterpret_cast<float*>(sh + 2 * N);
   __shared__ int s_count;
+  __shared__ int qs[128];
   const int b = blockIdx.x;
-  if (threadIdx.x == 0) s_count = 0;
+  if (threadIdx.x == 0) {
+    s_count = 0;
+    float sl = 0.f;
+    for (int l = 0; l < L; ++l) {
+      if (ent) {
+        float e = 0.f;
+        for (int h = 0; h < H; ++h) e += ent[((size_t)b * L + l) * H + h];
+        const float u = 1.0f - e / (float)(H * n_instr);
+        sl = l == 0 ? u : sl + (u - sl) * 0.5f;
+        qs[l] = (int)floorf(1000.0f * fminf(fmaxf(sl, 0.f), 1.f));
+        q_out[(size_t)b * L + l] = qs[l];
+      } else {
+        qs[l] = pm.q[l];
+      }
+    }
+  }
   if (tv)
     for (int n = threadIdx.x; n < N; n += blockDim.x) {
       float sc = 0.f;
@@ -99,7 +121,7 @@ __global__ __launch_bounds__(512) void k_rank_mask(const int* __restrict__ stats
       }
     }
     for (int l = 0; l < L; ++l) {
-      const int k = (int)(((long long)pm.q[l] * S) / 1000);
+      const int k = (int)(((long long)qs[l] * S) / 1000);
       mask[((size_t)b * L + l) * N + n] = (kd && rank < k) ? 1 : 0;
     }
   }
@@ -116,12 +138,13 @@ hipError_t launch_patch_stats(const uint8_t* ft, const uint8_t* fp, int B, int v
 
 hipError_t launch_rank_mask(const int* stats, int B, int N, int L, long long tau_num, long long tau_den,
                             const int* permille_host, uint8_t* mask, int* n_static, const float* tv, int LH,
-                            int topk, hipStream_t s) {
+                            int topk, const float* ent, int H, int n_instr, int* q_out, hipStream_t s) {
+  if (L > 128 || (ent && (!q_out || H < 1 || n_instr < 1))) return hipErrorInvalidValue;
   Permille pm;
   for (int l = 0; l < 128; ++l) pm.q[l] = l < L ? permille_host[l] : 0;
   const size_t shm = (size_t)N * 2 * sizeof(unsigned long long) + (size_t)N * sizeof(float);
   hipLaunchKernelGGL(k_rank_mask, dim3(B), dim3(512), shm, s, stats, N, L, tau_num, tau_den, pm, mask, n_static, tv,
-                     LH, topk);
+                     LH, topk, ent, H, n_instr, q_out);
   return hipGetLastError();
 }
 

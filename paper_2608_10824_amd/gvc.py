@@ -12,7 +12,8 @@ _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libgvc.so"
 
 GVC_OK, GVC_EINVAL, GVC_ESTATE, GVC_ENOMEM, GVC_EDEVICE = 0, 1, 2, 3, 4
 REDUCE_MEAN, REDUCE_MIN = 0, 1
-STATE_H, STATE_K, STATE_V, STATE_HEAD_LOGITS, STATE_VALID, STATE_ROWS, STATE_MARGINS, STATE_TV = range(8)
+(STATE_H, STATE_K, STATE_V, STATE_HEAD_LOGITS, STATE_VALID, STATE_ROWS, STATE_MARGINS, STATE_TV, STATE_ENTROPY,
+ STATE_LAYER_Q) = range(10)
 
 (K_DECODE_QKV, K_DECODE_ATTN, K_DECODE_O, K_DECODE_GU, K_DECODE_DOWN, K_DECODE_HEAD, K_PREFILL_QKV,
  K_PREFILL_ATTN, K_PREFILL_O, K_PREFILL_GU, K_PREFILL_DOWN, K_PREFILL_HEAD, K_EMBED, K_NORM, K_SELECT,
@@ -33,7 +34,8 @@ class Desc(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in (
         "batch", "n_layers", "d_model", "n_heads", "ffn", "vocab", "n_bins", "img", "patch", "n_views",
         "n_text", "n_proprio", "n_action_q", "n_decode", "parallel_decode", "norm_full_vocab")] + [
-        ("rms_eps", ctypes.c_float), ("rope_theta", ctypes.c_float), ("task_topk", ctypes.c_int32)]
+        ("rms_eps", ctypes.c_float), ("rope_theta", ctypes.c_float), ("task_topk", ctypes.c_int32),
+        ("entropy_reuse", ctypes.c_int32)]
 
 
 class LayerWeights(ctypes.Structure):

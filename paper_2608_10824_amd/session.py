@@ -16,7 +16,7 @@ def desc_from(cfg) -> gvc.Desc:
                     n_views=cfg.n_views, n_text=cfg.n_text, n_proprio=cfg.n_proprio, n_action_q=cfg.n_action_q,
                     n_decode=cfg.n_decode, parallel_decode=int(cfg.parallel_decode),
                     norm_full_vocab=int(cfg.norm_full_vocab), rms_eps=cfg.rms_eps, rope_theta=cfg.rope_theta,
-                    task_topk=cfg.task_topk)
+                    task_topk=cfg.task_topk, entropy_reuse=int(cfg.entropy_reuse))
 
 
 def _ptr(t):
@@ -118,4 +118,8 @@ class Session:
             return buf.view(torch.float32).view(B, cfg.n_decode)
         if item == gvc.STATE_TV:
             return buf.view(torch.float32).view(B, cfg.n_layers, H, cfg.n_patches)
+        if item == gvc.STATE_ENTROPY:
+            return buf.view(torch.float32).view(B, cfg.n_layers, H)
+        if item == gvc.STATE_LAYER_Q:
+            return buf.view(torch.int32).view(B, cfg.n_layers)
         return buf
