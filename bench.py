@@ -39,7 +39,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-c3", action="store_true", help="skip the C3 episode (recompute rate)")
-    ap.add_argument("--no-stage2", action="store_true", help="skip the Stage 2 (top-k = 120) steps")
+    ap.add_argument("--no-stage2", action="store_true",
+                    help="skip the Stage 2 (top-k = 120) and Stage 2 + entropy Stage 3 steps")
     return ap.parse_args()
 
 
@@ -134,16 +135,17 @@ def c3_episode(dev):
             "tau": "%d/%d" % cfg.tau, "theta": cfg.theta}
 
 
-def stage2_steps(cfg, w, si, dev, steps, warmup):
+def staged_steps(cfg, w, si, dev, steps, warmup, entropy=False):
     """The C2 workload with Stage 2 on (the paper's top-k = 120): Stage 1's
     128 static patches minus those among the 120 that drew the most
-    instruction attention in the previous pass.  Reports the time per
-    control step, the patches left static, the rows recomputed per layer and
-    the signal kernel's time per layer."""
+    instruction attention in the previous pass; with entropy, Stage 3's
+    per-layer proportions come from the previous pass's attention entropy.
+    Reports the time per control step, the patches left static, the rows
+    recomputed per layer and the signal kernel's time per layer."""
     import torch
     from paper_2608_10824_amd import gvc
     from paper_2608_10824_amd.session import Session
-    cfg2 = cfg.with_(task_topk=120)
+    cfg2 = cfg.with_(task_topk=120, entropy_reuse=entropy)
     s = Session(cfg2, w, device=dev)
     torch.cuda.synchronize()
     fp, ft = si["frame_prev"].to(dev), si["frame_t"].to(dev)
@@ -167,14 +169,19 @@ def stage2_steps(cfg, w, si, dev, steps, warmup):
     dt = time.perf_counter() - t0
     n_static = int(s.n_static[0].item())
     rows = s.read(gvc.STATE_ROWS).cpu().tolist()
+    layer_q = s.read(gvc.STATE_LAYER_Q)[0].cpu().tolist() if entropy else None
     gvc.profile_begin(s.ctx, gvc.K_STAGE2, cfg.n_layers * 2 + 8)
     step()
     torch.cuda.synchronize()
     sig_ms, sig_n = gvc.profile_end(s.ctx)
     s.close()
-    return {"task_topk": 120, "ms_per_step": dt * 1e3 / steps, "steps": steps, "static_patches": n_static,
-            "recomputed_rows_per_layer": rows[0], "signal_us_per_layer": sig_ms * 1e3 / max(sig_n, 1),
-            "signal_launches_per_step": sig_n}
+    out = {"task_topk": 120, "ms_per_step": dt * 1e3 / steps, "steps": steps, "static_patches": n_static,
+           "recomputed_rows_per_layer": rows[0] if not entropy else rows,
+           "signal_us_per_layer": sig_ms * 1e3 / max(sig_n, 1), "signal_launches_per_step": sig_n}
+    if entropy:
+        out["entropy_reuse"] = True
+        out["layer_permille"] = layer_q
+    return out
 
 
 def stored_traffic(kernel_sources):
@@ -346,8 +353,10 @@ def main():
     del s
     torch.cuda.empty_cache()
     if w_stage2 is not None:
-        out["stage2"] = stage2_steps(cfg, w_stage2, si, dev, min(args.steps, 10), 2)
+        out["stage2"] = staged_steps(cfg, w_stage2, si, dev, min(args.steps, 10), 2)
         note("Stage 2 steps done: %d static patches left" % out["stage2"]["static_patches"])
+        out["stage3_entropy"] = staged_steps(cfg, w_stage2, si, dev, min(args.steps, 10), 2, entropy=True)
+        note("Stage 2 + 3 steps done: layer proportions %s" % out["stage3_entropy"]["layer_permille"][:4])
         del w_stage2
         torch.cuda.empty_cache()
     if not args.no_c3:
