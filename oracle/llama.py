@@ -30,12 +30,12 @@ def rope_row(x: np.ndarray, pos: int, base: float) -> np.ndarray:
     return np.concatenate([a * c - b * s, b * c + a * s], axis=1)
 
 
-def attend_row(q: np.ndarray, pos: int, K: np.ndarray, V: np.ndarray) -> np.ndarray:
-    """Causal attention of one query row [H][d_h] at position pos over the key
-    slots 0..pos of K, V ([T][H][d_h])."""
+def attend_row(q: np.ndarray, last: int, K: np.ndarray, V: np.ndarray) -> np.ndarray:
+    """Attention of one query row [H][d_h] over the key slots 0..last of K, V
+    ([T][H][d_h]); causal when last is the row's own position."""
     H, dh = q.shape
-    k = K[: pos + 1]                     # [pos+1][H][dh]
-    v = V[: pos + 1]
+    k = K[: last + 1]                    # [last+1][H][dh]
+    v = V[: last + 1]
     s = np.einsum("hd,thd->ht", q, k) / np.sqrt(dh)
     s = s - s.max(axis=1, keepdims=True)
     p = np.exp(s)
@@ -48,11 +48,12 @@ def silu(x):
 
 
 def layer_rows(w: dict, h_in: np.ndarray, rows, pos, K: np.ndarray, V: np.ndarray,
-               n_heads: int, eps: float, base: float) -> np.ndarray:
+               n_heads: int, eps: float, base: float, key_last=None) -> np.ndarray:
     """One decoder layer over the row set `rows` (indices into h_in) at the
     absolute positions `pos`, writing fresh K/V into the slots `pos` of the
     persistent K, V arrays and attending over all slots up to each row's
-    position.  Returns the layer outputs [len(rows)][d]."""
+    position (or up to key_last[i] when given: a bidirectional block).
+    Returns the layer outputs [len(rows)][d]."""
     d = h_in.shape[-1]
     dh = d // n_heads
     qs = []
@@ -68,7 +69,7 @@ def layer_rows(w: dict, h_in: np.ndarray, rows, pos, K: np.ndarray, V: np.ndarra
         V[p] = v
     out = np.empty((len(rows), d))
     for i, (r, p) in enumerate(zip(rows, pos)):
-        o = attend_row(qs[i], p, K, V).reshape(d)
+        o = attend_row(qs[i], p if key_last is None else key_last[i], K, V).reshape(d)
         res = h_in[r] + w["wo"] @ o
         rn = rmsnorm(res, w["ffn_norm"], eps)
         out[i] = res + w["wd"] @ (silu(w["wg"] @ rn) * (w["wu"] @ rn))

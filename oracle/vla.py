@@ -116,6 +116,19 @@ class OracleVLA:
         return masks, n_static
 
     # ---------------------------------------------------------- prompt pass
+    def key_last(self, rows):
+        """Last key slot each row attends to: its own position (causal), or,
+        for the OFT model's parallel action-dimension decoding (Sec. V-A,
+        models and baselines; the mask is not given there, the reading is
+        that the action-query rows see each other both ways), the last
+        prompt position for the action-query rows.  None when every row is
+        causal."""
+        cfg = self.cfg
+        if not cfg.action_bidir:
+            return None
+        a0 = self.lay.P - cfg.n_action_q
+        return [self.lay.P - 1 if p >= a0 else p for p in rows]
+
     def embed_row(self, b, pos, frame_t, text_ids, extra_rows):
         cfg, lay = self.cfg, self.lay
         N = cfg.n_patches
@@ -159,7 +172,8 @@ class OracleVLA:
                     for p in rows:
                         self.H[0, b, p] = self.embed_row(b, p, frame_t, text_ids, extra_rows)
                 out = layer_rows(self.w["layers"][l], self.H[l, b], rows, rows,
-                                 self.K[l, b], self.V[l, b], cfg.n_heads, cfg.rms_eps, cfg.rope_theta)
+                                 self.K[l, b], self.V[l, b], cfg.n_heads, cfg.rms_eps, cfg.rope_theta,
+                                 self.key_last(rows))
                 if stage2:
                     self.tv[b, l] = text_vision_attention(self.w["layers"][l], self.H[l, b], self.K[l, b],
                                                           cfg.n_patches, cfg.n_text, cfg.n_heads, cfg.rms_eps,

@@ -42,6 +42,7 @@ class VLAConfig:
     norm_full_vocab: bool = True    # softmax normaliser over the full vocabulary
     task_topk: int = 0          # Stage 2: patches with the most instruction attention leave S (0: off)
     entropy_reuse: bool = False # Stage 3: per-layer proportions from the instruction tokens' attention entropy
+    action_bidir: bool = False  # OFT action block: the action-query rows attend to each other both ways
 
     @property
     def head_dim(self) -> int:
