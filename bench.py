@@ -39,6 +39,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-c3", action="store_true", help="skip the C3 episode (recompute rate)")
+    ap.add_argument("--no-c4", action="store_true", help="skip the C4 action-chunk queries")
     ap.add_argument("--no-stage2", action="store_true",
                     help="skip the Stage 2 (top-k = 120) and Stage 2 + entropy Stage 3 steps")
     return ap.parse_args()
@@ -133,6 +134,54 @@ def c3_episode(dev):
             "prompt_len": cfg.prompt_len, "ms_per_step": dt * 1e3 / (n - 1),
             "reuse_permille": "%d -> %d over the layers" % (cfg.permille()[0], cfg.permille()[-1]),
             "tau": "%d/%d" % cfg.tau, "theta": cfg.theta}
+
+
+def c4_chunk(dev, steps, warmup):
+    """The OFT-style action chunk at the 7B shape (two views, 512 visual + 20
+    text tokens, a proprio row and 56 action-query rows, 307 static patches
+    reused): one query is gate -> Stage 1 -> partial prompt pass -> the 56
+    head rows, decoded in parallel with the action rows attending to each
+    other both ways; executing the 8-step chunk means one query per 8
+    control steps.  Reports the time per query, queries/s and the control
+    steps/s that chunked execution gives."""
+    import torch
+    import synth
+    from paper_2608_10824_amd import gvc
+    from paper_2608_10824_amd.session import Session
+    cfg = synth.config_c4().with_(action_bidir=True)
+    w = synth.model_weights(cfg, device=dev)
+    s = Session(cfg, w, device=dev)
+    torch.cuda.synchronize()
+    del w
+    torch.cuda.empty_cache()
+    note("C4 weights generated")
+    si = synth.step_inputs(cfg, 307)
+    fp, ft = si["frame_prev"].to(dev), si["frame_t"].to(dev)
+    ids, ex = si["text_ids"].to(dev), si["extra_rows"].to(dev)
+    s.step_prefill(fp, ids, ex)
+    s.decode_actions()
+
+    def query():
+        s.margin_gate(force=[0])
+        mask, _ = s.select_static(ft, fp)
+        s.step_prefill(ft, ids, ex, mask)
+        s.decode_actions()
+
+    for _ in range(warmup):
+        query()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        query()
+    torch.cuda.synchronize()
+    dt = (time.perf_counter() - t0) / steps
+    rows = s.read(gvc.STATE_ROWS).cpu().tolist()
+    s.close()
+    chunk = cfg.n_action_q // 7
+    return {"prompt_len": cfg.prompt_len, "action_rows": cfg.n_action_q, "action_bidir": True,
+            "static_patches_reused": 307, "recomputed_rows_per_layer": rows[0], "ms_per_query": dt * 1e3,
+            "queries_per_s": 1.0 / dt, "chunk_steps": chunk, "control_steps_per_s_chunked": chunk / dt,
+            "steps": steps}
 
 
 def staged_steps(cfg, w, si, dev, steps, warmup, entropy=False):
@@ -359,6 +408,9 @@ def main():
         note("Stage 2 + 3 steps done: layer proportions %s" % out["stage3_entropy"]["layer_permille"][:4])
         del w_stage2
         torch.cuda.empty_cache()
+    if not args.no_c4:
+        out["c4_chunk"] = c4_chunk(dev, min(args.steps, 10), 2)
+        note("C4 chunk queries done: %.2f ms per query" % out["c4_chunk"]["ms_per_query"])
     if not args.no_c3:
         out["c3"] = c3_episode(dev)
         note("C3 episode done: recompute rate %.3f" % out["c3"]["recompute_rate"])

@@ -113,6 +113,10 @@ typedef struct gvc_desc {
                              gvc_select_static reuses q_l = floor(1000 s_l) per mille in layer l,
                              s_0 = u_0, s_l = s_{l-1} + (u_l - s_{l-1}) / 2, u_l = 1 - E_l, clamped to
                              [0, 1]: low-entropy layers reuse more.  Same limits as Stage 2. */
+  int32_t action_bidir;   /* OFT action block (Sec. V-A, parallel action-dimension decoding): 0 = every
+                             row causal; 1 = the n_action_q action-query rows (the last rows of the
+                             prompt) attend to every prompt key, so they see each other both ways.
+                             Needs parallel_decode = 1 and n_action_q >= 1. */
 } gvc_desc;
 
 /* bf16 weights of one decoder layer, canonical [out_features][in_features]. */

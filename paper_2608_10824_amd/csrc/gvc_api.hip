@@ -58,6 +58,7 @@ struct Plan {
       state_bytes;
   bool stage2;   // task_topk > 0 and at least one instruction token after the image
   bool stage3;   // entropy_reuse and at least one instruction token after the image
+  int block_first, block_last;   // bidirectional action block [block_first, P - 1], or empty
   size_t layer_kv_elems;
   // workspace
   size_t rows_off, counts_off, epc_off, epo_off, stats_off, x_off, q_off, o_off, r_off, act_off, xdec_off, xf_off,
@@ -105,6 +106,11 @@ int32_t make_plan(const gvc_desc* dsc, Plan& p) {
   if (p.kv_pad > 8192) return fail(GVC_EINVAL, "sequence too long");
   if (d.task_topk < 0 || d.task_topk > p.N) return fail(GVC_EINVAL, "task_topk must lie in [0, N]");
   if (d.entropy_reuse != 0 && d.entropy_reuse != 1) return fail(GVC_EINVAL, "entropy_reuse must be 0 or 1");
+  if (d.action_bidir != 0 && d.action_bidir != 1) return fail(GVC_EINVAL, "action_bidir must be 0 or 1");
+  if (d.action_bidir && (!d.parallel_decode || d.n_action_q < 1))
+    return fail(GVC_EINVAL, "action_bidir needs parallel_decode and n_action_q >= 1");
+  p.block_first = d.action_bidir ? p.P - d.n_action_q : p.P;
+  p.block_last = p.P - 1;
   p.stage2 = d.task_topk > 0 && d.n_text >= 2;
   p.stage3 = d.entropy_reuse && d.n_text >= 2;
   if ((p.stage2 || p.stage3) && (d.n_text - 1 > 32 || p.N + d.n_text >= 640 || (dh != 64 && dh != 128)))
@@ -320,7 +326,7 @@ int32_t run_layer(gvc_ctx* c, int l, const RowMap& rows, int M, float* src, floa
   {
     ProfScope ps(c, k0 + 1);
     HIP_TRY(launch_attn_prefill(Q, c->Kc(l), c->Vc(l), rows.pos, epc, epo, p.B, p.H, p.dh, p.kv_pad, max_tiles, O,
-                                p.KBd, c->stream));
+                                p.KBd, p.block_first, p.block_last, c->stream));
   }
   if (p.stage2 || p.stage3) {   // Stage 2 / 3 signals of this layer, for the next step's selection
     ProfScope ps(c, GVC_K_STAGE2);

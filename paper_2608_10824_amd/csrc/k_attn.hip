@@ -7,7 +7,9 @@
 // whose queries are an arbitrary, position-sorted subset of the prompt.
 //
 // Prefill: one workgroup per (episode, head, 16 query rows), its waves
-// splitting the key tiles.  S = Q K^T and O += P V
+// splitting the key tiles.  Rows at positions >= block_first form a
+// bidirectional block: they see every key up to block_last (the OFT action
+// chunk decoded in parallel); block_first > block_last leaves all causal.  S = Q K^T and O += P V
 // run on MFMA v_mfma_f32_16x16x32_bf16 over key tiles of 32 with an fp32
 // online softmax; P is re-laid out through a 1 KiB LDS tile into the A
 // operand order; V is stored transposed so the B operand of P V is 16
@@ -26,7 +28,7 @@ template <int DH>
 __global__ __launch_bounds__(kAttnWaves * 64) void k_attn_prefill(
     const bf16* __restrict__ q, const bf16* __restrict__ kc, const bf16* __restrict__ vc,
     const int* __restrict__ rows_pos, const int* __restrict__ ep_counts, const int* __restrict__ ep_offsets, int H,
-    int kv_pad, bf16* __restrict__ o, int KB) {
+    int kv_pad, bf16* __restrict__ o, int KB, int block_first, int block_last) {
   constexpr int NK = DH / 32;   // k-steps of QK^T
   constexpr int NO = DH / 16;   // output column blocks
   static_assert(NO % kAttnWaves == 0, "output blocks per merging wave");
@@ -42,13 +44,15 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn_prefill(
   const int col = lane & 15, grp = lane >> 4;
   const int d = H * DH;
   const int last = min(cnt, tile * 16 + 16) - 1;     // last valid row of the tile
-  const int max_pos = rows_pos[off + last];
+  // last key a row at position p sees (non-decreasing in p; rows are sorted)
+  auto key_last = [&](int p) { return p >= block_first ? block_last : p; };
+  const int max_pos = key_last(rows_pos[off + last]);
   // this lane's rows in the C layout
   int qpos[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int r = min(tile * 16 + grp * 4 + i, last);
-    qpos[i] = rows_pos[off + r];
+    qpos[i] = key_last(rows_pos[off + r]);
   }
   // Q fragments (A operand): row col, dims grp*8 + 32*kk
   bf16x8 qf[NK];
@@ -483,14 +487,15 @@ __global__ __launch_bounds__(512) void k_attn_decode(const float* __restrict__ q
 
 hipError_t launch_attn_prefill(const bf16* q, const bf16* kc, const bf16* vc, const int* rows_pos,
                                const int* ep_counts, const int* ep_offsets, int B, int H, int head_dim, int kv_pad,
-                               int max_tiles, bf16* o, int KB, hipStream_t s) {
+                               int max_tiles, bf16* o, int KB, int block_first, int block_last, hipStream_t s) {
+  if (block_first <= block_last && block_last >= kv_pad) return hipErrorInvalidValue;
   dim3 grid(max_tiles, H, B);
   if (head_dim == 128)
     hipLaunchKernelGGL(k_attn_prefill<128>, grid, dim3(kAttnWaves * 64), 0, s, q, kc, vc, rows_pos, ep_counts,
-                       ep_offsets, H, kv_pad, o, KB);
+                       ep_offsets, H, kv_pad, o, KB, block_first, block_last);
   else if (head_dim == 64)
     hipLaunchKernelGGL(k_attn_prefill<64>, grid, dim3(kAttnWaves * 64), 0, s, q, kc, vc, rows_pos, ep_counts,
-                       ep_offsets, H, kv_pad, o, KB);
+                       ep_offsets, H, kv_pad, o, KB, block_first, block_last);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();

@@ -35,7 +35,7 @@ class Desc(ctypes.Structure):
         "batch", "n_layers", "d_model", "n_heads", "ffn", "vocab", "n_bins", "img", "patch", "n_views",
         "n_text", "n_proprio", "n_action_q", "n_decode", "parallel_decode", "norm_full_vocab")] + [
         ("rms_eps", ctypes.c_float), ("rope_theta", ctypes.c_float), ("task_topk", ctypes.c_int32),
-        ("entropy_reuse", ctypes.c_int32)]
+        ("entropy_reuse", ctypes.c_int32), ("action_bidir", ctypes.c_int32)]
 
 
 class LayerWeights(ctypes.Structure):

@@ -16,7 +16,8 @@ def desc_from(cfg) -> gvc.Desc:
                     n_views=cfg.n_views, n_text=cfg.n_text, n_proprio=cfg.n_proprio, n_action_q=cfg.n_action_q,
                     n_decode=cfg.n_decode, parallel_decode=int(cfg.parallel_decode),
                     norm_full_vocab=int(cfg.norm_full_vocab), rms_eps=cfg.rms_eps, rope_theta=cfg.rope_theta,
-                    task_topk=cfg.task_topk, entropy_reuse=int(cfg.entropy_reuse))
+                    task_topk=cfg.task_topk, entropy_reuse=int(cfg.entropy_reuse),
+                    action_bidir=int(cfg.action_bidir))
 
 
 def _ptr(t):

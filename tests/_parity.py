@@ -104,8 +104,12 @@ def check_layer_sampled(cfg, wl, h_in, h_out, K, V, sample_pos):
     keys) and compare fresh K/V and the layer output.  Returns the errors."""
     from oracle.llama import layer_rows
     Ko, Vo = K.copy(), V.copy()
+    key_last = None
+    if cfg.action_bidir:   # the action-query rows see every prompt key
+        a0 = cfg.prompt_len - cfg.n_action_q
+        key_last = [cfg.prompt_len - 1 if p >= a0 else p for p in sample_pos]
     out = layer_rows(wl, h_in, list(sample_pos), list(sample_pos), Ko, Vo, cfg.n_heads, cfg.rms_eps,
-                     cfg.rope_theta)
+                     cfg.rope_theta, key_last)
     sp = list(sample_pos)
     errs = {"k": rel_err(K[sp], Ko[sp]), "v": rel_err(V[sp], Vo[sp]), "out": rel_err(h_out[sp], out)}
     return errs

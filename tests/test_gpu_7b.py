@@ -151,10 +151,10 @@ def test_c2_head_and_decode_chain(c2):
 
 
 # ---------------------------------------------------------------- C4
-@pytest.fixture(scope="module")
-def c4():
+@pytest.fixture(scope="module", params=["causal", "bidir"])
+def c4(request):
     from paper_2608_10824_amd import gvc
-    cfg = synth.config_c4()
+    cfg = synth.config_c4().with_(action_bidir=request.param == "bidir")
     s, w = _session(cfg)
     si = synth.step_inputs(cfg, 307)
     fp, ft, ids, ex = _two_steps(cfg, s, si)
@@ -182,7 +182,9 @@ def test_c4_masks_counts_layers(c4):
     assert np.array_equal(c4["mask"], mo) and c4["n_static"].tolist() == ns.tolist() == [307]
     assert c4["rows"].tolist() == [cfg.prompt_len - 307] * cfg.n_layers
     recomputed = [p for p in range(cfg.prompt_len) if not (1 <= p <= cfg.n_patches and mo[0, 0, p - 1])]
-    sample = _sample_rows(cfg, recomputed) + [cfg.n_patches + cfg.n_text]      # the proprio row
+    # plus the proprio row and the first action-query row (with the block it
+    # sees all the later action rows)
+    sample = _sample_rows(cfg, recomputed) + [cfg.n_patches + cfg.n_text, cfg.prompt_len - cfg.n_action_q]
     for l in c4["layers"]:
         errs = check_layer_sampled(cfg, layer_w64(c4["w"], l), c4["H"][l], c4["H"][l + 1], c4["K"][l], c4["V"][l],
                                    sorted(set(sample)))

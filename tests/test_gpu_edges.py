@@ -30,12 +30,24 @@ def _state(s, cfg):
     return H, K, V, s.read(gvc.STATE_HEAD_LOGITS).cpu().numpy()
 
 
-def test_parallel_action_chunk_complete_parity():
-    """Two views, a proprio row and 8 action-query rows decoded in one pass
-    (the OFT variant, Sec. V-A): state, the 8 positions' logits, tokens,
-    margins and the minimum-margin gate."""
+def _chunk_cfg(name):
+    if name == "C4T":
+        return synth.config_c4_tiny()
+    if name == "C4T-bidir":
+        return synth.config_c4_tiny().with_(action_bidir=True)
+    # heads of 128 and a 56-row block that starts inside a 16-row tile
+    return synth.config_mid().with_(n_proprio=1, n_action_q=56, n_decode=56, parallel_decode=True,
+                                    reduce_min=True, action_bidir=True)
+
+
+@pytest.mark.parametrize("name", ["C4T", "C4T-bidir", "MID-bidir"])
+def test_parallel_action_chunk_complete_parity(name):
+    """Two views, a proprio row and the action-query rows decoded in one pass
+    (the OFT variant, Sec. V-A), causal or with the action rows attending to
+    each other both ways: state, every position's logits, tokens, margins
+    and the minimum-margin gate."""
     from paper_2608_10824_amd import gvc
-    cfg = synth.config_c4_tiny()
+    cfg = _chunk_cfg(name)
     w = synth.model_weights(cfg)
     si = synth.step_inputs(cfg, 90)
     s = _session(cfg, w)
@@ -53,9 +65,23 @@ def test_parallel_action_chunk_complete_parity():
     s.step_prefill(ft.to(DEV), ids.to(DEV), ex.to(DEV), mask)
     o.step_prefill(ft.numpy(), ids.numpy(), ex.numpy(), mo)
     H, K, V, z = _state(s, cfg)
+    P = cfg.prompt_len
     for l in range(cfg.n_layers + 1):
         assert rel_err(H[l], o.H[l]) <= TOL
+    for l in range(cfg.n_layers):
+        assert rel_err(K[l][:, :, :P], o.K[l].transpose(0, 2, 1, 3)[:, :, :P]) <= TOL
     assert rel_err(z, o.head_logits) <= TOL
+    if cfg.action_bidir:
+        # the block is really applied: the action rows sit much closer to the
+        # oracle with the block than to the oracle without it
+        oc = OracleVLA(cfg.with_(action_bidir=False), w)
+        oc.step_prefill(fp.numpy(), ids.numpy(), ex.numpy())
+        oc.step_prefill(ft.numpy(), ids.numpy(), ex.numpy(), mo)
+        a0, L = P - cfg.n_action_q, cfg.n_layers
+        e_block = rel_err(H[L][:, a0:], o.H[L][:, a0:])
+        e_causal = rel_err(o.H[L][:, a0:], oc.H[L][:, a0:])
+        print("%s action rows: err %.2e, causal distance %.2e" % (name, e_block, e_causal))
+        assert e_block < e_causal / 4
     tok, mg, lg = s.decode_actions(logits=True)
     tok_o, mg_o, lg_o = o.decode_actions()
     torch.cuda.synchronize()
