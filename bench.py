@@ -23,7 +23,8 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
 # sources of the dominant kernel; its stored traffic figure is used only while they are unchanged
-KERNEL_SOURCES = ("paper_2608_10824_amd/csrc/k_decode.hip", "paper_2608_10824_amd/csrc/gvc_kernels.h")
+KERNEL_SOURCES = ("paper_2608_10824_amd/csrc/k_decode.hip", "paper_2608_10824_amd/csrc/gvc_kernels.h",
+                  "paper_2608_10824_amd/csrc/gvc_decode.h")
 BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 
 

@@ -92,100 +92,8 @@ __device__ __forceinline__ float group_max(float v) {
   return v;
 }
 
-// ------------------------------------------------------------------ GEMM
-// Work units of a GEMM launch.  Pair maps give a workgroup two 16-row weight
-// blocks whose epilogue partners share lanes; single maps give it one block.
-enum { MAP_PLAIN = 0, MAP_QKV = 1, MAP_GU = 2, MAP_SINGLE = 3, MAP_QKV_SINGLE = 4 };
-enum { EPI_QKV = 0, EPI_RESID = 1, EPI_SILU = 2, EPI_STORE = 3, EPI_EMBED = 4, EPI_QKV_RAW = 5 };
-
-struct RowMap {
-  const int* idx;   // row index into the residual / output arrays
-  const int* ep;    // episode b
-  const int* pos;   // absolute position
-};
-
-struct EpiArgs {
-  RowMap rows;
-  // EPI_QKV (and EPI_QKV_RAW: q, k before RoPE as fp32 [M][d] in qraw, kraw)
-  float* qraw; float* kraw;
-  bf16* q;            // [Mp][d] row-major, after RoPE
-  bf16* kc;           // this layer's K cache
-  bf16* vc;           // this layer's V cache (transposed)
-  const float2* rope; // [kv_pad][head_dim/2] (cos, sin)
-  int d, head_dim, n_heads, kv_pad;
-  // EPI_RESID: out[row] = resid[row] + acc, rows mapped through rows.idx when *_mapped
-  const float* resid; int resid_mapped;
-  float* out; int out_mapped;
-  // EPI_SILU: frag-layout bf16 activations with kb_act k-fragments per row block
-  bf16* act; int kb_act; int n_feat;
-  // EPI_STORE
-  float* store; int ld_store;
-  // EPI_EMBED
-  float* h0; const bf16* embed; const int* text_ids; const float* extra;
-  int n_patches, n_text, n_extra;
-  // Folded RMSNorm (decode): the GEMM input is bf16(x * gain) and the
-  // accumulator is scaled by 1/sqrt(sum(x^2)/norm_dim + norm_eps), the sum
-  // of squares of row m being the sum of ssq_in[m * ssq_parts + 0..parts-1].
-  const float* ssq_in; int ssq_parts; float norm_eps; int norm_dim;
-  // EPI_RESID, when xn != nullptr: also writes bf16(out * xn_gain) in frag
-  // layout (xn_kb k-fragments) and, per row, this pair's sum of squares of
-  // out into ssq_out[m * ssq_out_parts + pair].
-  bf16* xn; const float* xn_gain; float* ssq_out; int xn_kb; int ssq_out_parts;
-};
-
-struct GemmArgs {
-  const bf16x8* w[3];   // packed matrices (fragment units)
-  int wblk[3];          // 16-row blocks per matrix
-  int map;
-  int n_pairs;          // work units (pairs, or single blocks for the single maps)
-  int n_out;            // output features of the (first) matrix, for MAP_PLAIN
-  int KB;               // k-fragments (K padded / 32)
-  int splits, kb_per_split;   // waves per workgroup (token groups x k shares), k-steps per share
-  int tgroups;                // token groups per workgroup (KT)
-  const bf16x8* x;      // frag-layout activations
-  int M, mblocks, mtiles;
-  EpiArgs e;
-};
-
-// k-steps per pipelined register chunk for a tile of NT blocks of 16 token rows.
-constexpr int gemm_pf(int NT) { return NT == 1 ? 8 : (NT <= 3 ? 4 : (NT <= 6 ? 2 : 1)); }
-
-// ------------------------------------------------------------------ persistent decode pass
-// One single-token pass over all layers for one episode (k_decode.hip).
-constexpr int kDecodeMaxSeg = 8;       // weight blocks per workgroup per step
-constexpr int kDecodeAbortWord = 512;  // barrier words: abort flag
-constexpr int kDecodeXccWord = 544;    // barrier words: set when a workgroup is not on XCD blockIdx % 8
-constexpr int kDecodeHeadWord = 1024;  // barrier words: per-head counters, 32 words apart
-constexpr int kDecodeMaxHeads = 64;
-constexpr int kDecodeBarWords = kDecodeHeadWord + 32 * kDecodeMaxHeads;   // zeroed before a launch sequence
-// grid barriers and per-head barriers of one pass over L layers
-constexpr int decode_grid_barriers(int L) { return 1 + 3 * L; }
-constexpr int decode_head_barriers(int L) { return L; }
-
-struct DecodeArgs {
-  // packed weights of layer 0 (k = q + qkv_stride, v = q + 2 qkv_stride,
-  // up = gate + gu_stride); layer l's are l * layer_stride further (bf16x8 units)
-  const bf16x8* wq; const bf16x8* wo; const bf16x8* wg; const bf16x8* wd;
-  size_t qkv_stride, gu_stride, layer_stride;
-  bf16* kc; bf16* vc;          // layer 0 caches (episode 0); layer l at l * kv_layer_elems
-  size_t kv_layer_elems;
-  const float* gains;          // [L][2][d]: attention norm, FFN norm
-  const float2* rope;          // [kv_pad][head_dim/2]
-  float* x;                    // [d] layer input / output (in place)
-  float* r;                    // [d] residual after attention
-  float* qkv;                  // [3d] q, k, v before RoPE
-  bf16* act;                   // [F] SwiGLU output
-  unsigned* bar;               // kDecodeBarWords barrier words
-  unsigned bar_base;           // grid barriers completed by earlier launches since the words were zeroed
-  unsigned hbar_base;          // per-head barriers completed by earlier launches
-  long long timeout_ticks;     // barrier wait limit in wall-clock ticks (100 MHz)
-  int L, d, F, H, head_dim, KBd, KBf, kv_pad, pos, act_bytes;
-  float eps;
-  int flags;                   // kDecodeNtWeights | kDecodeWarmKv
-};
-constexpr int kDecodeNtWeights = 1;   // weight loads marked non-temporal
-constexpr int kDecodeWarmKv = 2;      // step 1 pulls the head's cached keys and values into L2
-
 }  // namespace gvc
 
+#include "gvc_gemm.h"
+#include "gvc_decode.h"
 #include "gvc_launch.h"
