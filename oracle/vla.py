@@ -30,6 +30,7 @@ from .patches import select_static as _select_one
 from .llama import layer_rows, head_row, rmsnorm
 from .relevance import text_vision_attention, text_attention_entropy, entropy_permille, relevant_patches
 from .margin import position_margin, reduce_margin, gate_fires
+from .vit import visual_embeddings
 
 
 def _f64(t):
@@ -38,9 +39,11 @@ def _f64(t):
 
 def convert_weights(w: dict) -> dict:
     """bf16 torch weights (synth layout) -> float64 numpy."""
-    out = {k: _f64(v) for k, v in w.items() if k != "layers"}
+    out = {k: _f64(v) for k, v in w.items() if k not in ("layers", "vit")}
     if "layers" in w:
         out["layers"] = [{k: _f64(v) for k, v in lw.items()} for lw in w["layers"]]
+    if "vit" in w:
+        out["vit"] = convert_weights(w["vit"])
     return out
 
 
@@ -77,6 +80,7 @@ class OracleVLA:
         self.recomputed = None     # [B][L] rows recomputed by the last prefill
         self.tv = None             # [B][L][H][N] Stage 2 attention of the last prefill (task_topk > 0)
         self.ent = None            # [B][L][H] Stage 3 entropy sums of the last prefill (entropy_reuse)
+        self.vis_emb = None        # [B][N][d] visual embeddings of the last prefill's frame (vit_layers > 0)
 
     # ---------------------------------------------------------- Stage 1 + 3
     def relevant(self, b, scores=None):
@@ -132,6 +136,8 @@ class OracleVLA:
     def embed_row(self, b, pos, frame_t, text_ids, extra_rows):
         cfg, lay = self.cfg, self.lay
         N = cfg.n_patches
+        if 1 <= pos <= N and self.vis_emb is not None:
+            return self.vis_emb[b, pos - 1].copy()
         if 1 <= pos <= N:
             n = pos - 1
             v, rc = divmod(n, cfg.patches_per_side ** 2)
@@ -161,6 +167,9 @@ class OracleVLA:
             self.tv = np.zeros((cfg.batch, L, cfg.n_heads, cfg.n_patches))
         if stage3:
             self.ent = np.zeros((cfg.batch, L, cfg.n_heads))
+        if cfg.vit_layers > 0:   # the front end runs on the whole frame every pass
+            self.vis_emb = np.stack([visual_embeddings(self.w["vit"], frame_t[b], cfg.patch, cfg.vit_heads,
+                                                       cfg.vit_eps) for b in range(cfg.batch)])
         for b in range(cfg.batch):
             use_mask = masks is not None and self.valid[b]
             for l in range(L):

@@ -20,17 +20,19 @@ rounds to bf16 with round-to-nearest-even (torch's fp32->bf16 cast); the
 bits are the same on every device.
 """
 from .hashgen import lowbias32, hash_u32, uniform_f32, uniform_bf16, uniform_u8
-from .configs import VLAConfig, config_c1, config_mid, config_c4_tiny, config_c2, config_c3, config_c4, config_c5, ALL_CONFIGS
+from .configs import (VLAConfig, config_c1, config_mid, config_c4_tiny, config_c2, config_c3, config_c4, config_c5,
+                      config_c1v, config_c2v, ALL_CONFIGS)
 from .workload import (
-    TensorId, layer_weights, global_weights, model_weights,
+    TensorId, layer_weights, global_weights, model_weights, vit_weights,
     random_frame, changed_patch_order, perturb_patches, text_ids, extra_rows,
     step_inputs, c3_episode_frames, reuse_schedule,
 )
 
 __all__ = [
     "lowbias32", "hash_u32", "uniform_f32", "uniform_bf16", "uniform_u8",
-    "VLAConfig", "config_c1", "config_mid", "config_c4_tiny", "config_c2", "config_c3", "config_c4", "config_c5", "ALL_CONFIGS",
-    "TensorId", "layer_weights", "global_weights", "model_weights",
+    "VLAConfig", "config_c1", "config_mid", "config_c4_tiny", "config_c2", "config_c3", "config_c4", "config_c5",
+    "config_c1v", "config_c2v", "ALL_CONFIGS",
+    "TensorId", "layer_weights", "global_weights", "model_weights", "vit_weights",
     "random_frame", "changed_patch_order", "perturb_patches", "text_ids", "extra_rows",
     "step_inputs", "c3_episode_frames", "reuse_schedule",
 ]

@@ -43,6 +43,13 @@ class VLAConfig:
     task_topk: int = 0          # Stage 2: patches with the most instruction attention leave S (0: off)
     entropy_reuse: bool = False # Stage 3: per-layer proportions from the instruction tokens' attention entropy
     action_bidir: bool = False  # OFT action block: the action-query rows attend to each other both ways
+    # vision front end: 0 = linear patch projection; else a ViT of vit_layers
+    # pre-norm blocks (no class token) and a two-layer GELU projector to d_model
+    vit_layers: int = 0
+    vit_dim: int = 1024
+    vit_heads: int = 16
+    vit_ffn: int = 4096
+    vit_eps: float = 1e-6
 
     @property
     def head_dim(self) -> int:
@@ -128,6 +135,18 @@ def config_c2() -> VLAConfig:
     """Llama-2-7B shape, 256 visual + 20 text tokens, one step at 50% reuse,
     then 7-token autoregressive action decode."""
     return VLAConfig(name="C2", seed=2)
+
+
+def config_c1v() -> VLAConfig:
+    """C1 with a tiny ViT front end: 2 blocks of width 128 (2 heads of 64),
+    MLP 512, and the GELU projector to d = 256."""
+    return config_c1().with_(name="C1V", vit_layers=2, vit_dim=128, vit_heads=2, vit_ffn=512)
+
+
+def config_c2v() -> VLAConfig:
+    """C2 with a ViT-L/14-shaped front end (24 blocks of width 1024, 16 heads
+    of 64, MLP 4096) and the GELU projector 1024 -> 4096 -> 4096."""
+    return config_c2().with_(name="C2V", vit_layers=24)
 
 
 def config_c3() -> VLAConfig:

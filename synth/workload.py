@@ -22,6 +22,10 @@ class TensorId:
     # per layer: LAYER_BASE + 16*l + kind
     LAYER_BASE = 1000
     WQ, WK, WV, WO, WG, WU, WD, ATTN_NORM, FFN_NORM = range(9)
+    # vision front end: VIT_BASE + 32*l + kind per block, VIT_* globals
+    VIT_PATCH_W, VIT_PATCH_B, VIT_POS, VIT_POST_G, VIT_POST_B, VIT_PROJ1, VIT_PROJ1_B, VIT_PROJ2, VIT_PROJ2_B = \
+        range(20, 29)
+    VIT_BASE = 3000
     # inputs
     FRAME = 100000
     CHANGE_ORDER = 110000
@@ -67,9 +71,52 @@ def global_weights(cfg: VLAConfig, device="cpu") -> dict:
     }
 
 
+VIT_LAYER_KINDS = ("ln1_g", "ln1_b", "wq", "bq", "wk", "bk", "wv", "bv", "wo", "bo", "ln2_g", "ln2_b",
+                   "w1", "b1", "w2", "b2")
+
+
+def vit_weights(cfg: VLAConfig, device="cpu") -> dict:
+    """bf16 weights of the vision front end: patch embedding [Dv][p*p*3]
+    (input in the H, W, C order of a patch) with bias, a position embedding
+    per patch of a view [S][Dv], the blocks, the final LayerNorm and the
+    projector [d][Dv], [d][d] with biases.  Matrices U[-2^s, 2^s) with the
+    model's s; biases U[-2^-6, 2^-6); LayerNorm gains 1 + U[-1/16, 1/16)."""
+    Dv, Fv, d, s, a = cfg.vit_dim, cfg.vit_ffn, cfg.d_model, cfg.seed, cfg.wscale_log2
+    S = cfg.patches_per_side ** 2
+    T = TensorId
+    vid = lambda l, k: T.VIT_BASE + 32 * l + k
+    shapes = {"ln1_g": (Dv,), "ln1_b": (Dv,), "wq": (Dv, Dv), "bq": (Dv,), "wk": (Dv, Dv), "bk": (Dv,),
+              "wv": (Dv, Dv), "bv": (Dv,), "wo": (Dv, Dv), "bo": (Dv,), "ln2_g": (Dv,), "ln2_b": (Dv,),
+              "w1": (Fv, Dv), "b1": (Fv,), "w2": (Dv, Fv), "b2": (Dv,)}
+
+    def gen(tid, name, shape):
+        if name.endswith("_g"):
+            return uniform_bf16(s, tid, shape, -4, device, offset=1.0)
+        if len(shape) == 1 or name.startswith("b") or name.endswith("_b"):
+            return uniform_bf16(s, tid, shape, -6, device)
+        return uniform_bf16(s, tid, shape, a, device)
+
+    layers = [{k: gen(vid(l, i), k, shapes[k]) for i, k in enumerate(VIT_LAYER_KINDS)}
+              for l in range(cfg.vit_layers)]
+    return {
+        "patch_w": gen(T.VIT_PATCH_W, "patch_w", (Dv, cfg.patch_dim)),
+        "patch_b": gen(T.VIT_PATCH_B, "patch_b", (Dv,)),
+        "pos": uniform_bf16(s, T.VIT_POS, (S, Dv), a, device),
+        "post_g": gen(T.VIT_POST_G, "post_g", (Dv,)),
+        "post_b": gen(T.VIT_POST_B, "post_b", (Dv,)),
+        "proj1": gen(T.VIT_PROJ1, "proj1", (d, Dv)),
+        "proj1_b": gen(T.VIT_PROJ1_B, "proj1_b", (d,)),
+        "proj2": gen(T.VIT_PROJ2, "proj2", (d, d)),
+        "proj2_b": gen(T.VIT_PROJ2_B, "proj2_b", (d,)),
+        "layers": layers,
+    }
+
+
 def model_weights(cfg: VLAConfig, device="cpu") -> dict:
     w = global_weights(cfg, device)
     w["layers"] = [layer_weights(cfg, l, device) for l in range(cfg.n_layers)]
+    if cfg.vit_layers > 0:
+        w["vit"] = vit_weights(cfg, device)
     return w
 
 
