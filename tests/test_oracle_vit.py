@@ -102,6 +102,14 @@ def test_prompt_pass_uses_the_front_end():
     N = cfg.n_patches
     assert np.array_equal(o.H[0, 0, 1:N + 1], vis)
     assert vis.shape == (N, cfg.d_model)
-    # the projector is the last step: its input is the encoder output
+    # the projector is the last step: its input is the encoder output; it
+    # equals torch's Linear -> GELU(tanh) -> Linear with the same weights
     z = vit_view(vw, view_patches(si["frame_t"].numpy()[0, 0], cfg.patch), cfg.vit_heads, cfg.vit_eps)
     assert np.array_equal(project(vw, z), vis[: cfg.patches_per_side ** 2])
+    mlp = torch.nn.Sequential(torch.nn.Linear(cfg.vit_dim, cfg.d_model), torch.nn.GELU(approximate="tanh"),
+                              torch.nn.Linear(cfg.d_model, cfg.d_model)).double()
+    with torch.no_grad():
+        mlp[0].weight.copy_(torch.from_numpy(vw["proj1"])); mlp[0].bias.copy_(torch.from_numpy(vw["proj1_b"]))
+        mlp[2].weight.copy_(torch.from_numpy(vw["proj2"])); mlp[2].bias.copy_(torch.from_numpy(vw["proj2_b"]))
+        ref = mlp(torch.from_numpy(z)).numpy()
+    assert np.abs(project(vw, z) - ref).max() < 1e-12
