@@ -117,6 +117,19 @@ typedef struct gvc_desc {
                              row causal; 1 = the n_action_q action-query rows (the last rows of the
                              prompt) attend to every prompt key, so they see each other both ways.
                              Needs parallel_decode = 1 and n_action_q >= 1. */
+  int32_t vit_layers;     /* vision front end (Sec. III-A, Sec. V-A models): 0 = a visual token's
+                             embedding is (patch pixels / 255) . patch_proj^T; else every prompt pass
+                             runs, per camera view, a ViT without class token over all the view's
+                             patches -- patch embedding (pixels / 255, H,W,C order) with bias plus a
+                             learned position embedding, vit_layers pre-norm blocks (LayerNorm with
+                             bias; multi-head attention with biases in which every patch sees every
+                             patch of its view; MLP fc1 -> GELU (tanh form) -> fc2 with biases), a
+                             final LayerNorm -- and the projector Linear(vit_dim, d) -> GELU ->
+                             Linear(d, d) with biases gives the embedding.  At most 64. */
+  int32_t vit_dim;        /* ViT width, a multiple of 64; vit_dim / vit_heads is 64 or 128 */
+  int32_t vit_heads;
+  int32_t vit_ffn;        /* ViT MLP width, a multiple of 32 */
+  float vit_eps;          /* LayerNorm epsilon of the ViT (> 0) */
 } gvc_desc;
 
 /* bf16 weights of one decoder layer, canonical [out_features][in_features]. */
@@ -132,12 +145,41 @@ typedef struct gvc_layer_weights {
   const void* ffn_norm;   /* dev bf16 [d] RMSNorm gain before the FFN */
 } gvc_layer_weights;
 
+/* bf16 weights of one ViT block, matrices [out_features][in_features]
+ * (Dv = vit_dim, Fv = vit_ffn); vectors hold Dv values unless noted. */
+typedef struct gvc_vit_layer_weights {
+  const void* ln1_g; const void* ln1_b;   /* LayerNorm before attention */
+  const void* wq; const void* bq;         /* [Dv][Dv], [Dv] */
+  const void* wk; const void* bk;
+  const void* wv; const void* bv;
+  const void* wo; const void* bo;
+  const void* ln2_g; const void* ln2_b;   /* LayerNorm before the MLP */
+  const void* w1; const void* b1;         /* [Fv][Dv], [Fv] */
+  const void* w2; const void* b2;         /* [Dv][Fv], [Dv] */
+} gvc_vit_layer_weights;
+
+/* bf16 weights of the vision front end (desc.vit_layers > 0). */
+typedef struct gvc_vit_weights {
+  const void* patch_w;     /* dev bf16 [Dv][p*p*3], input in a patch's H, W, C order */
+  const void* patch_b;     /* dev bf16 [Dv] */
+  const void* pos;         /* dev bf16 [(img/p)^2][Dv] position embedding, raster order within a view */
+  const void* post_g;      /* dev bf16 [Dv] final LayerNorm */
+  const void* post_b;
+  const void* proj1;       /* dev bf16 [d][Dv] */
+  const void* proj1_b;     /* dev bf16 [d] */
+  const void* proj2;       /* dev bf16 [d][d] */
+  const void* proj2_b;     /* dev bf16 [d] */
+  const gvc_vit_layer_weights* layers; /* host array of vit_layers entries */
+} gvc_vit_weights;
+
 typedef struct gvc_weights {
   const void* embed;       /* dev bf16 [V][d] token embedding table */
-  const void* patch_proj;  /* dev bf16 [d][p*p*3]: visual row = (pixels/255) . W^T (Sec. III-A) */
+  const void* patch_proj;  /* dev bf16 [d][p*p*3]: visual row = (pixels/255) . W^T (Sec. III-A);
+                              unused (may be NULL) with the vision front end */
   const void* lm_head;     /* dev bf16 [V][d] */
   const void* final_norm;  /* dev bf16 [d] */
   const gvc_layer_weights* layers; /* host array of L entries */
+  const gvc_vit_weights* vit;      /* host pointer; NULL unless desc.vit_layers > 0 */
 } gvc_weights;
 
 typedef struct gvc_ctx gvc_ctx;
@@ -240,7 +282,9 @@ enum gvc_kernel_class {
   GVC_K_DECODE_DOWN = 4, GVC_K_DECODE_HEAD = 5,
   GVC_K_PREFILL_QKV = 6, GVC_K_PREFILL_ATTN = 7, GVC_K_PREFILL_O = 8, GVC_K_PREFILL_GU = 9,
   GVC_K_PREFILL_DOWN = 10, GVC_K_PREFILL_HEAD = 11, GVC_K_EMBED = 12, GVC_K_NORM = 13,
-  GVC_K_SELECT = 14, GVC_K_DECODE_PASS = 15, GVC_K_STAGE2 = 16, GVC_K_COUNT = 17
+  GVC_K_SELECT = 14, GVC_K_DECODE_PASS = 15, GVC_K_STAGE2 = 16,
+  GVC_K_VIT = 17,          /* every launch of the vision front end and the first projector GEMM */
+  GVC_K_COUNT = 18
 };
 
 /* Starts timing every launch of kernel class `cls` (enum gvc_kernel_class):

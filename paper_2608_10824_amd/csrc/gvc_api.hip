@@ -59,6 +59,13 @@ struct Plan {
   bool stage2;   // task_topk > 0 and at least one instruction token after the image
   bool stage3;   // entropy_reuse and at least one instruction token after the image
   int block_first, block_last;   // bidirectional action block [block_first, P - 1], or empty
+  // vision front end (vit_layers > 0): Sv patches per view, E = B * views
+  // view passes, Mv = B * N rows; fp32 vectors at vvec_off (see vit_vec_*)
+  bool vit = false;
+  int Sv = 0, E = 0, Mv = 0, Mvp = 0, Dv = 0, Hv = 0, dhv = 0, Fv = 0, KBv = 0, KBvf = 0, kvpad_v = 0;
+  std::vector<Packed> vq, vk, vv, vo, v1, v2;
+  Packed vpatch, vproj1, vproj2;
+  size_t vvec_off, vrows_off, vepc_off, vepo_off, vx_off, vq_off, vk_off, vv_off, vo_off, vh_off, va_off, vp_off;
   size_t layer_kv_elems;
   // workspace
   size_t rows_off, counts_off, epc_off, epo_off, stats_off, x_off, q_off, o_off, r_off, act_off, xdec_off, xf_off,
@@ -74,6 +81,18 @@ Packed plan_packed(Bump& a, int N, int K) {
   p.KB = (K + 31) / 32;
   p.off = a.take((size_t)p.Nblk * 16 * p.KB * 32 * 2);
   return p;
+}
+
+// fp32 vectors of the vision front end, in floats from vvec_off: patch bias
+// [Dv], position table [Sv][Dv], final LayerNorm gain and bias [Dv], projector
+// biases [d] and [d]; then per block ln1 gain, ln1 bias, bq, bk, bv, bo, ln2
+// gain, ln2 bias, b2 (each [Dv]) and b1 [Fv].
+size_t vit_vec_glob(const Plan& p) { return (size_t)p.Dv * (3 + p.Sv) + 2 * (size_t)p.d.d_model; }
+size_t vit_vec_floats(const Plan& p) { return vit_vec_glob(p) + (size_t)p.d.vit_layers * (9 * p.Dv + p.Fv); }
+enum { VV_LN1G = 0, VV_LN1B, VV_BQ, VV_BK, VV_BV, VV_BO, VV_LN2G, VV_LN2B, VV_B2, VV_B1 };
+// offset (floats) of vector `which` of ViT block l
+size_t vit_vec_layer(const Plan& p, int l, int which) {
+  return vit_vec_glob(p) + (size_t)l * (9 * p.Dv + p.Fv) + (size_t)which * p.Dv;
 }
 
 int32_t make_plan(const gvc_desc* dsc, Plan& p) {
@@ -111,6 +130,25 @@ int32_t make_plan(const gvc_desc* dsc, Plan& p) {
     return fail(GVC_EINVAL, "action_bidir needs parallel_decode and n_action_q >= 1");
   p.block_first = d.action_bidir ? p.P - d.n_action_q : p.P;
   p.block_last = p.P - 1;
+  if (d.vit_layers < 0 || d.vit_layers > 64) return fail(GVC_EINVAL, "vit_layers must be in [0, 64]");
+  p.vit = d.vit_layers > 0;
+  if (p.vit) {
+    if (d.vit_dim < 64 || d.vit_dim % 64 || d.vit_dim > 8192)
+      return fail(GVC_EINVAL, "vit_dim must be a multiple of 64 in [64, 8192]");
+    if (d.vit_heads < 1 || d.vit_dim % d.vit_heads) return fail(GVC_EINVAL, "vit_heads must divide vit_dim");
+    p.dhv = d.vit_dim / d.vit_heads;
+    if (p.dhv != 64 && p.dhv != 128) return fail(GVC_EINVAL, "vit_dim / vit_heads must be 64 or 128");
+    if (d.vit_ffn < 32 || d.vit_ffn % 32 || d.vit_ffn > 32768)
+      return fail(GVC_EINVAL, "vit_ffn must be a multiple of 32 in [32, 32768]");
+    if (!(d.vit_eps > 0.f)) return fail(GVC_EINVAL, "vit_eps must be > 0");
+    p.Sv = side * side;
+    p.E = d.batch * d.n_views;
+    p.Mv = d.batch * p.N;
+    p.Mvp = (p.Mv + 15) / 16 * 16;
+    p.Dv = d.vit_dim; p.Hv = d.vit_heads; p.Fv = d.vit_ffn;
+    p.KBv = p.Dv / 32; p.KBvf = p.Fv / 32;
+    p.kvpad_v = (p.Sv + 31) / 32 * 32;
+  }
   p.stage2 = d.task_topk > 0 && d.n_text >= 2;
   p.stage3 = d.entropy_reuse && d.n_text >= 2;
   if ((p.stage2 || p.stage3) && (d.n_text - 1 > 32 || p.N + d.n_text >= 640 || (dh != 64 && dh != 128)))
@@ -136,6 +174,20 @@ int32_t make_plan(const gvc_desc* dsc, Plan& p) {
     p.wd.push_back(plan_packed(w, d.d_model, d.ffn));
   }
   p.patch = plan_packed(w, d.d_model, p.patch_dim);
+  if (p.vit) {
+    for (int l = 0; l < d.vit_layers; ++l) {
+      p.vq.push_back(plan_packed(w, p.Dv, p.Dv));
+      p.vk.push_back(plan_packed(w, p.Dv, p.Dv));
+      p.vv.push_back(plan_packed(w, p.Dv, p.Dv));
+      p.vo.push_back(plan_packed(w, p.Dv, p.Dv));
+      p.v1.push_back(plan_packed(w, p.Fv, p.Dv));
+      p.v2.push_back(plan_packed(w, p.Dv, p.Fv));
+    }
+    p.vpatch = plan_packed(w, p.Dv, p.patch_dim);
+    p.vproj1 = plan_packed(w, d.d_model, p.Dv);
+    p.vproj2 = plan_packed(w, d.d_model, d.d_model);
+    p.vvec_off = w.take(vit_vec_floats(p) * 4);
+  }
   p.lm = plan_packed(w, d.vocab, d.d_model);
   p.embed_off = w.take((size_t)d.vocab * d.d_model * 2);
   p.gains_off = w.take((size_t)p.L * 2 * d.d_model * 4);
@@ -183,6 +235,20 @@ int32_t make_plan(const gvc_desc* dsc, Plan& p) {
   p.gate_f_off = k.take((size_t)p.B * 4);
   p.qkv3_off = k.take((size_t)3 * p.B * d.d_model * 4);
   p.bar_off = k.take((size_t)kDecodeBarWords * 4);
+  if (p.vit) {
+    const size_t kvv = (size_t)p.E * p.Hv * p.kvpad_v * p.dhv * 2;
+    p.vrows_off = k.take((size_t)4 * p.Mv * 4);
+    p.vepc_off = k.take((size_t)p.E * 4);
+    p.vepo_off = k.take((size_t)p.E * 4);
+    p.vx_off = k.take((size_t)p.Mvp * std::max(p.KBv, p.KBp) * 32 * 2);
+    p.vq_off = k.take((size_t)p.Mvp * p.Dv * 2);
+    p.vk_off = k.take(kvv);
+    p.vv_off = k.take(kvv);
+    p.vo_off = k.take((size_t)p.Mvp * p.KBv * 32 * 2);
+    p.vh_off = k.take((size_t)p.Mvp * p.Dv * 4);
+    p.va_off = k.take((size_t)p.Mvp * p.KBvf * 32 * 2);
+    p.vp_off = k.take((size_t)p.Mvp * p.KBd * 32 * 2);
+  }
   p.ws_bytes = k.off;
   return GVC_OK;
 }
@@ -283,8 +349,10 @@ GemmArgs base_args(const gvc_ctx* c) {
   a.e.n_heads = c->p.H;
   a.e.kv_pad = c->p.kv_pad;
   a.e.rope = c->K<float2>(c->p.rope_off);
+  a.e.vis_scale = 1.0f / 255.0f;
   return a;
 }
+
 
 int32_t run_gemm(gvc_ctx* c, GemmArgs& a, int epi, int M, int cls) {
   if (M <= 0) return GVC_OK;
@@ -294,6 +362,122 @@ int32_t run_gemm(gvc_ctx* c, GemmArgs& a, int epi, int M, int cls) {
     return fail(GVC_EINVAL, "folded norm needs one token block and at most 32 parts per wave");
   ProfScope ps(c, cls);
   HIP_TRY(launch_gemm(a, epi, nt_of(a), c->stream));
+  return GVC_OK;
+}
+
+// GEMM arguments of a vision front end launch: row width Dv, heads of dhv,
+// no rotary embedding.
+GemmArgs vit_args(const gvc_ctx* c) {
+  GemmArgs a = base_args(c);
+  a.e.d = c->p.Dv;
+  a.e.head_dim = c->p.dhv;
+  a.e.n_heads = c->p.Hv;
+  a.e.kv_pad = c->p.kvpad_v;
+  a.e.rope = nullptr;
+  return a;
+}
+
+// The vision front end over every view of frame_t: patch embedding, the ViT
+// blocks, the final LayerNorm and the first projector layer (GELU), leaving
+// bf16 [B*N][d] in frag layout at vp_off for the embedding step.
+int32_t run_vit(gvc_ctx* c, const uint8_t* frame_t) {
+  const Plan& p = c->p;
+  hipStream_t s = c->stream;
+  const int Mv = p.Mv;
+  const int* vr = c->K<int>(p.vrows_off);
+  const RowMap rows{vr, vr + Mv, vr + 2 * Mv};   // idx (for the patch gather), view pass, position in view
+  const int* posl = vr + 3 * Mv;                 // prompt position of the row's visual token
+  const float* vec = c->W<float>(p.vvec_off);
+  bf16* X = c->K<bf16>(p.vx_off);
+  bf16* Q = c->K<bf16>(p.vq_off);
+  bf16* Kv = c->K<bf16>(p.vk_off);
+  bf16* Vv = c->K<bf16>(p.vv_off);
+  bf16* O = c->K<bf16>(p.vo_off);
+  float* h = c->K<float>(p.vh_off);
+  bf16* A = c->K<bf16>(p.va_off);
+  const float eps = p.d.vit_eps;
+  {
+    ProfScope ps(c, GVC_K_VIT);
+    HIP_TRY(launch_im2row(frame_t, p.d.n_views, p.d.img, p.d.patch, rows.idx, posl, Mv, p.P, p.KBp, X, s));
+  }
+  {
+    GemmArgs a = vit_args(c);
+    a.w[0] = c->packed(p.vpatch); a.wblk[0] = p.vpatch.Nblk;
+    a.map = MAP_PLAIN; a.n_pairs = (p.vpatch.Nblk + 1) / 2; a.n_out = p.Dv; a.KB = p.KBp;
+    a.x = reinterpret_cast<const bf16x8*>(X);
+    a.e.rows = rows; a.e.store = h; a.e.ld_store = p.Dv; a.e.bias[0] = vec; a.e.pos_tab = vec + p.Dv;
+    int32_t r = run_gemm(c, a, EPI_PATCH, Mv, GVC_K_VIT);
+    if (r) return r;
+  }
+  for (int l = 0; l < p.d.vit_layers; ++l) {
+    auto V = [&](int which) { return vec + vit_vec_layer(p, l, which); };
+    {
+      ProfScope ps(c, GVC_K_VIT);
+      HIP_TRY(launch_layernorm(h, Mv, p.Dv, V(VV_LN1G), V(VV_LN1B), eps, X, p.KBv, s));
+    }
+    {
+      GemmArgs a = vit_args(c);
+      a.w[0] = c->packed(p.vq[l]); a.w[1] = c->packed(p.vk[l]); a.w[2] = c->packed(p.vv[l]);
+      a.wblk[0] = a.wblk[1] = a.wblk[2] = p.vq[l].Nblk;
+      a.map = MAP_QKV; a.n_pairs = 3 * p.vq[l].Nblk / 2; a.n_out = p.Dv; a.KB = p.KBv;
+      a.x = reinterpret_cast<const bf16x8*>(X);
+      a.e.rows = rows; a.e.q = Q; a.e.kc = Kv; a.e.vc = Vv;
+      a.e.bias[0] = V(VV_BQ); a.e.bias[1] = V(VV_BK); a.e.bias[2] = V(VV_BV);
+      int32_t r = run_gemm(c, a, EPI_QKV, Mv, GVC_K_VIT);
+      if (r) return r;
+    }
+    {
+      ProfScope ps(c, GVC_K_VIT);
+      HIP_TRY(launch_attn_prefill(Q, Kv, Vv, rows.pos, c->K<int>(p.vepc_off), c->K<int>(p.vepo_off), p.E, p.Hv,
+                                  p.dhv, p.kvpad_v, (p.Sv + 15) / 16, O, p.KBv, 0, p.Sv - 1, s));
+    }
+    {
+      GemmArgs a = vit_args(c);
+      a.w[0] = c->packed(p.vo[l]); a.wblk[0] = p.vo[l].Nblk;
+      a.map = MAP_PLAIN; a.n_pairs = (p.vo[l].Nblk + 1) / 2; a.n_out = p.Dv; a.KB = p.KBv;
+      a.x = reinterpret_cast<const bf16x8*>(O);
+      a.e.rows = rows; a.e.resid = h; a.e.out = h; a.e.bias[0] = V(VV_BO);   // in place: each element once
+      int32_t r = run_gemm(c, a, EPI_RESID, Mv, GVC_K_VIT);
+      if (r) return r;
+    }
+    {
+      ProfScope ps(c, GVC_K_VIT);
+      HIP_TRY(launch_layernorm(h, Mv, p.Dv, V(VV_LN2G), V(VV_LN2B), eps, X, p.KBv, s));
+    }
+    {
+      GemmArgs a = vit_args(c);
+      a.w[0] = c->packed(p.v1[l]); a.wblk[0] = p.v1[l].Nblk;
+      a.map = MAP_PLAIN; a.n_pairs = (p.v1[l].Nblk + 1) / 2; a.n_out = p.Fv; a.KB = p.KBv;
+      a.x = reinterpret_cast<const bf16x8*>(X);
+      a.e.rows = rows; a.e.act = A; a.e.kb_act = p.KBvf; a.e.n_feat = p.Fv; a.e.bias[0] = V(VV_B1);
+      int32_t r = run_gemm(c, a, EPI_GELU, Mv, GVC_K_VIT);
+      if (r) return r;
+    }
+    {
+      GemmArgs a = vit_args(c);
+      a.w[0] = c->packed(p.v2[l]); a.wblk[0] = p.v2[l].Nblk;
+      a.map = MAP_PLAIN; a.n_pairs = (p.v2[l].Nblk + 1) / 2; a.n_out = p.Dv; a.KB = p.KBvf;
+      a.x = reinterpret_cast<const bf16x8*>(A);
+      a.e.rows = rows; a.e.resid = h; a.e.out = h; a.e.bias[0] = V(VV_B2);
+      int32_t r = run_gemm(c, a, EPI_RESID, Mv, GVC_K_VIT);
+      if (r) return r;
+    }
+  }
+  const size_t glob_ln = (size_t)p.Dv * (1 + p.Sv);   // final LayerNorm gain, then bias
+  {
+    ProfScope ps(c, GVC_K_VIT);
+    HIP_TRY(launch_layernorm(h, Mv, p.Dv, vec + glob_ln, vec + glob_ln + p.Dv, eps, X, p.KBv, s));
+  }
+  {
+    GemmArgs a = vit_args(c);
+    a.w[0] = c->packed(p.vproj1); a.wblk[0] = p.vproj1.Nblk;
+    a.map = MAP_PLAIN; a.n_pairs = (p.vproj1.Nblk + 1) / 2; a.n_out = p.d.d_model; a.KB = p.KBv;
+    a.x = reinterpret_cast<const bf16x8*>(X);
+    a.e.rows = rows; a.e.act = c->K<bf16>(p.vp_off); a.e.kb_act = p.KBd; a.e.n_feat = p.d.d_model;
+    a.e.bias[0] = vec + glob_ln + 2 * p.Dv;
+    int32_t r = run_gemm(c, a, EPI_GELU, Mv, GVC_K_VIT);
+    if (r) return r;
+  }
   return GVC_OK;
 }
 
@@ -560,8 +744,21 @@ int32_t gvc_init_cache(const gvc_desc* desc, const gvc_weights* wt, void* weight
   Plan p;
   int32_t r = make_plan(desc, p);
   if (r) return r;
-  if (!wt || !wt->embed || !wt->patch_proj || !wt->lm_head || !wt->final_norm || !wt->layers)
+  if (!wt || !wt->embed || (!wt->patch_proj && !p.vit) || !wt->lm_head || !wt->final_norm || !wt->layers)
     return fail(GVC_EINVAL, "null weight pointer");
+  if (p.vit) {
+    const gvc_vit_weights* vw = wt->vit;
+    if (!vw || !vw->patch_w || !vw->patch_b || !vw->pos || !vw->post_g || !vw->post_b || !vw->proj1 ||
+        !vw->proj1_b || !vw->proj2 || !vw->proj2_b || !vw->layers)
+      return fail(GVC_EINVAL, "null vision front end weight pointer");
+    for (int l = 0; l < p.d.vit_layers; ++l) {
+      const gvc_vit_layer_weights& v = vw->layers[l];
+      const void* ptrs[16] = {v.ln1_g, v.ln1_b, v.wq, v.bq, v.wk, v.bk, v.wv, v.bv,
+                              v.wo, v.bo, v.ln2_g, v.ln2_b, v.w1, v.b1, v.w2, v.b2};
+      for (const void* q : ptrs)
+        if (!q) return fail(GVC_EINVAL, "null vision front end weight pointer at block " + std::to_string(l));
+    }
+  }
   for (int l = 0; l < p.L; ++l) {
     const gvc_layer_weights& lw = wt->layers[l];
     if (!lw.wq || !lw.wk || !lw.wv || !lw.wo || !lw.wg || !lw.wu || !lw.wd || !lw.attn_norm || !lw.ffn_norm)
@@ -605,8 +802,57 @@ int32_t gvc_init_cache(const gvc_desc* desc, const gvc_weights* wt, void* weight
     INIT_TRY(launch_convert_gain(static_cast<const bf16*>(lw.attn_norm), g, dm, s));
     INIT_TRY(launch_convert_gain(static_cast<const bf16*>(lw.ffn_norm), g + dm, dm, s));
   }
-  INIT_TRY(launch_pack(static_cast<const bf16*>(wt->patch_proj), p.patch.N, p.patch.K, c->W<bf16>(p.patch.off),
-                       p.patch.Nblk, p.patch.KB, s));
+  if (wt->patch_proj)
+    INIT_TRY(launch_pack(static_cast<const bf16*>(wt->patch_proj), p.patch.N, p.patch.K, c->W<bf16>(p.patch.off),
+                         p.patch.Nblk, p.patch.KB, s));
+  if (p.vit) {
+    const gvc_vit_weights* vw = wt->vit;
+    auto pack = [&](const void* src, const Packed& m) {
+      return launch_pack(static_cast<const bf16*>(src), m.N, m.K, c->W<bf16>(m.off), m.Nblk, m.KB, s);
+    };
+    float* vec = c->W<float>(p.vvec_off);
+    auto cvt = [&](const void* src, size_t off, int n) {
+      return launch_convert_gain(static_cast<const bf16*>(src), vec + off, n, s);
+    };
+    const int Dv = p.Dv;
+    INIT_TRY(pack(vw->patch_w, p.vpatch));
+    INIT_TRY(pack(vw->proj1, p.vproj1));
+    INIT_TRY(pack(vw->proj2, p.vproj2));
+    INIT_TRY(cvt(vw->patch_b, 0, Dv));
+    INIT_TRY(cvt(vw->pos, Dv, p.Sv * Dv));
+    INIT_TRY(cvt(vw->post_g, (size_t)Dv * (1 + p.Sv), Dv));
+    INIT_TRY(cvt(vw->post_b, (size_t)Dv * (2 + p.Sv), Dv));
+    INIT_TRY(cvt(vw->proj1_b, (size_t)Dv * (3 + p.Sv), dm));
+    INIT_TRY(cvt(vw->proj2_b, (size_t)Dv * (3 + p.Sv) + dm, dm));
+    for (int l = 0; l < p.d.vit_layers; ++l) {
+      const gvc_vit_layer_weights& v = vw->layers[l];
+      INIT_TRY(pack(v.wq, p.vq[l]));
+      INIT_TRY(pack(v.wk, p.vk[l]));
+      INIT_TRY(pack(v.wv, p.vv[l]));
+      INIT_TRY(pack(v.wo, p.vo[l]));
+      INIT_TRY(pack(v.w1, p.v1[l]));
+      INIT_TRY(pack(v.w2, p.v2[l]));
+      const void* vecs[9] = {v.ln1_g, v.ln1_b, v.bq, v.bk, v.bv, v.bo, v.ln2_g, v.ln2_b, v.b2};
+      for (int i = 0; i < 9; ++i) INIT_TRY(cvt(vecs[i], vit_vec_layer(p, l, i), Dv));
+      INIT_TRY(cvt(v.b1, vit_vec_layer(p, l, VV_B1), p.Fv));
+    }
+    // rows of the front end: visual token n of episode b is row b*N + n, in
+    // view pass e = b*views + n / Sv at position n % Sv
+    std::vector<int> vr((size_t)4 * p.Mv), epc(p.E, p.Sv), epo(p.E);
+    for (int b = 0; b < p.B; ++b)
+      for (int n = 0; n < p.N; ++n) {
+        const int m = b * p.N + n;
+        vr[m] = b * p.P + 1 + n;
+        vr[p.Mv + m] = b * p.d.n_views + n / p.Sv;
+        vr[2 * p.Mv + m] = n % p.Sv;
+        vr[3 * p.Mv + m] = 1 + n;
+      }
+    for (int e = 0; e < p.E; ++e) epo[e] = e * p.Sv;
+    INIT_TRY(hipMemcpyAsync(c->K<int>(p.vrows_off), vr.data(), vr.size() * 4, hipMemcpyHostToDevice, s));
+    INIT_TRY(hipMemcpyAsync(c->K<int>(p.vepc_off), epc.data(), epc.size() * 4, hipMemcpyHostToDevice, s));
+    INIT_TRY(hipMemcpyAsync(c->K<int>(p.vepo_off), epo.data(), epo.size() * 4, hipMemcpyHostToDevice, s));
+    INIT_TRY(hipStreamSynchronize(s));   // the host vectors end here
+  }
   INIT_TRY(launch_pack(static_cast<const bf16*>(wt->lm_head), p.lm.N, p.lm.K, c->W<bf16>(p.lm.off), p.lm.Nblk,
                        p.lm.KB, s));
   INIT_TRY(hipMemcpyAsync(c->W<char>(p.embed_off), wt->embed, (size_t)p.V * dm * 2, hipMemcpyDeviceToDevice, s));
@@ -680,13 +926,26 @@ int32_t gvc_step_prefill(gvc_ctx* c, const uint8_t* frame_t, const int32_t* text
     if (c->counts[l] < 1 || c->counts[l] > p.B * p.P) return fail(GVC_EDEVICE, "corrupt row count");
 
   // layer-0 embeddings of the rows recomputed at layer 0
+  if (p.vit) {
+    int32_t r = run_vit(c, frame_t);
+    if (r) return r;
+  }
   {
     const RowMap r0 = c->rows(0);
     bf16* X = c->K<bf16>(p.x_off);
-    HIP_TRY(launch_im2row(frame_t, p.d.n_views, p.d.img, p.d.patch, r0.idx, r0.pos, c->counts[0], p.P, p.KBp, X, s));
     GemmArgs a = base_args(c);
-    a.w[0] = c->packed(p.patch); a.wblk[0] = p.patch.Nblk;
-    a.map = MAP_PLAIN; a.n_pairs = (p.patch.Nblk + 1) / 2; a.n_out = p.d.d_model; a.KB = p.KBp;
+    if (p.vit) {   // visual rows: the projector's second layer over the ViT rows recomputed at layer 0
+      HIP_TRY(launch_gather_visual(c->K<bf16>(p.vp_off), r0.idx, r0.pos, c->counts[0], p.P, p.N, p.KBd, X, s));
+      a.w[0] = c->packed(p.vproj2); a.wblk[0] = p.vproj2.Nblk;
+      a.map = MAP_PLAIN; a.n_pairs = (p.vproj2.Nblk + 1) / 2; a.n_out = p.d.d_model; a.KB = p.KBd;
+      a.e.vis_scale = 1.0f;
+      a.e.bias[0] = c->W<float>(p.vvec_off) + (size_t)p.Dv * (3 + p.Sv) + p.d.d_model;
+    } else {
+      HIP_TRY(launch_im2row(frame_t, p.d.n_views, p.d.img, p.d.patch, r0.idx, r0.pos, c->counts[0], p.P, p.KBp, X,
+                            s));
+      a.w[0] = c->packed(p.patch); a.wblk[0] = p.patch.Nblk;
+      a.map = MAP_PLAIN; a.n_pairs = (p.patch.Nblk + 1) / 2; a.n_out = p.d.d_model; a.KB = p.KBp;
+    }
     a.x = reinterpret_cast<const bf16x8*>(X);
     a.e.rows = r0; a.e.h0 = c->H(0); a.e.embed = c->W<bf16>(p.embed_off); a.e.text_ids = text_ids;
     a.e.extra = extra_rows; a.e.n_patches = p.N; a.e.n_text = p.d.n_text; a.e.n_extra = p.n_extra;

@@ -8,7 +8,8 @@ namespace gvc {
 // Work units of a GEMM launch.  Pair maps give a workgroup two 16-row weight
 // blocks whose epilogue partners share lanes; single maps give it one block.
 enum { MAP_PLAIN = 0, MAP_QKV = 1, MAP_GU = 2, MAP_SINGLE = 3, MAP_QKV_SINGLE = 4 };
-enum { EPI_QKV = 0, EPI_RESID = 1, EPI_SILU = 2, EPI_STORE = 3, EPI_EMBED = 4, EPI_QKV_RAW = 5 };
+enum { EPI_QKV = 0, EPI_RESID = 1, EPI_SILU = 2, EPI_STORE = 3, EPI_EMBED = 4, EPI_QKV_RAW = 5, EPI_PATCH = 6,
+       EPI_GELU = 7 };
 
 struct RowMap {
   const int* idx;   // row index into the residual / output arrays
@@ -23,12 +24,20 @@ struct EpiArgs {
   bf16* q;            // [Mp][d] row-major, after RoPE
   bf16* kc;           // this layer's K cache
   bf16* vc;           // this layer's V cache (transposed)
-  const float2* rope; // [kv_pad][head_dim/2] (cos, sin)
+  const float2* rope; // [kv_pad][head_dim/2] (cos, sin); nullptr: no rotation
+  // fp32 biases added to the accumulators (nullptr: none): per matrix for
+  // EPI_QKV, bias[0] for EPI_RESID, EPI_GELU, EPI_PATCH and EPI_EMBED
+  const float* bias[3];
+  // EPI_EMBED: visual rows are acc * vis_scale (+ bias[0])
+  float vis_scale;
+  // EPI_PATCH: store[m][f] = acc / 255 + bias[0][f] + pos_tab[rows.pos[m]][f] (ld_store floats per row)
+  const float* pos_tab;
   int d, head_dim, n_heads, kv_pad;
   // EPI_RESID: out[row] = resid[row] + acc, rows mapped through rows.idx when *_mapped
   const float* resid; int resid_mapped;
   float* out; int out_mapped;
-  // EPI_SILU: frag-layout bf16 activations with kb_act k-fragments per row block
+  // EPI_SILU (gate, up pairs) and EPI_GELU (bias, then GELU): frag-layout
+  // bf16 activations with kb_act k-fragments per row block
   bf16* act; int kb_act; int n_feat;
   // EPI_STORE
   float* store; int ld_store;

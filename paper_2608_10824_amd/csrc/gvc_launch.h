@@ -24,6 +24,10 @@ hipError_t launch_build_rows(const uint8_t* mask, const int* valid, int B, int L
                              int* rows, int* counts, int* ep_counts, int* ep_offsets, hipStream_t s);
 hipError_t launch_im2row(const uint8_t* frame, int views, int img, int patch, const int* idx, const int* pos,
                          int M, int P, int KB, bf16* x, hipStream_t s);
+hipError_t launch_layernorm(const float* src, int M, int d, const float* gain, const float* bias, float eps,
+                            bf16* x, int KB, hipStream_t s);
+hipError_t launch_gather_visual(const bf16* src, const int* idx, const int* pos, int M, int P, int N, int KB,
+                                bf16* x, hipStream_t s);
 hipError_t launch_rmsnorm(const float* src, const int* idx, int M, int d, const float* gain, float eps,
                           bf16* x, int KB, hipStream_t s);
 hipError_t launch_gemm(const GemmArgs& a, int epi, int NT, hipStream_t s);

@@ -49,6 +49,16 @@ __device__ __forceinline__ bf16x8 wload(const bf16x8* p) { return *p; }
 
 __device__ __forceinline__ float silu_f(float g) { return g / (1.0f + __expf(-g)); }
 
+// GELU, tanh form: x/2 (1 + tanh(sqrt(2/pi) (x + 0.044715 x^3))).
+__device__ __forceinline__ float gelu_f(float x) {
+  return 0.5f * x * (1.0f + tanhf(0.7978845608028654f * (x + 0.044715f * x * x * x)));
+}
+
+__device__ __forceinline__ void add_bias(floatx4& v, const float* bias, int f) {
+  const float4 b = *(const float4*)(bias + f);
+  v[0] += b.x; v[1] += b.y; v[2] += b.z; v[3] += b.w;
+}
+
 // Epilogue of one lane: 4 consecutive output features of block A and of
 // block B for token row m.  Every lane of the wave calls it (some epilogues
 // shuffle across lanes); `valid` says whether row m exists (m is already
@@ -70,8 +80,12 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, int pair, int lane, 
     const int ia = (blk_a % (dh >> 4)) * 16 + sub;   // dim within head, < half
     const int pos = e.rows.pos[m];
     const int b = e.rows.ep[m];
+    if (e.bias[mat_a]) {
+      add_bias(va, e.bias[mat_a], blk_a * 16 + sub);
+      add_bias(vb, e.bias[mat_a], blk_b * 16 + sub);
+    }
     float ra[4], rb[4];
-    if (mat_a < 2) {
+    if (mat_a < 2 && e.rope) {
       const float2* cs = e.rope + (size_t)pos * half + ia;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
@@ -123,6 +137,10 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, int pair, int lane, 
     const size_t ri = (size_t)(e.resid_mapped ? e.rows.idx[m] : m) * d;
     const size_t oi = (size_t)(e.out_mapped ? e.rows.idx[m] : m) * d;
     const int fa = blk_a * 16 + sub, fb = blk_b * 16 + sub;
+    if (e.bias[0]) {
+      add_bias(va, e.bias[0], fa);
+      if (b_ok) add_bias(vb, e.bias[0], fb);
+    }
     const float4 r0 = *(const float4*)(e.resid + ri + fa);
     const float4 oa = {r0.x + va[0], r0.y + va[1], r0.z + va[2], r0.w + va[3]};
     float4 ob = {0.f, 0.f, 0.f, 0.f};
@@ -159,6 +177,31 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, int pair, int lane, 
       for (int i = 0; i < 4; ++i) o[i] = f2bf(silu_f(va[i]) * vb[i]);
       *(u16x4*)(e.act + frag_off(m, f, e.kb_act)) = o;
     }
+  } else if constexpr (EPI == EPI_GELU) {
+#pragma unroll
+    for (int half = 0; half < 2; ++half) {
+      if (half == 1 && !b_ok) break;
+      const int f = (half ? blk_b : blk_a) * 16 + sub;
+      floatx4 v = half ? vb : va;
+      if (!valid || f >= e.n_feat) continue;
+      if (e.bias[0]) add_bias(v, e.bias[0], f);
+      const u16x4 o = {f2bf(gelu_f(v[0])), f2bf(gelu_f(v[1])), f2bf(gelu_f(v[2])), f2bf(gelu_f(v[3]))};
+      *(u16x4*)(e.act + frag_off(m, f, e.kb_act)) = o;
+    }
+  } else if constexpr (EPI == EPI_PATCH) {
+    if (!valid) return;
+    const float inv255 = 1.0f / 255.0f;
+    float* o = e.store + (size_t)m * e.ld_store;
+    const float* pt = e.pos_tab + (size_t)e.rows.pos[m] * e.ld_store;
+#pragma unroll
+    for (int half = 0; half < 2; ++half) {
+      if (half == 1 && !b_ok) break;
+      const int f = (half ? blk_b : blk_a) * 16 + sub;
+      const floatx4& v = half ? vb : va;
+      const float4 bb = *(const float4*)(e.bias[0] + f), pp = *(const float4*)(pt + f);
+      *(float4*)(o + f) = float4{v[0] * inv255 + bb.x + pp.x, v[1] * inv255 + bb.y + pp.y,
+                                 v[2] * inv255 + bb.z + pp.z, v[3] * inv255 + bb.w + pp.w};
+    }
   } else if constexpr (EPI == EPI_STORE) {
     if (!valid) return;
     float* o = e.store + (size_t)m * e.ld_store;
@@ -171,7 +214,7 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, int pair, int lane, 
     const int d = e.d;
     const int pos = e.rows.pos[m], b = e.rows.ep[m];
     float* h = e.h0 + (size_t)e.rows.idx[m] * d;
-    const float inv255 = 1.0f / 255.0f;
+    const float sc = e.vis_scale;
 #pragma unroll
     for (int half = 0; half < 2; ++half) {
       if (half == 1 && !b_ok) break;
@@ -179,7 +222,11 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, int pair, int lane, 
       const floatx4& v = half ? vb : va;
       float4 o;
       if (pos >= 1 && pos <= e.n_patches) {
-        o.x = v[0] * inv255; o.y = v[1] * inv255; o.z = v[2] * inv255; o.w = v[3] * inv255;
+        o.x = v[0] * sc; o.y = v[1] * sc; o.z = v[2] * sc; o.w = v[3] * sc;
+        if (e.bias[0]) {
+          const float4 bb = *(const float4*)(e.bias[0] + f);
+          o.x += bb.x; o.y += bb.y; o.z += bb.z; o.w += bb.w;
+        }
       } else if (pos < e.n_patches + e.n_text) {
         const int t = pos == 0 ? 0 : pos - e.n_patches;
         const bf16* er = e.embed + (size_t)e.text_ids[b * e.n_text + t] * d + f;
@@ -409,6 +456,8 @@ hipError_t launch_gemm(const GemmArgs& a, int epi, int NT, hipStream_t s) {
     case EPI_STORE: return launch_epi<EPI_STORE>(a, NT, s);
     case EPI_EMBED: return launch_epi<EPI_EMBED>(a, NT, s);
     case EPI_QKV_RAW: return launch_epi<EPI_QKV_RAW>(a, NT, s);
+    case EPI_PATCH: return launch_epi<EPI_PATCH>(a, NT, s);
+    case EPI_GELU: return launch_epi<EPI_GELU>(a, NT, s);
     default: return hipErrorInvalidValue;
   }
 }

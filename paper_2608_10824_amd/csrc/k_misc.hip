@@ -191,6 +191,63 @@ __global__ __launch_bounds__(256) void k_rmsnorm(const float* __restrict__ src, 
   }
 }
 
+// LayerNorm of fp32 rows (ViT blocks): (x - mean) / sqrt(var + eps) * gain
+// + bias, the variance taken about the mean in a second pass over the row;
+// bf16 out in frag layout.  One workgroup of 256 threads per row; d % 8 == 0.
+__global__ __launch_bounds__(256) void k_layernorm(const float* __restrict__ src, int d,
+                                                   const float* __restrict__ gain, const float* __restrict__ bias,
+                                                   float eps, bf16* __restrict__ x, int KB) {
+  __shared__ float red[2][4];
+  const int m = blockIdx.x;
+  const float* row = src + (size_t)m * d;
+  float s = 0.f;
+  for (int c = threadIdx.x * 8; c < d; c += 256 * 8) {
+    const float4 a = *(const float4*)(row + c), b = *(const float4*)(row + c + 4);
+    s += a.x + a.y + a.z + a.w + b.x + b.y + b.z + b.w;
+  }
+  for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o);
+  if ((threadIdx.x & 63) == 0) red[0][threadIdx.x >> 6] = s;
+  __syncthreads();
+  const float mean = (red[0][0] + red[0][1] + red[0][2] + red[0][3]) / (float)d;
+  float ss = 0.f;
+  for (int c = threadIdx.x * 8; c < d; c += 256 * 8) {
+    const float4 a = *(const float4*)(row + c), b = *(const float4*)(row + c + 4);
+    const float v[8] = {a.x - mean, a.y - mean, a.z - mean, a.w - mean, b.x - mean, b.y - mean, b.z - mean,
+                        b.w - mean};
+#pragma unroll
+    for (int i = 0; i < 8; ++i) ss += v[i] * v[i];
+  }
+  for (int o = 32; o > 0; o >>= 1) ss += __shfl_xor(ss, o);
+  if ((threadIdx.x & 63) == 0) red[1][threadIdx.x >> 6] = ss;
+  __syncthreads();
+  const float inv = 1.0f / sqrtf((red[1][0] + red[1][1] + red[1][2] + red[1][3]) / (float)d + eps);
+  for (int c = threadIdx.x * 8; c < d; c += 256 * 8) {
+    const float4 a = *(const float4*)(row + c), b = *(const float4*)(row + c + 4);
+    const float v[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+    u16x8 o;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) o[i] = f2bf((v[i] - mean) * inv * gain[c + i] + bias[c + i]);
+    *(u16x8*)(x + frag_off(m, c, KB)) = o;
+  }
+}
+
+// Projector input rows of the visual tokens recomputed at layer 0: row m of
+// the (position-sorted) list with position 1 <= pos <= N takes frag row
+// (episode * N + pos - 1) of src; other rows are zero (their embedding comes
+// from the token table or the given rows).  One thread per 8-element chunk.
+__global__ void k_gather_visual(const bf16* __restrict__ src, const int* __restrict__ idx,
+                                const int* __restrict__ pos_arr, int M, int P, int N, int KB,
+                                bf16* __restrict__ x) {
+  const int chunks = KB * 4;
+  const int e = blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= M * chunks) return;
+  const int m = e / chunks, k0 = (e % chunks) * 8;
+  const int pos = pos_arr[m];
+  u16x8 v = {0, 0, 0, 0, 0, 0, 0, 0};
+  if (pos >= 1 && pos <= N) v = *(const u16x8*)(src + frag_off((idx[m] / P) * N + pos - 1, k0, KB));
+  *(u16x8*)(x + frag_off(m, k0, KB)) = v;
+}
+
 // ------------------------------------------------------------------ logits
 // One workgroup per head row: greedy bin token (ties to the lower id) and
 // margin p1 - p2 with the softmax normaliser over the whole vocabulary (Eq. 1).
@@ -358,6 +415,22 @@ hipError_t launch_rmsnorm(const float* src, const int* idx, int M, int d, const 
                           int KB, hipStream_t s) {
   if (M == 0) return hipSuccess;
   hipLaunchKernelGGL(k_rmsnorm, dim3(M), dim3(256), 0, s, src, idx, d, gain, eps, x, KB);
+  return hipGetLastError();
+}
+
+hipError_t launch_layernorm(const float* src, int M, int d, const float* gain, const float* bias, float eps,
+                            bf16* x, int KB, hipStream_t s) {
+  if (M == 0) return hipSuccess;
+  if (d % 8) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_layernorm, dim3(M), dim3(256), 0, s, src, d, gain, bias, eps, x, KB);
+  return hipGetLastError();
+}
+
+hipError_t launch_gather_visual(const bf16* src, const int* idx, const int* pos, int M, int P, int N, int KB,
+                                bf16* x, hipStream_t s) {
+  const int n = M * KB * 4;
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_gather_visual, dim3((n + 255) / 256), dim3(256), 0, s, src, idx, pos, M, P, N, KB, x);
   return hipGetLastError();
 }
 

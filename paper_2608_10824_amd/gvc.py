@@ -17,7 +17,7 @@ REDUCE_MEAN, REDUCE_MIN = 0, 1
 
 (K_DECODE_QKV, K_DECODE_ATTN, K_DECODE_O, K_DECODE_GU, K_DECODE_DOWN, K_DECODE_HEAD, K_PREFILL_QKV,
  K_PREFILL_ATTN, K_PREFILL_O, K_PREFILL_GU, K_PREFILL_DOWN, K_PREFILL_HEAD, K_EMBED, K_NORM, K_SELECT,
- K_DECODE_PASS, K_STAGE2) = range(17)
+ K_DECODE_PASS, K_STAGE2, K_VIT) = range(18)
 
 EXPORTED = ("gvc_sizes", "gvc_init_cache", "gvc_select_static", "gvc_step_prefill", "gvc_decode_actions",
             "gvc_margin_gate", "gvc_invalidate", "gvc_read_state", "gvc_state_item_bytes", "gvc_profile_begin",
@@ -35,16 +35,32 @@ class Desc(ctypes.Structure):
         "batch", "n_layers", "d_model", "n_heads", "ffn", "vocab", "n_bins", "img", "patch", "n_views",
         "n_text", "n_proprio", "n_action_q", "n_decode", "parallel_decode", "norm_full_vocab")] + [
         ("rms_eps", ctypes.c_float), ("rope_theta", ctypes.c_float), ("task_topk", ctypes.c_int32),
-        ("entropy_reuse", ctypes.c_int32), ("action_bidir", ctypes.c_int32)]
+        ("entropy_reuse", ctypes.c_int32), ("action_bidir", ctypes.c_int32), ("vit_layers", ctypes.c_int32),
+        ("vit_dim", ctypes.c_int32), ("vit_heads", ctypes.c_int32), ("vit_ffn", ctypes.c_int32),
+        ("vit_eps", ctypes.c_float)]
 
 
 class LayerWeights(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in ("wq", "wk", "wv", "wo", "wg", "wu", "wd", "attn_norm", "ffn_norm")]
 
 
+VIT_LAYER_FIELDS = ("ln1_g", "ln1_b", "wq", "bq", "wk", "bk", "wv", "bv", "wo", "bo", "ln2_g", "ln2_b", "w1", "b1",
+                    "w2", "b2")
+VIT_FIELDS = ("patch_w", "patch_b", "pos", "post_g", "post_b", "proj1", "proj1_b", "proj2", "proj2_b")
+
+
+class VitLayerWeights(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in VIT_LAYER_FIELDS]
+
+
+class VitWeights(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in VIT_FIELDS] + [("layers", ctypes.POINTER(VitLayerWeights))]
+
+
 class Weights(ctypes.Structure):
     _fields_ = [("embed", ctypes.c_void_p), ("patch_proj", ctypes.c_void_p), ("lm_head", ctypes.c_void_p),
-                ("final_norm", ctypes.c_void_p), ("layers", ctypes.POINTER(LayerWeights))]
+                ("final_norm", ctypes.c_void_p), ("layers", ctypes.POINTER(LayerWeights)),
+                ("vit", ctypes.POINTER(VitWeights))]
 
 
 _lib = None

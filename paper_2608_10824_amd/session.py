@@ -4,6 +4,8 @@ PyTorch provides device memory and the stream; every computation is a call
 into libgvc.  The session owns the arenas the library asks for, the output
 buffers of each call and the context handle.
 """
+import ctypes
+
 import torch
 
 from . import gvc
@@ -17,11 +19,17 @@ def desc_from(cfg) -> gvc.Desc:
                     n_decode=cfg.n_decode, parallel_decode=int(cfg.parallel_decode),
                     norm_full_vocab=int(cfg.norm_full_vocab), rms_eps=cfg.rms_eps, rope_theta=cfg.rope_theta,
                     task_topk=cfg.task_topk, entropy_reuse=int(cfg.entropy_reuse),
-                    action_bidir=int(cfg.action_bidir))
+                    action_bidir=int(cfg.action_bidir), vit_layers=cfg.vit_layers, vit_dim=cfg.vit_dim,
+                    vit_heads=cfg.vit_heads, vit_ffn=cfg.vit_ffn, vit_eps=cfg.vit_eps)
 
 
 def _ptr(t):
     return None if t is None else t.data_ptr()
+
+
+def _bf16_ptr(t):
+    assert t.is_cuda and t.dtype == torch.bfloat16 and t.is_contiguous()
+    return t.data_ptr()
 
 
 class Session:
@@ -48,6 +56,15 @@ class Session:
         w = gvc.Weights(embed=weights["embed"].data_ptr(), patch_proj=weights["patch_proj"].data_ptr(),
                         lm_head=weights["lm_head"].data_ptr(), final_norm=weights["final_norm"].data_ptr(),
                         layers=layers)
+        if cfg.vit_layers > 0:
+            vw = weights["vit"]
+            vl = (gvc.VitLayerWeights * cfg.vit_layers)()
+            for l, lw in enumerate(vw["layers"]):
+                for k in gvc.VIT_LAYER_FIELDS:
+                    setattr(vl[l], k, _bf16_ptr(lw[k]))
+            self._vit = gvc.VitWeights(layers=vl, **{k: _bf16_ptr(vw[k]) for k in gvc.VIT_FIELDS})
+            self._vit_layers = vl
+            w.vit = ctypes.pointer(self._vit)
         self.stream = torch.cuda.current_stream(self.device)
         self.ctx = gvc.init_cache(self.desc, w, self.weight_arena.data_ptr(), wb, self.state.data_ptr(), sb,
                                   self.workspace.data_ptr(), kb, self.stream.cuda_stream)

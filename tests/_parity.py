@@ -13,8 +13,10 @@ def rel_err(g, o) -> float:
 
 
 def to_dev(w, dev):
-    out = {k: v.to(dev) for k, v in w.items() if k != "layers"}
+    out = {k: v.to(dev) for k, v in w.items() if k not in ("layers", "vit")}
     out["layers"] = [{k: v.to(dev) for k, v in lw.items()} for lw in w["layers"]]
+    if "vit" in w:
+        out["vit"] = to_dev(w["vit"], dev)
     return out
 
 

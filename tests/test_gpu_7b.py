@@ -150,6 +150,54 @@ def test_c2_head_and_decode_chain(c2):
     check_margins(c2["mg"][0], m_o, lg, zo, cfg.bin_lo)
 
 
+# ---------------------------------------------------------------- C2 with the ViT front end
+def test_c2v_front_end_and_layers():
+    """ViT-L/14-shaped front end at the 7B shape: the layer-0 input of every
+    prompt row (visual rows from the GPU's ViT and projector) against the
+    oracle's, after a full and after a partial step; sampled layers; the
+    head logits."""
+    from paper_2608_10824_amd import gvc
+    from oracle.vit import visual_embeddings
+    from oracle.vla import convert_weights
+    cfg = synth.config_c2v()
+    s, w = _session(cfg)
+    si = synth.step_inputs(cfg, 128)
+    fp, ft, ids, ex = _two_steps(cfg, s, si)
+    P, N, L = cfg.prompt_len, cfg.n_patches, cfg.n_layers
+    vw = convert_weights({"vit": w["vit"]})["vit"]
+    g = glob_w64(w)
+    ids_np = si["text_ids"].numpy()[0]
+
+    def h0_oracle(frame):
+        h = np.empty((P, cfg.d_model))
+        h[0] = g["embed"][ids_np[0]]
+        h[1:N + 1] = visual_embeddings(vw, frame, cfg.patch, cfg.vit_heads, cfg.vit_eps)
+        h[N + 1:] = g["embed"][ids_np[1:]]
+        return h
+
+    e_full = rel_err(state64(s, gvc.STATE_H, 0, 0, P), h0_oracle(si["frame_prev"].numpy()[0]))
+    mask, _ = s.select_static(ft, fp)
+    mask = mask.cpu().numpy().astype(bool)
+    s.step_prefill(ft, ids, ex, s.mask)
+    H0 = state64(s, gvc.STATE_H, 0, 0, P)
+    ref = h0_oracle(si["frame_t"].numpy()[0])
+    reused = [1 + n for n in np.nonzero(mask[0, 0])[0]]
+    fresh = [p for p in range(P) if p not in reused]
+    e_part = rel_err(H0[fresh], ref[fresh])
+    print("layer-0 input rel err: full %.2e, recomputed rows of the partial step %.2e" % (e_full, e_part))
+    assert e_full <= TOL and e_part <= TOL
+    sample = _sample_rows(cfg, fresh)
+    for l in (0, L - 1):
+        errs = check_layer_sampled(cfg, layer_w64(w, l), state64(s, gvc.STATE_H, l, 0, P),
+                                   state64(s, gvc.STATE_H, l + 1, 0, P), state64(s, gvc.STATE_K, l, 0, P),
+                                   state64(s, gvc.STATE_V, l, 0, P), sample)
+        print("layer", l, {k: "%.2e" % v for k, v in errs.items()})
+        assert all(v <= TOL for v in errs.values()), (l, errs)
+    z0 = head_row(state64(s, gvc.STATE_H, L, 0, P)[P - 1], g["final_norm"], g["lm_head"], cfg.rms_eps)
+    assert rel_err(s.read(gvc.STATE_HEAD_LOGITS).cpu().numpy()[0, 0], z0) <= TOL
+    s.close()
+
+
 # ---------------------------------------------------------------- C4
 @pytest.fixture(scope="module", params=["causal", "bidir"])
 def c4(request):

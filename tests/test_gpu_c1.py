@@ -3,7 +3,9 @@
 rows: five 16-row token blocks, the last one partial) and on a mid-size
 config (d=2048, 16 heads of 128, FFN 5504: several pipelined k chunks per
 wave plus a ragged k tail; two views, 136 rows: two token groups of 16-row
-blocks, the last one partial).  Every call goes through the C ABI."""
+blocks, the last one partial), each also with the ViT front end (C1V: one
+view, heads of 64; MIDV: two views, heads of 128), whose visual embeddings
+then enter every compared state.  Every call goes through the C ABI."""
 import numpy as np
 import pytest
 import torch
@@ -15,11 +17,17 @@ from tests._parity import TOL, rel_err, to_dev, gpu_k, gpu_v, check_tokens, chec
 pytestmark = pytest.mark.gpu
 
 
-@pytest.fixture(scope="module", params=["C1", "MID"])
+def _config_midv():
+    """MID (two views, heads of 128) with a ViT front end of heads of 128."""
+    return synth.config_mid().with_(name="MIDV", vit_layers=2, vit_dim=256, vit_heads=2, vit_ffn=1024)
+
+
+@pytest.fixture(scope="module", params=["C1", "MID", "C1V", "MIDV"])
 def c1(request):
     from paper_2608_10824_amd.session import Session
     from paper_2608_10824_amd import gvc
-    cfg = synth.config_c1() if request.param == "C1" else synth.config_mid()
+    cfg = {"C1": synth.config_c1, "MID": synth.config_mid, "C1V": synth.config_c1v, "MIDV": _config_midv}[
+        request.param]()
     w = synth.model_weights(cfg)
     si = synth.step_inputs(cfg, 45 * cfg.n_views)
     dev = torch.device("cuda:0")
