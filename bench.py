@@ -41,6 +41,7 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-c3", action="store_true", help="skip the C3 episode (recompute rate)")
     ap.add_argument("--no-c4", action="store_true", help="skip the C4 action-chunk queries")
+    ap.add_argument("--no-vit", action="store_true", help="skip the steps with the ViT front end")
     ap.add_argument("--no-stage2", action="store_true",
                     help="skip the Stage 2 (top-k = 120) and Stage 2 + entropy Stage 3 steps")
     return ap.parse_args()
@@ -183,6 +184,54 @@ def c4_chunk(dev, steps, warmup):
             "static_patches_reused": 307, "recomputed_rows_per_layer": rows[0], "ms_per_query": dt * 1e3,
             "queries_per_s": 1.0 / dt, "chunk_steps": chunk, "control_steps_per_s_chunked": chunk / dt,
             "steps": steps}
+
+
+def vit_steps(dev, steps, warmup):
+    """C2 with the ViT-L/14-shaped front end (24 blocks of width 1024, GELU
+    projector to 4096) in place of the linear patch projection: every step
+    runs the front end over all 256 patches, then the same partial prompt
+    pass (128 static patches reused) and decode.  Reports the time per
+    control step and the front end's GPU time per step."""
+    import torch
+    import synth
+    from paper_2608_10824_amd import gvc
+    from paper_2608_10824_amd.session import Session
+    cfg = synth.config_c2v()
+    w = synth.model_weights(cfg, device=dev)
+    s = Session(cfg, w, device=dev)
+    torch.cuda.synchronize()
+    del w
+    torch.cuda.empty_cache()
+    note("C2 + ViT weights generated")
+    si = synth.step_inputs(cfg, 128)
+    fp, ft = si["frame_prev"].to(dev), si["frame_t"].to(dev)
+    ids = si["text_ids"].to(dev)
+    s.step_prefill(fp, ids)
+    s.decode_actions()
+
+    def step():
+        s.margin_gate(force=[0])
+        mask, _ = s.select_static(ft, fp)
+        s.step_prefill(ft, ids, None, mask)
+        s.decode_actions()
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    dt = (time.perf_counter() - t0) / steps
+    per_step = 2 + cfg.vit_layers * 7 + 2
+    gvc.profile_begin(s.ctx, gvc.K_VIT, per_step + 8)
+    step()
+    torch.cuda.synchronize()
+    vit_ms, vit_n = gvc.profile_end(s.ctx)
+    s.close()
+    return {"vit": "ViT-L/14 shape: 24 blocks, width 1024, 16 heads, MLP 4096; projector 1024 -> 4096 -> 4096",
+            "ms_per_step": dt * 1e3, "control_steps_per_s": 1.0 / dt, "front_end_ms_per_step": vit_ms,
+            "front_end_launches": vit_n, "steps": steps}
 
 
 def staged_steps(cfg, w, si, dev, steps, warmup, entropy=False):
@@ -409,6 +458,9 @@ def main():
         note("Stage 2 + 3 steps done: layer proportions %s" % out["stage3_entropy"]["layer_permille"][:4])
         del w_stage2
         torch.cuda.empty_cache()
+    if not args.no_vit:
+        out["c2_vit"] = vit_steps(dev, min(args.steps, 10), 2)
+        note("C2 + ViT steps done: %.2f ms per step" % out["c2_vit"]["ms_per_step"])
     if not args.no_c4:
         out["c4_chunk"] = c4_chunk(dev, min(args.steps, 10), 2)
         note("C4 chunk queries done: %.2f ms per query" % out["c4_chunk"]["ms_per_query"])
