@@ -42,6 +42,7 @@ def parse():
     ap.add_argument("--no-c3", action="store_true", help="skip the C3 episode (recompute rate)")
     ap.add_argument("--no-c4", action="store_true", help="skip the C4 action-chunk queries")
     ap.add_argument("--no-vit", action="store_true", help="skip the steps with the ViT front end")
+    ap.add_argument("--no-c5", action="store_true", help="skip the batch-16 prompt passes")
     ap.add_argument("--no-stage2", action="store_true",
                     help="skip the Stage 2 (top-k = 120) and Stage 2 + entropy Stage 3 steps")
     return ap.parse_args()
@@ -184,6 +185,58 @@ def c4_chunk(dev, steps, warmup):
             "static_patches_reused": 307, "recomputed_rows_per_layer": rows[0], "ms_per_query": dt * 1e3,
             "queries_per_s": 1.0 / dt, "chunk_steps": chunk, "control_steps_per_s_chunked": chunk / dt,
             "steps": steps}
+
+
+def c5_prefill(dev, reps, ks=(0, 128, 230)):
+    """C5, 16 episodes batched: the prompt pass after a full step, for k of
+    256 patches static in every episode.  With 16 x 148 = 2368 recomputed
+    rows the projections are MFMA-bound, so this is where the prompt pass's
+    MFMA utilisation is measured.  Reports per k the time of the partial
+    prompt pass, its algorithmic TFLOP/s and the fraction of the dense bf16
+    MFMA peak."""
+    import torch
+    import synth
+    from paper_2608_10824_amd import gvc
+    from paper_2608_10824_amd.session import Session
+    cfg = synth.config_c5()
+    w = synth.model_weights(cfg, device=dev)
+    s = Session(cfg, w, device=dev)
+    torch.cuda.synchronize()
+    del w
+    torch.cuda.empty_cache()
+    note("C5 weights generated")
+    d, F, V, L, P, B = cfg.d_model, cfg.ffn, cfg.vocab, cfg.n_layers, cfg.prompt_len, cfg.batch
+    out = []
+    for k in ks:
+        si = synth.step_inputs(cfg, k, stream=k + 1)
+        fp, ft = si["frame_prev"].to(dev), si["frame_t"].to(dev)
+        ids = si["text_ids"].to(dev)
+        s.invalidate()
+        s.step_prefill(fp, ids)
+        s.decode_actions()
+        s.margin_gate(force=[0] * B)
+        mask, _ = s.select_static(ft, fp)
+        s.step_prefill(ft, ids, None, mask)       # warm-up of this row count
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            s.step_prefill(ft, ids, None, mask)   # the cache stays valid: the same partial pass each time
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / reps
+        m = mask.cpu().numpy().astype(bool)
+        flops = 2 * B * V * d
+        for b in range(B):
+            for l in range(L):
+                qpos = [p for p in range(P) if not (1 <= p <= cfg.n_patches and m[b, l, p - 1])]
+                flops += 2 * len(qpos) * (4 * d * d + 3 * d * F) + 2 * sum(2 * (p + 1) * d for p in qpos)
+        tf = flops / (ms / 1e3) / 1e12
+        out.append({"static_per_episode": k, "rows_per_layer": B * (P - k), "prefill_ms": ms, "tflops": tf,
+                    "mfma_util_pct": 100.0 * tf / BF16_PEAK_TFLOPS})
+        note("C5 k=%d: %.2f ms, %.0f TFLOP/s" % (k, ms, tf))
+    s.close()
+    return out
 
 
 def vit_steps(dev, steps, warmup):
@@ -458,6 +511,8 @@ def main():
         note("Stage 2 + 3 steps done: layer proportions %s" % out["stage3_entropy"]["layer_permille"][:4])
         del w_stage2
         torch.cuda.empty_cache()
+    if not args.no_c5:
+        out["c5_prefill"] = c5_prefill(dev, min(args.steps, 5))
     if not args.no_vit:
         out["c2_vit"] = vit_steps(dev, min(args.steps, 10), 2)
         note("C2 + ViT steps done: %.2f ms per step" % out["c2_vit"]["ms_per_step"])

@@ -29,6 +29,7 @@ int32_t fail(int32_t code, const std::string& msg) {
 
 constexpr size_t kAlign = 256;
 constexpr int kMaxNT = 5;   // token blocks per GEMM workgroup (best of 2..16 on the 7B prompt pass)
+constexpr int kBigRows = 1024;  // sessions with at least this many prompt rows use k_gemm_big
 
 struct Bump {
   size_t off = 0;
@@ -265,6 +266,11 @@ struct gvc_ctx {
   bool prefill_done = false;
   bool decode_done = false;
   int force_splits = 0;   // GVC_FORCE_SPLITS: waves splitting each GEMM's k range (4 or 8; testing)
+  // prompt-pass projections on the many-row kernel: sessions of at least
+  // kBigRows prompt rows (B * P), for every pass of the session, so a row's
+  // result never depends on how many rows a pass recomputes; GVC_GEMM=big
+  // or small overrides (testing)
+  bool big_gemm = false;
   // persistent decode pass (k_decode.hip): eligible shape, its grid and LDS
   bool persist = false;
   int persist_wg = 0;
@@ -354,8 +360,16 @@ GemmArgs base_args(const gvc_ctx* c) {
 }
 
 
-int32_t run_gemm(gvc_ctx* c, GemmArgs& a, int epi, int M, int cls) {
+int32_t run_gemm(gvc_ctx* c, GemmArgs& a, int epi, int M, int cls, bool big = false) {
   if (M <= 0) return GVC_OK;
+  if (big) {
+    a.M = M;
+    a.mblocks = (M + 15) / 16;
+    a.mtiles = (a.mblocks + kGemmBigTok - 1) / kGemmBigTok;
+    ProfScope ps(c, cls);
+    HIP_TRY(launch_gemm_big(a, epi, c->stream));
+    return GVC_OK;
+  }
   tile_gemm(a, M, c->force_splits);
   // the folded RMSNorm reads at most 16 partial sums per lane, 4 lanes per wave per row
   if (a.e.ssq_in && (a.mblocks > 1 || a.e.ssq_parts > 16 * 4 * a.splits))
@@ -504,7 +518,7 @@ int32_t run_layer(gvc_ctx* c, int l, const RowMap& rows, int M, float* src, floa
     a.map = MAP_QKV; a.n_pairs = 3 * p.wq[l].Nblk / 2; a.n_out = p.d.d_model; a.KB = p.KBd;
     a.x = reinterpret_cast<const bf16x8*>(X);
     a.e.rows = rows; a.e.q = Q; a.e.kc = c->Kc(l); a.e.vc = c->Vc(l);
-    int32_t r = run_gemm(c, a, EPI_QKV, M, k0);
+    int32_t r = run_gemm(c, a, EPI_QKV, M, k0, c->big_gemm);
     if (r) return r;
   }
   {
@@ -525,7 +539,7 @@ int32_t run_layer(gvc_ctx* c, int l, const RowMap& rows, int M, float* src, floa
     a.map = MAP_PLAIN; a.n_pairs = (p.wo[l].Nblk + 1) / 2; a.n_out = p.d.d_model; a.KB = p.KBd;
     a.x = reinterpret_cast<const bf16x8*>(O);
     a.e.rows = rows; a.e.resid = src; a.e.resid_mapped = mapped; a.e.out = R; a.e.out_mapped = 0;
-    int32_t r = run_gemm(c, a, EPI_RESID, M, k0 + 2);
+    int32_t r = run_gemm(c, a, EPI_RESID, M, k0 + 2, c->big_gemm);
     if (r) return r;
   }
   {
@@ -539,7 +553,7 @@ int32_t run_layer(gvc_ctx* c, int l, const RowMap& rows, int M, float* src, floa
     a.map = MAP_GU; a.n_pairs = p.wg[l].Nblk; a.n_out = p.F; a.KB = p.KBd;
     a.x = reinterpret_cast<const bf16x8*>(X);
     a.e.rows = rows; a.e.act = A; a.e.kb_act = p.KBf; a.e.n_feat = p.F;
-    int32_t r = run_gemm(c, a, EPI_SILU, M, k0 + 3);
+    int32_t r = run_gemm(c, a, EPI_SILU, M, k0 + 3, c->big_gemm);
     if (r) return r;
   }
   {
@@ -548,7 +562,7 @@ int32_t run_layer(gvc_ctx* c, int l, const RowMap& rows, int M, float* src, floa
     a.map = MAP_PLAIN; a.n_pairs = (p.wd[l].Nblk + 1) / 2; a.n_out = p.d.d_model; a.KB = p.KBf;
     a.x = reinterpret_cast<const bf16x8*>(A);
     a.e.rows = rows; a.e.resid = R; a.e.resid_mapped = 0; a.e.out = dst; a.e.out_mapped = mapped;
-    int32_t r = run_gemm(c, a, EPI_RESID, M, k0 + 4);
+    int32_t r = run_gemm(c, a, EPI_RESID, M, k0 + 4, c->big_gemm);
     if (r) return r;
   }
   return GVC_OK;
@@ -789,6 +803,11 @@ int32_t gvc_init_cache(const gvc_desc* desc, const gvc_weights* wt, void* weight
 
   INIT_TRY(hipGetDevice(&c->device));
   if (const char* fs = getenv("GVC_FORCE_SPLITS")) c->force_splits = atoi(fs);
+  c->big_gemm = p.B * p.P >= kBigRows;
+  if (const char* g = getenv("GVC_GEMM")) {
+    if (!strcmp(g, "big")) c->big_gemm = true;
+    if (!strcmp(g, "small")) c->big_gemm = false;
+  }
   INIT_TRY(launch_fill_u32(reinterpret_cast<uint32_t*>(c->st), 0u, p.state_bytes / 4, s));
   INIT_TRY(launch_fill_u32(reinterpret_cast<uint32_t*>(c->ws), 0u, p.ws_bytes / 4, s));
   for (int l = 0; l < p.L; ++l) {
@@ -949,7 +968,7 @@ int32_t gvc_step_prefill(gvc_ctx* c, const uint8_t* frame_t, const int32_t* text
     a.x = reinterpret_cast<const bf16x8*>(X);
     a.e.rows = r0; a.e.h0 = c->H(0); a.e.embed = c->W<bf16>(p.embed_off); a.e.text_ids = text_ids;
     a.e.extra = extra_rows; a.e.n_patches = p.N; a.e.n_text = p.d.n_text; a.e.n_extra = p.n_extra;
-    int32_t r = run_gemm(c, a, EPI_EMBED, c->counts[0], GVC_K_EMBED);
+    int32_t r = run_gemm(c, a, EPI_EMBED, c->counts[0], GVC_K_EMBED, c->big_gemm);
     if (r) return r;
   }
   const int max_tiles = (p.P + 15) / 16;

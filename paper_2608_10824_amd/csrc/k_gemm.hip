@@ -394,6 +394,138 @@ __global__ __launch_bounds__(KS * KT * 64) void k_gemm_ks(const GemmArgs a) {
   }
 }
 
+// Many-row variant (batched episodes: thousands of rows, MFMA-bound).  A
+// workgroup of 8 waves owns kBigPairs weight pairs x kBigTok blocks of 16
+// token rows and walks the whole k range; every k step, both operands'
+// fragments for the tile (2 kBigPairs weight + kBigTok token fragments)
+// are copied straight into LDS (global_load_lds), three stages deep so one
+// step is in flight while another is read, with one workgroup barrier per
+// step.  Wave (wp, wt) multiplies pairs wp*2..wp*2+1 by token blocks
+// wt*4..wt*4+3 (16 MFMAs per k step from 8 LDS fragment reads) and runs the
+// same fused epilogue as k_gemm_ks.  Each row's sum runs over k in order, so
+// a row's result does not depend on the tile it falls in.
+constexpr int kBigWP = 2, kBigWT = 4, kBigPW = 2, kBigTW = 4;
+constexpr int kBigPairs = kBigWP * kBigPW, kBigTok = kBigWT * kBigTW;
+static_assert(kBigTok == kGemmBigTok, "token tile of the many-row kernel");
+constexpr int kBigFrags = 2 * kBigPairs + kBigTok;   // fragments per k step
+constexpr int kBigStages = 3;
+constexpr int kBigLds = kBigStages * kBigFrags * 1024;
+
+typedef unsigned u32x4b __attribute__((ext_vector_type(4)));
+#define GPB(p) ((const void __attribute__((address_space(1)))*)(p))
+#define LPB(p) ((void __attribute__((address_space(3)))*)(p))
+
+template <int N>
+__device__ __forceinline__ void big_wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x0F70);
+}
+
+template <int EPI>
+__global__ __launch_bounds__(kBigWP * kBigWT * 64) void k_gemm_big(const GemmArgs a) {
+  constexpr int NW = kBigWP * kBigWT;
+  constexpr int WF = 2 * kBigPairs;
+  constexpr int LPW = (kBigFrags + NW - 1) / NW;   // fragment copies per wave per k step
+  extern __shared__ u32x4b big_lds[];              // [kBigStages][kBigFrags][64]
+  const int lane = threadIdx.x & 63, wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wp = wv % kBigWP, wt = wv / kBigWP;
+  // XCD-aware order: all tiles of one weight tile run on XCD (tile % 8) and
+  // share its weights in that L2
+  const int x = blockIdx.x, xcd = x & 7, i = x >> 3;
+  const int nt = xcd + 8 * (i / a.mtiles), mt = i % a.mtiles;
+  const int ntiles = (a.n_pairs + kBigPairs - 1) / kBigPairs;
+  if (nt >= ntiles) return;
+  const int pair0 = nt * kBigPairs, tb0 = mt * kBigTok;
+  const bf16x8* src[LPW];
+  int dst[LPW];
+#pragma unroll
+  for (int l = 0; l < LPW; ++l) {
+    const int f = min(wv + l * NW, kBigFrags - 1);
+    dst[l] = f;
+    if (f < WF) {
+      int ma, ba, mb, bb; bool ok;
+      map_pair(a, min(pair0 + f / 2, a.n_pairs - 1), ma, ba, mb, bb, ok);
+      src[l] = (f & 1) ? a.w[mb] + (size_t)bb * a.KB * 64 + lane : a.w[ma] + (size_t)ba * a.KB * 64 + lane;
+    } else {
+      src[l] = a.x + (size_t)min(tb0 + f - WF, a.mblocks - 1) * a.KB * 64 + lane;
+    }
+  }
+  auto issue = [&](int k) {   // k steps past the end re-read the last one (in bounds)
+    u32x4b* st = big_lds + (k % kBigStages) * kBigFrags * 64;
+    const size_t o = (size_t)min(k, a.KB - 1) * 64;
+#pragma unroll
+    for (int l = 0; l < LPW; ++l) __builtin_amdgcn_global_load_lds(GPB(src[l] + o), LPB(st + dst[l] * 64), 16, 0, 0);
+  };
+  floatx4 acc[2 * kBigPW][kBigTW];
+#pragma unroll
+  for (int p = 0; p < 2 * kBigPW; ++p)
+#pragma unroll
+    for (int j = 0; j < kBigTW; ++j) acc[p][j] = floatx4{0, 0, 0, 0};
+  issue(0);
+  for (int k = 0; k < a.KB; ++k) {
+    // stage (k + 1) % 3 last held step k - 2, which every wave finished
+    // before the barrier of step k - 1
+    issue(k + 1);
+    big_wait_vm<LPW>();
+    __syncthreads();
+    const u32x4b* st = big_lds + (k % kBigStages) * kBigFrags * 64;
+    bf16x8 wf[2 * kBigPW], xf[kBigTW];
+#pragma unroll
+    for (int p = 0; p < 2 * kBigPW; ++p) wf[p] = __builtin_bit_cast(bf16x8, st[(2 * wp * kBigPW + p) * 64 + lane]);
+#pragma unroll
+    for (int j = 0; j < kBigTW; ++j) xf[j] = __builtin_bit_cast(bf16x8, st[(WF + wt * kBigTW + j) * 64 + lane]);
+#pragma unroll
+    for (int j = 0; j < kBigTW; ++j)
+#pragma unroll
+      for (int p = 0; p < 2 * kBigPW; ++p) acc[p][j] = mfma16(wf[p], xf[j], acc[p][j]);
+  }
+  big_wait_vm<0>();
+  const int col = lane & 15;
+#pragma unroll
+  for (int p = 0; p < kBigPW; ++p) {
+    const int pair = pair0 + wp * kBigPW + p;
+    if (pair >= a.n_pairs) continue;
+    int ma, ba, mb, bb; bool b_ok;
+    map_pair(a, pair, ma, ba, mb, bb, b_ok);
+#pragma unroll
+    for (int j = 0; j < kBigTW; ++j) {
+      const int m = (tb0 + wt * kBigTW + j) * 16 + col;
+      epilogue<EPI>(a, pair, lane, min(m, a.M - 1), acc[2 * p][j], acc[2 * p + 1][j], b_ok, m < a.M, 1.0f);
+    }
+  }
+}
+
+template <int EPI>
+static hipError_t launch_big_epi(const GemmArgs& a, hipStream_t s) {
+  static bool attr = false;
+  if (!attr) {
+    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_gemm_big<EPI>),
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, kBigLds);
+    if (e != hipSuccess) return e;
+    attr = true;
+  }
+  const int ntiles = (a.n_pairs + kBigPairs - 1) / kBigPairs;
+  const dim3 grid(8 * ((ntiles + 7) / 8) * a.mtiles);
+  hipLaunchKernelGGL(k_gemm_big<EPI>, grid, dim3(kBigWP * kBigWT * 64), kBigLds, s, a);
+  return hipGetLastError();
+}
+
+// a.mtiles counts tiles of kBigTok token blocks here; pair maps only, no
+// folded norm.
+hipError_t launch_gemm_big(const GemmArgs& a, int epi, hipStream_t s) {
+  if (a.map == MAP_SINGLE || a.map == MAP_QKV_SINGLE || a.e.ssq_in) return hipErrorInvalidValue;
+  switch (epi) {
+    case EPI_QKV: return launch_big_epi<EPI_QKV>(a, s);
+    case EPI_RESID: return launch_big_epi<EPI_RESID>(a, s);
+    case EPI_SILU: return launch_big_epi<EPI_SILU>(a, s);
+    case EPI_STORE: return launch_big_epi<EPI_STORE>(a, s);
+    case EPI_EMBED: return launch_big_epi<EPI_EMBED>(a, s);
+    case EPI_PATCH: return launch_big_epi<EPI_PATCH>(a, s);
+    case EPI_GELU: return launch_big_epi<EPI_GELU>(a, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
 template <int EPI, int KT, int NT, bool ONE>
 static hipError_t launch_one(const GemmArgs& a, hipStream_t s) {
   constexpr int PF = gemm_pf(NT);

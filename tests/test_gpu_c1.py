@@ -5,7 +5,11 @@ config (d=2048, 16 heads of 128, FFN 5504: several pipelined k chunks per
 wave plus a ragged k tail; two views, 136 rows: two token groups of 16-row
 blocks, the last one partial), each also with the ViT front end (C1V: one
 view, heads of 64; MIDV: two views, heads of 128), whose visual embeddings
-then enter every compared state.  Every call goes through the C ABI."""
+then enter every compared state, and each with the prompt-pass projections
+on the many-row kernel (C1-big, MID-big) that sessions of 1024 or more
+prompt rows use.  Every call goes through the C ABI."""
+import os
+
 import numpy as np
 import pytest
 import torch
@@ -22,16 +26,23 @@ def _config_midv():
     return synth.config_mid().with_(name="MIDV", vit_layers=2, vit_dim=256, vit_heads=2, vit_ffn=1024)
 
 
-@pytest.fixture(scope="module", params=["C1", "MID", "C1V", "MIDV"])
+@pytest.fixture(scope="module", params=["C1", "MID", "C1V", "MIDV", "C1-big", "MID-big"])
 def c1(request):
     from paper_2608_10824_amd.session import Session
     from paper_2608_10824_amd import gvc
-    cfg = {"C1": synth.config_c1, "MID": synth.config_mid, "C1V": synth.config_c1v, "MIDV": _config_midv}[
-        request.param]()
+    name = request.param.replace("-big", "")
+    cfg = {"C1": synth.config_c1, "MID": synth.config_mid, "C1V": synth.config_c1v, "MIDV": _config_midv}[name]()
     w = synth.model_weights(cfg)
     si = synth.step_inputs(cfg, 45 * cfg.n_views)
     dev = torch.device("cuda:0")
-    s = Session(cfg, to_dev(w, dev), device=dev)
+    # "-big": the prompt-pass projections on the many-row kernel, which
+    # sessions of at least 1024 prompt rows use
+    if request.param.endswith("-big"):
+        os.environ["GVC_GEMM"] = "big"
+    try:
+        s = Session(cfg, to_dev(w, dev), device=dev)
+    finally:
+        os.environ.pop("GVC_GEMM", None)
     o = OracleVLA(cfg, w)
     yield cfg, w, si, s, o, dev
     s.close()

@@ -94,14 +94,21 @@ def test_parallel_action_chunk_complete_parity(name):
     s.close()
 
 
-def test_identical_frame_full_reuse_is_bit_identical():
+@pytest.mark.parametrize("gemm", ["small", "big"])
+def test_identical_frame_full_reuse_is_bit_identical(gemm):
     """After a full step, the same frame with every patch reused recomputes
     only the text rows; with deterministic, row-independent kernels the
-    whole state must equal the previous step bit for bit."""
+    whole state must equal the previous step bit for bit (with either
+    prompt-pass GEMM kernel)."""
+    import os
     cfg = synth.config_c1()
     w = synth.model_weights(cfg)
     si = synth.step_inputs(cfg, 45)
-    s = _session(cfg, w)
+    os.environ["GVC_GEMM"] = gemm
+    try:
+        s = _session(cfg, w)
+    finally:
+        os.environ.pop("GVC_GEMM", None)
     fp, ids = si["frame_prev"].to(DEV), si["text_ids"].to(DEV)
     s.step_prefill(fp, ids)
     ref = _state(s, cfg)
