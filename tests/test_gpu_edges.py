@@ -238,3 +238,47 @@ def test_decode_pass_matches_per_step_launches(cfg_fn, monkeypatch):
     assert rel_err(got["single"], lg_o) <= TOL
     assert rel_err(got["legacy"], lg_o) <= TOL
     assert rel_err(got["single"], got["legacy"]) <= TOL
+
+
+@pytest.mark.parametrize("name", ["C1V-B2", "C4T-bidir-B2"])
+def test_batched_front_end_and_action_block(name):
+    """Two episodes at once: the ViT front end (two views, so four view
+    passes) and the action block each run per episode; every state element
+    of both episodes after a full and a partial step, against the oracle."""
+    from paper_2608_10824_amd import gvc
+    if name == "C1V-B2":
+        cfg = synth.config_c1v().with_(batch=2, n_views=2)
+    else:
+        cfg = synth.config_c4_tiny().with_(batch=2, action_bidir=True)
+    w = synth.model_weights(cfg)
+    si = synth.step_inputs(cfg, [40, 70])
+    s = _session(cfg, w)
+    o = OracleVLA(cfg, w)
+    fp, ft, ids, ex = si["frame_prev"], si["frame_t"], si["text_ids"], si["extra_rows"]
+    exd = None if ex is None else ex.to(DEV)
+    exn = None if ex is None else ex.numpy()
+    s.step_prefill(fp.to(DEV), ids.to(DEV), exd)
+    o.step_prefill(fp.numpy(), ids.numpy(), exn)
+    H, K, V, z = _state(s, cfg)
+    for l in range(cfg.n_layers + 1):
+        assert rel_err(H[l], o.H[l]) <= TOL, ("full", l)
+    assert rel_err(z, o.head_logits) <= TOL
+    s.decode_actions()
+    o.decode_actions()
+    s.margin_gate(force=[0, 0])
+    o.margin_gate(force=[0, 0])
+    mask, n_static = s.select_static(ft.to(DEV), fp.to(DEV))
+    mo, no = o.select_static(ft.numpy(), fp.numpy())
+    assert np.array_equal(mask.cpu().numpy().astype(bool), mo) and n_static.cpu().tolist() == no.tolist()
+    s.step_prefill(ft.to(DEV), ids.to(DEV), exd, mask)
+    o.step_prefill(ft.numpy(), ids.numpy(), exn, mo)
+    assert s.read(gvc.STATE_ROWS).cpu().tolist() == [int(x) for x in o.recomputed.sum(axis=0)]
+    H, K, V, z = _state(s, cfg)
+    P = cfg.prompt_len
+    errs = {"H%d" % l: rel_err(H[l], o.H[l]) for l in range(cfg.n_layers + 1)}
+    for l in range(cfg.n_layers):
+        errs["K%d" % l] = rel_err(K[l][:, :, :P], o.K[l].transpose(0, 2, 1, 3)[:, :, :P])
+    errs["logits"] = rel_err(z, o.head_logits)
+    print(name, {k: "%.2e" % v for k, v in errs.items()})
+    assert all(v <= TOL for v in errs.values()), errs
+    s.close()
