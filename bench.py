@@ -187,9 +187,9 @@ def c4_chunk(dev, steps, warmup):
             "steps": steps}
 
 
-def c5_prefill(dev, reps, ks=(0, 128, 230)):
+def c5_prefill(dev, reps, ks=(0, 64, 128, 192, 230)):
     """C5, 16 episodes batched: the prompt pass after a full step, for k of
-    256 patches static in every episode.  With 16 x 148 = 2368 recomputed
+    256 patches static in every episode (0, 25, 50, 75 and 90%).  With 16 x 148 = 2368 recomputed
     rows the projections are MFMA-bound, so this is where the prompt pass's
     MFMA utilisation is measured.  Reports per k the time of the partial
     prompt pass, its algorithmic TFLOP/s and the fraction of the dense bf16
