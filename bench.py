@@ -232,8 +232,20 @@ def c5_prefill(dev, reps, ks=(0, 64, 128, 192, 230)):
                 qpos = [p for p in range(P) if not (1 <= p <= cfg.n_patches and m[b, l, p - 1])]
                 flops += 2 * len(qpos) * (4 * d * d + 3 * d * F) + 2 * sum(2 * (p + 1) * d for p in qpos)
         tf = flops / (ms / 1e3) / 1e12
-        out.append({"static_per_episode": k, "rows_per_layer": B * (P - k), "prefill_ms": ms, "tflops": tf,
-                    "mfma_util_pct": 100.0 * tf / BF16_PEAK_TFLOPS})
+        rec = {"static_per_episode": k, "rows_per_layer": B * (P - k), "prefill_ms": ms, "tflops": tf,
+               "mfma_util_pct": 100.0 * tf / BF16_PEAK_TFLOPS}
+        if k == 128:   # the 16-episode action decode after the 50% reuse pass
+            evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+            for ea, eb in evs:
+                s.step_prefill(ft, ids, None, mask)
+                ea.record()
+                s.decode_actions()
+                eb.record()
+            torch.cuda.synchronize()
+            dms = sum(ea.elapsed_time(eb) for ea, eb in evs) / reps
+            dbytes = (cfg.n_decode - 1) * (L * layer_weight_bytes(cfg) + V * d * 2)
+            rec.update(decode_ms=dms, decode_gbs=dbytes / (dms / 1e3) / 1e9)
+        out.append(rec)
         note("C5 k=%d: %.2f ms, %.0f TFLOP/s" % (k, ms, tf))
     s.close()
     return out
