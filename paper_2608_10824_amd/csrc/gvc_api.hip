@@ -30,6 +30,12 @@ int32_t fail(int32_t code, const std::string& msg) {
 constexpr size_t kAlign = 256;
 constexpr int kMaxNT = 5;   // token blocks per GEMM workgroup (best of 2..16 on the 7B prompt pass)
 constexpr int kBigRows = 1024;  // sessions with at least this many prompt rows use k_gemm_big
+// Split-k prompt-pass GEMM (k_gemm_sk) of the other sessions: kernel variant
+// and k slices, fixed per matrix shape.  Measured inside the 7B prompt pass
+// at 148 rows (median per launch): gate/up 58 µs + 11 for the slice sum,
+// against 85 for the per-pair kernel; QKV 44 + 11 against 50 and down 34 + 12
+// against 46, so only the gate/up projection takes it.
+constexpr int kSkGuSlices = 2;
 
 struct Bump {
   size_t off = 0;
@@ -70,7 +76,7 @@ struct Plan {
   size_t layer_kv_elems;
   // workspace
   size_t rows_off, counts_off, epc_off, epo_off, stats_off, x_off, q_off, o_off, r_off, act_off, xdec_off, xf_off,
-      ssq_a_off, ssq_f_off, qraw_off, kraw_off,
+      ssq_a_off, ssq_f_off, qraw_off, kraw_off, part_off, part_bytes,
       logits_off, rope_off, decrows_off, headrows_off, tokens_off, gate_m_off, gate_f_off, qkv3_off, bar_off,
       ws_bytes;
 };
@@ -236,6 +242,12 @@ int32_t make_plan(const gvc_desc* dsc, Plan& p) {
   p.gate_f_off = k.take((size_t)p.B * 4);
   p.qkv3_off = k.take((size_t)3 * p.B * d.d_model * 4);
   p.bar_off = k.take((size_t)kDecodeBarWords * 4);
+  {   // split-k partial sums of the gate/up projection: slices x rows x features
+    const int kps = (p.KBd + kSkGuSlices - 1) / kSkGuSlices;
+    const size_t slices = (p.KBd + kps - 1) / kps;
+    p.part_bytes = (size_t)p.Mp * slices * 2 * (size_t)((d.ffn + 15) / 16 * 16) * 4;
+    p.part_off = k.take(p.part_bytes);
+  }
   if (p.vit) {
     const size_t kvv = (size_t)p.E * p.Hv * p.kvpad_v * p.dhv * 2;
     p.vrows_off = k.take((size_t)4 * p.Mv * 4);
@@ -271,6 +283,9 @@ struct gvc_ctx {
   // result never depends on how many rows a pass recomputes; GVC_GEMM=big
   // or small overrides (testing)
   bool big_gemm = false;
+  // the other sessions' gate/up projection on the split-k kernel (GVC_SK=0
+  // turns it off: testing)
+  bool sk_gemm = true;
   // persistent decode pass (k_decode.hip): eligible shape, its grid and LDS
   bool persist = false;
   int persist_wg = 0;
@@ -359,6 +374,28 @@ GemmArgs base_args(const gvc_ctx* c) {
   return a;
 }
 
+
+// Split-k launch of a prompt-pass projection (k_gemm_sk + slice sum and
+// epilogue); the slices depend only on the matrix shape.
+int32_t run_gemm_sk(gvc_ctx* c, GemmArgs& a, int epi, int M, int cls, int slices) {
+  if (M <= 0) return GVC_OK;
+  const Plan& p = c->p;
+  a.M = M;
+  a.mblocks = (M + 15) / 16;
+  const int kps = (a.KB + slices - 1) / slices;
+  a.sk_steps = kps;
+  a.sk_slices = (a.KB + kps - 1) / kps;
+  const int nblk = a.wblk[0] * (a.map == MAP_QKV ? 3 : (a.map == MAP_GU ? 2 : 1));
+  const int gb = gemm_sk_group_blocks();
+  a.sk_groups = (nblk + gb - 1) / gb;
+  a.part = c->K<float>(p.part_off);
+  a.part_ld = nblk * 16;
+  a.part_rows = a.mblocks * 16;
+  if ((size_t)a.sk_slices * a.part_rows * a.part_ld * 4 > p.part_bytes) return fail(GVC_EINVAL, "split-k buffer");
+  ProfScope ps(c, cls);
+  HIP_TRY(launch_gemm_sk(a, epi, c->stream));
+  return GVC_OK;
+}
 
 int32_t run_gemm(gvc_ctx* c, GemmArgs& a, int epi, int M, int cls, bool big = false) {
   if (M <= 0) return GVC_OK;
@@ -553,7 +590,8 @@ int32_t run_layer(gvc_ctx* c, int l, const RowMap& rows, int M, float* src, floa
     a.map = MAP_GU; a.n_pairs = p.wg[l].Nblk; a.n_out = p.F; a.KB = p.KBd;
     a.x = reinterpret_cast<const bf16x8*>(X);
     a.e.rows = rows; a.e.act = A; a.e.kb_act = p.KBf; a.e.n_feat = p.F;
-    int32_t r = run_gemm(c, a, EPI_SILU, M, k0 + 3, c->big_gemm);
+    int32_t r = c->sk_gemm && !c->big_gemm ? run_gemm_sk(c, a, EPI_SILU, M, k0 + 3, kSkGuSlices)
+                                           : run_gemm(c, a, EPI_SILU, M, k0 + 3, c->big_gemm);
     if (r) return r;
   }
   {
@@ -804,6 +842,7 @@ int32_t gvc_init_cache(const gvc_desc* desc, const gvc_weights* wt, void* weight
   INIT_TRY(hipGetDevice(&c->device));
   if (const char* fs = getenv("GVC_FORCE_SPLITS")) c->force_splits = atoi(fs);
   c->big_gemm = p.B * p.P >= kBigRows;
+  if (const char* sk = getenv("GVC_SK")) c->sk_gemm = atoi(sk) != 0;
   if (const char* g = getenv("GVC_GEMM")) {
     if (!strcmp(g, "big")) c->big_gemm = true;
     if (!strcmp(g, "small")) c->big_gemm = false;

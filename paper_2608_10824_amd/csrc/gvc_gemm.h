@@ -65,6 +65,12 @@ struct GemmArgs {
   int tgroups;                // token groups per workgroup (KT)
   const bf16x8* x;      // frag-layout activations
   int M, mblocks, mtiles;
+  // split-k variant (k_gemm_sk + k_gemm_sk_epi): the k range in sk_slices
+  // slices of sk_steps k steps, fp32 partial sums part[slice][row][feature]
+  // with part_ld features per row (all matrices' blocks, matrix-major) and
+  // part_rows rows per slice; sk_groups weight-block groups per slice
+  float* part;
+  int sk_slices, sk_steps, sk_groups, part_ld, part_rows;
   EpiArgs e;
 };
 

@@ -526,6 +526,177 @@ hipError_t launch_gemm_big(const GemmArgs& a, int epi, hipStream_t s) {
   }
 }
 
+// Split-k variant for a large prompt-pass projection at a few hundred rows
+// (the 7B gate/up projection at batch 1).  The per-pair
+// kernel reads each token fragment once per weight pair, so its L2 -> CU
+// traffic is several times the weight bytes; here a workgroup of 8 waves
+// owns 8 * NBW consecutive weight blocks (of all the launch's matrices, in
+// order) for one k slice and one tile of T token blocks, and the tile's
+// token fragments pass through LDS once for all 8 waves.  Per chunk of KC k
+// steps the waves copy the token fragments straight into LDS
+// (global_load_lds) D chunks ahead, D + 2 stages deep (the stage written at
+// chunk c last held chunk c - 2, which every wave finished before the
+// barrier of chunk c - 1), and each wave loads its NBW weight fragments into
+// registers D chunks ahead.  Partial sums go to part[slice][row][feature];
+// k_gemm_sk_epi then adds the slices in order and runs the fused epilogue.
+// The slices depend only on the matrix shape, so a row's result never
+// depends on how many rows a pass recomputes.
+template <int T, int NBW, int KC, int D>
+__global__ __launch_bounds__(8 * 64) void k_gemm_sk(const GemmArgs a) {
+  constexpr int NW = 8;
+  constexpr int NF = KC * T;                       // token fragments per chunk
+  constexpr int ITOK = (NF + NW - 1) / NW;         // copies per wave per chunk (duplicates pad the last)
+  constexpr int IW = KC * NBW;
+  constexpr int NST = D + 2;
+  static_assert(D * (ITOK + IW) < 64, "vmcnt range");
+  extern __shared__ u32x4b sk_lds[];               // [NST][KC][T][64]
+  const int lane = threadIdx.x & 63, wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  int id = blockIdx.x;
+  const int g = id % a.sk_groups;
+  id /= a.sk_groups;
+  const int s = id % a.sk_slices, mt = id / a.sk_slices;
+  const int kb0 = s * a.sk_steps, nk = min(a.KB, kb0 + a.sk_steps) - kb0;
+  if (nk <= 0) return;
+  const int mb0 = mt * T, nT = min(T, a.mblocks - mb0);
+  const int nblk = a.wblk[0] * (a.map == MAP_QKV ? 3 : (a.map == MAP_GU ? 2 : 1));
+  const bf16x8* wp[NBW];
+  int vbs[NBW];
+#pragma unroll
+  for (int j = 0; j < NBW; ++j) {
+    const int vb = (g * NW + wv) * NBW + j;
+    vbs[j] = vb;
+    const int vc = min(vb, nblk - 1), mat = vc / a.wblk[0], blk = vc % a.wblk[0];
+    wp[j] = a.w[mat] + ((size_t)blk * a.KB + kb0) * 64 + lane;
+  }
+  const int nchunks = (nk + KC - 1) / KC;
+  auto issue_tok = [&](int c) {   // chunks past the end re-read the last k step (in bounds)
+    u32x4b* buf = sk_lds + (c % NST) * NF * 64;
+#pragma unroll
+    for (int i = 0; i < ITOK; ++i) {
+      const int f = min(wv + i * NW, NF - 1), kk = f / T, t = f % T;
+      const int kb = kb0 + min(c * KC + kk, nk - 1);
+      const int tb = mb0 + min(t, nT - 1);
+      __builtin_amdgcn_global_load_lds(GPB(a.x + ((size_t)tb * a.KB + kb) * 64 + lane), LPB(buf + f * 64), 16, 0, 0);
+    }
+  };
+  bf16x8 wb[D + 1][KC][NBW];
+  auto issue_w = [&](int c, bf16x8 (&W)[KC][NBW]) {
+#pragma unroll
+    for (int kk = 0; kk < KC; ++kk) {
+      const size_t k = (size_t)min(c * KC + kk, nk - 1) * 64;
+#pragma unroll
+      for (int j = 0; j < NBW; ++j) W[kk][j] = wp[j][k];
+    }
+  };
+  floatx4 acc[NBW][T];
+#pragma unroll
+  for (int j = 0; j < NBW; ++j)
+#pragma unroll
+    for (int t = 0; t < T; ++t) acc[j][t] = floatx4{0, 0, 0, 0};
+#pragma unroll
+  for (int u = 0; u < D; ++u) {
+    issue_tok(u);
+    issue_w(u, wb[u]);
+  }
+  for (int c0 = 0; c0 < nchunks; c0 += D + 1) {
+#pragma unroll
+    for (int u = 0; u <= D; ++u) {
+      const int c = c0 + u;
+      if (c < nchunks) {
+        issue_tok(c + D);
+        issue_w(c + D, wb[(u + D) % (D + 1)]);
+        big_wait_vm<D * (ITOK + IW)>();
+        __syncthreads();
+        const u32x4b* buf = sk_lds + (c % NST) * NF * 64;
+#pragma unroll
+        for (int kk = 0; kk < KC; ++kk) {
+          if (c * KC + kk < nk) {
+#pragma unroll
+            for (int t = 0; t < T; ++t) {
+              const bf16x8 xf = __builtin_bit_cast(bf16x8, buf[(kk * T + t) * 64 + lane]);
+#pragma unroll
+              for (int j = 0; j < NBW; ++j) acc[j][t] = mfma16(wb[u][kk][j], xf, acc[j][t]);
+            }
+          }
+        }
+      }
+    }
+  }
+  big_wait_vm<0>();
+  const int col = lane & 15, sub = (lane >> 4) * 4;
+#pragma unroll
+  for (int j = 0; j < NBW; ++j) {
+    if (vbs[j] >= nblk) continue;
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+      if (t >= nT) continue;
+      const int m = (mb0 + t) * 16 + col;
+      *(floatx4*)(a.part + ((size_t)s * a.part_rows + m) * a.part_ld + vbs[j] * 16 + sub) = acc[j][t];
+    }
+  }
+}
+
+// Sums the k slices of k_gemm_sk in order and runs the epilogue: one wave
+// per (work pair, block of 16 rows), in the lane layout of the MFMA result.
+template <int EPI>
+__global__ __launch_bounds__(256) void k_gemm_sk_epi(const GemmArgs a) {
+  const int lane = threadIdx.x & 63;
+  const int w = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (w >= a.n_pairs * a.mblocks) return;
+  const int pair = w / a.mblocks, mb = w % a.mblocks;
+  int ma, ba, mb2, bb; bool b_ok;
+  map_pair(a, pair, ma, ba, mb2, bb, b_ok);
+  const int m = mb * 16 + (lane & 15), sub = (lane >> 4) * 4;
+  const int fa = (ma * a.wblk[0] + ba) * 16 + sub, fb = (mb2 * a.wblk[0] + bb) * 16 + sub;
+  floatx4 va = {0, 0, 0, 0}, vb = {0, 0, 0, 0};
+  for (int s = 0; s < a.sk_slices; ++s) {
+    const float* row = a.part + ((size_t)s * a.part_rows + m) * a.part_ld;
+    va += *(const floatx4*)(row + fa);
+    if (b_ok) vb += *(const floatx4*)(row + fb);
+  }
+  epilogue<EPI>(a, pair, lane, min(m, a.M - 1), va, vb, b_ok, m < a.M, 1.0f);
+}
+
+template <int T, int NBW, int KC, int D>
+static hipError_t launch_sk_core(const GemmArgs& a, hipStream_t s) {
+  constexpr int lds = (D + 2) * KC * T * 1024;
+  static bool attr = false;
+  if (!attr) {
+    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_gemm_sk<T, NBW, KC, D>),
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+    if (e != hipSuccess) return e;
+    attr = true;
+  }
+  const int mtiles = (a.mblocks + T - 1) / T;
+  hipLaunchKernelGGL((k_gemm_sk<T, NBW, KC, D>), dim3(a.sk_groups * a.sk_slices * mtiles), dim3(8 * 64), lds, s, a);
+  return hipGetLastError();
+}
+
+template <int EPI>
+static hipError_t launch_sk_epi(const GemmArgs& a, hipStream_t s) {
+  const int waves = a.n_pairs * a.mblocks;
+  hipLaunchKernelGGL(k_gemm_sk_epi<EPI>, dim3((waves + 3) / 4), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+// Tiles of 10 token blocks, 2 weight blocks per wave (16 per workgroup),
+// chunks of 4 k steps, one chunk ahead.
+constexpr int kSkT = 10, kSkNBW = 2, kSkKC = 4, kSkD = 1;
+
+int gemm_sk_group_blocks() { return 8 * kSkNBW; }
+
+hipError_t launch_gemm_sk(const GemmArgs& a, int epi, hipStream_t s) {
+  if (a.map == MAP_SINGLE || a.map == MAP_QKV_SINGLE || a.e.ssq_in || !a.part) return hipErrorInvalidValue;
+  const hipError_t e = launch_sk_core<kSkT, kSkNBW, kSkKC, kSkD>(a, s);
+  if (e != hipSuccess) return e;
+  switch (epi) {
+    case EPI_QKV: return launch_sk_epi<EPI_QKV>(a, s);
+    case EPI_RESID: return launch_sk_epi<EPI_RESID>(a, s);
+    case EPI_SILU: return launch_sk_epi<EPI_SILU>(a, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
 template <int EPI, int KT, int NT, bool ONE>
 static hipError_t launch_one(const GemmArgs& a, hipStream_t s) {
   constexpr int PF = gemm_pf(NT);
