@@ -243,7 +243,10 @@ def c5_prefill(dev, reps, ks=(0, 64, 128, 192, 230)):
                 eb.record()
             torch.cuda.synchronize()
             dms = sum(ea.elapsed_time(eb) for ea, eb in evs) / reps
-            dbytes = (cfg.n_decode - 1) * (L * layer_weight_bytes(cfg) + V * d * 2)
+            # weights and LM head once per pass, plus every episode's K and V rows
+            # 0..pos of every layer (pass j attends over P + j keys)
+            dbytes = (cfg.n_decode - 1) * (L * layer_weight_bytes(cfg) + V * d * 2) + sum(
+                L * B * 2 * (P + j) * d * 2 for j in range(1, cfg.n_decode))
             rec.update(decode_ms=dms, decode_gbs=dbytes / (dms / 1e3) / 1e9)
         out.append(rec)
         note("C5 k=%d: %.2f ms, %.0f TFLOP/s" % (k, ms, tf))

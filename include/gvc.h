@@ -82,7 +82,7 @@ enum gvc_state_item {
  * RMSNorm, rotary embedding pairing dim i with i + head_dim/2, multi-head
  * attention, SwiGLU; no biases. */
 typedef struct gvc_desc {
-  int32_t batch;          /* B independent episodes stepped together */
+  int32_t batch;          /* B independent episodes stepped together, 1 <= B <= 16 */
   int32_t n_layers;       /* L */
   int32_t d_model;        /* d, a multiple of 64 */
   int32_t n_heads;        /* head_dim = d / n_heads must be 64 or 128 */

@@ -106,7 +106,8 @@ int32_t make_plan(const gvc_desc* dsc, Plan& p) {
   if (!dsc) return fail(GVC_EINVAL, "null desc");
   const gvc_desc& d = *dsc;
   p.d = d;
-  if (d.batch < 1 || d.batch > 64) return fail(GVC_EINVAL, "batch must be in [1, 64]");
+  // the batched decode folds each RMSNorm into GEMMs over one 16-row token block
+  if (d.batch < 1 || d.batch > 16) return fail(GVC_EINVAL, "batch must be in [1, 16]");
   if (d.n_layers < 1 || d.n_layers > 128) return fail(GVC_EINVAL, "n_layers must be in [1, 128]");
   if (d.d_model < 64 || d.d_model % 64) return fail(GVC_EINVAL, "d_model must be a positive multiple of 64");
   if (d.n_heads < 1 || d.d_model % d.n_heads) return fail(GVC_EINVAL, "n_heads must divide d_model");

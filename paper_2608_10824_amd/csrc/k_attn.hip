@@ -520,8 +520,19 @@ hipError_t launch_text_vis(const bf16* q, const bf16* kc, const int* ep_counts, 
 hipError_t launch_attn_decode(const float* qraw, const float* kraw, bf16* kc, const bf16* vc, const float2* rope,
                               int B, int H, int head_dim, int kv_pad, int pos, bf16* o, int KB, hipStream_t s) {
   const size_t shm = (size_t)kv_pad * sizeof(float);
-  if (head_dim == 128)
+  // Value slices per (head, episode): 4 when there are few (head, episode)
+  // pairs, so the grid still covers the chip; 1 once there are 256 or more,
+  // so the keys are read once (each slice recomputes every score).  The
+  // arithmetic of every output is the same either way.
+  const bool one = B * H >= 256;
+  if (head_dim == 128 && one)
+    hipLaunchKernelGGL((k_attn_decode<128, 1>), dim3(H, B, 1), dim3(512), shm, s, qraw, kraw, kc, vc, rope, H, kv_pad,
+                       pos, o, KB);
+  else if (head_dim == 128)
     hipLaunchKernelGGL((k_attn_decode<128, 4>), dim3(H, B, 4), dim3(512), shm, s, qraw, kraw, kc, vc, rope, H, kv_pad,
+                       pos, o, KB);
+  else if (head_dim == 64 && one)
+    hipLaunchKernelGGL((k_attn_decode<64, 1>), dim3(H, B, 1), dim3(512), shm, s, qraw, kraw, kc, vc, rope, H, kv_pad,
                        pos, o, KB);
   else if (head_dim == 64)
     hipLaunchKernelGGL((k_attn_decode<64, 4>), dim3(H, B, 4), dim3(512), shm, s, qraw, kraw, kc, vc, rope, H, kv_pad,

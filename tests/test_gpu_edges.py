@@ -282,3 +282,35 @@ def test_batched_front_end_and_action_block(name):
     print(name, {k: "%.2e" % v for k, v in errs.items()})
     assert all(v <= TOL for v in errs.values()), errs
     s.close()
+
+
+def test_sixteen_episodes_prompt_and_decode():
+    """16 episodes of the mid-size decoder (16 heads of 128, two views):
+    2176 prompt rows (the many-row projection kernel) and a batched decode
+    whose attention takes one value slice per (head, episode) (16 x 16 = 256
+    pairs).  Episodes are independent, so episodes 0 and 15 are checked
+    against a one-episode oracle each: the prompt state, and the decode
+    logits with the oracle fed the GPU's own tokens."""
+    from paper_2608_10824_amd import gvc
+    cfg = synth.config_mid().with_(batch=16)
+    w = synth.model_weights(cfg)
+    si = synth.step_inputs(cfg, 90)
+    s = _session(cfg, w)
+    fp, ids = si["frame_prev"], si["text_ids"]
+    s.step_prefill(fp.to(DEV), ids.to(DEV))
+    H, K, V, z = _state(s, cfg)
+    tok, mg, lg = s.decode_actions(logits=True)
+    torch.cuda.synchronize()
+    tok, lgn = tok.cpu().numpy(), lg.cpu().numpy()
+    one = cfg.with_(batch=1)
+    for b in (0, cfg.batch - 1):
+        o = OracleVLA(one, w)
+        o.step_prefill(fp.numpy()[b:b + 1], ids.numpy()[b:b + 1])
+        for l in range(cfg.n_layers + 1):
+            assert rel_err(H[l][b:b + 1], o.H[l]) <= TOL, (b, l)
+        _, _, lg_o = o.decode_actions(forced_tokens=tok[b:b + 1])
+        err = rel_err(lgn[b:b + 1], lg_o)
+        print("episode %d decode logits rel err %.2e" % (b, err))
+        assert err <= TOL
+        check_tokens(tok[b:b + 1], lgn[b:b + 1], tok[b:b + 1], lg_o, cfg.bin_lo)
+    s.close()
