@@ -39,8 +39,10 @@ def test_sizes_for_every_config():
     assert params * 2 <= w <= params * 2 * 1.01
 
 
-@pytest.mark.parametrize("field,value", [("n_heads", 48), ("d_model", 100), ("batch", 0), ("batch", 65),
-                                         ("ffn", 30), ("img", 100), ("n_text", 0)])
+@pytest.mark.parametrize("field,value", [("n_heads", 48), ("d_model", 100), ("batch", 0), ("batch", 17),
+                                         ("ffn", 30), ("img", 100), ("n_text", 0), ("task_topk", -1),
+                                         ("task_topk", 65), ("entropy_reuse", 2), ("action_bidir", 1),
+                                         ("vit_layers", 65), ("vit_layers", -1)])
 def test_bad_shapes_rejected(field, value):
     from paper_2608_10824_amd import gvc
     from paper_2608_10824_amd.session import desc_from
@@ -50,6 +52,33 @@ def test_bad_shapes_rejected(field, value):
         gvc.sizes(d)
     assert e.value.code == gvc.GVC_EINVAL
     assert gvc.last_error()
+
+
+@pytest.mark.parametrize("field,value", [("vit_dim", 96), ("vit_heads", 3), ("vit_heads", 16), ("vit_ffn", 40),
+                                         ("vit_eps", 0.0)])
+def test_bad_front_end_rejected(field, value):
+    """With the ViT front end on, its shape limits are checked (width a
+    multiple of 64, heads of 64 or 128, MLP width a multiple of 32, eps > 0)."""
+    from paper_2608_10824_amd import gvc
+    from paper_2608_10824_amd.session import desc_from
+    d = desc_from(synth.config_c1v())
+    gvc.sizes(d)
+    setattr(d, field, value)
+    with pytest.raises(gvc.GvcError) as e:
+        gvc.sizes(d)
+    assert e.value.code == gvc.GVC_EINVAL
+
+
+def test_stage_limits_and_action_block_need_their_shapes():
+    """Stages 2/3 need at most 32 instruction tokens after the image; the
+    action block needs parallel decode; both accepted on their configs."""
+    from paper_2608_10824_amd import gvc
+    from paper_2608_10824_amd.session import desc_from
+    gvc.sizes(desc_from(synth.config_c1().with_(task_topk=10, entropy_reuse=True)))
+    gvc.sizes(desc_from(synth.config_c4_tiny().with_(action_bidir=True)))
+    for cfg in (synth.config_c1().with_(n_text=40, task_topk=10), synth.config_c1().with_(n_text=40, entropy_reuse=True)):
+        with pytest.raises(gvc.GvcError):
+            gvc.sizes(desc_from(cfg))
 
 
 def test_null_context_calls_fail_cleanly():
