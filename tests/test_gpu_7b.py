@@ -66,6 +66,22 @@ def _sample_rows(cfg, rows_recomputed):
     return sorted(set(pick))
 
 
+def _oracle_decode_chain(cfg, w, h_last, Ks, Vs, fed):
+    """Logits [D][V] of the prompt's last row and of the D - 1 single-token
+    passes fed with `fed`, in float64 over one episode's prompt K/V."""
+    g = glob_w64(w)
+    P, D, L = cfg.prompt_len, cfg.n_decode, cfg.n_layers
+    z0 = head_row(h_last, g["final_norm"], g["lm_head"], cfg.rms_eps)
+    x = g["embed"][fed].copy()
+    pos = [P + j for j in range(D - 1)]
+    for l in range(L):
+        K = np.zeros((cfg.kv_len, cfg.n_heads, cfg.head_dim))
+        V = np.zeros_like(K)
+        K[:P], V[:P] = Ks[l], Vs[l]
+        x = layer_rows(layer_w64(w, l), x, list(range(D - 1)), pos, K, V, cfg.n_heads, cfg.rms_eps, cfg.rope_theta)
+    return np.stack([z0] + [head_row(x[j], g["final_norm"], g["lm_head"], cfg.rms_eps) for j in range(D - 1)])
+
+
 @pytest.fixture(scope="module")
 def c2():
     from paper_2608_10824_amd import gvc
@@ -335,12 +351,24 @@ def test_c5_sweep_masks_counts_and_layers(c5, k_static):
         for b in range(cfg.batch):
             zo = head_row(state64(s, gvc.STATE_H, L, b, P)[P - 1], g["final_norm"], g["lm_head"], cfg.rms_eps)
             assert rel_err(head[b, 0], zo) <= TOL
+    if k_static == 128:   # the batched decode of the last episode, as a float64 chain over its prompt K/V
+        b = cfg.batch - 1
+        P, L = cfg.prompt_len, cfg.n_layers
+        Ks = [state64(s, gvc.STATE_K, l, b, P) for l in range(L)]
+        Vs = [state64(s, gvc.STATE_V, l, b, P) for l in range(L)]
+        hL = state64(s, gvc.STATE_H, L, b, P)[P - 1]
     tok, mg, lg = s.decode_actions(logits=True)
     torch.cuda.synchronize()
     lgn = lg.cpu().numpy()
     for b in range(cfg.batch):
         for j in range(cfg.n_decode):
             assert tok[b, j].item() == cfg.bin_lo + int(np.argmax(lgn[b, j, cfg.bin_lo:]))
+    if k_static == 128:
+        b = cfg.batch - 1
+        zo = _oracle_decode_chain(cfg, w, hL, Ks, Vs, tok[b].cpu().numpy()[: cfg.n_decode - 1])
+        err = rel_err(lgn[b], zo)
+        print("episode %d batched decode chain logits rel err %.2e" % (b, err))
+        assert err <= TOL
 
 
 # ---------------------------------------------------------------- C3
