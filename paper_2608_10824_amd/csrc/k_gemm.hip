@@ -415,6 +415,20 @@ typedef unsigned u32x4b __attribute__((ext_vector_type(4)));
 #define GPB(p) ((const void __attribute__((address_space(1)))*)(p))
 #define LPB(p) ((void __attribute__((address_space(3)))*)(p))
 
+// Workgroup barrier for pipelines fed by direct-to-LDS loads.
+// __syncthreads() also fences memory, and that fence makes every wave wait
+// for all of its outstanding global loads (vmcnt 0), prefetches of later
+// steps included, before the barrier.  Here the caller first waits (with
+// s_waitcnt) for exactly the loads the next step reads; the empty asm
+// statements keep the compiler from moving memory accesses across the
+// barrier.  Only for LDS data written by those loads or read before the
+// previous barrier.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
 template <int N>
 __device__ __forceinline__ void big_wait_vm() {
   static_assert(N >= 0 && N < 64, "vmcnt range");
@@ -467,7 +481,7 @@ __global__ __launch_bounds__(kBigWP * kBigWT * 64) void k_gemm_big(const GemmArg
     // before the barrier of step k - 1
     issue(k + 1);
     big_wait_vm<LPW>();
-    __syncthreads();
+    lds_barrier();
     const u32x4b* st = big_lds + (k % kBigStages) * kBigFrags * 64;
     bf16x8 wf[2 * kBigPW], xf[kBigTW];
 #pragma unroll
@@ -606,7 +620,7 @@ __global__ __launch_bounds__(8 * 64) void k_gemm_sk(const GemmArgs a) {
         issue_tok(c + D);
         issue_w(c + D, wb[(u + D) % (D + 1)]);
         big_wait_vm<D * (ITOK + IW)>();
-        __syncthreads();
+        lds_barrier();
         const u32x4b* buf = sk_lds + (c % NST) * NF * 64;
 #pragma unroll
         for (int kk = 0; kk < KC; ++kk) {
