@@ -403,7 +403,6 @@ int32_t run_gemm(gvc_ctx* c, GemmArgs& a, int epi, int M, int cls, bool big = fa
   if (big) {
     a.M = M;
     a.mblocks = (M + 15) / 16;
-    a.mtiles = (a.mblocks + kGemmBigTok - 1) / kGemmBigTok;
     ProfScope ps(c, cls);
     HIP_TRY(launch_gemm_big(a, epi, c->stream));
     return GVC_OK;

@@ -74,9 +74,6 @@ struct GemmArgs {
   EpiArgs e;
 };
 
-// Token blocks of 16 rows per workgroup tile of the many-row kernel (k_gemm_big).
-constexpr int kGemmBigTok = 16;
-
 // k-steps per pipelined register chunk for a tile of NT blocks of 16 token rows.
 constexpr int gemm_pf(int NT) { return NT == 1 ? 8 : (NT <= 3 ? 4 : (NT <= 6 ? 2 : 1)); }
 

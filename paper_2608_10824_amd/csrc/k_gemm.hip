@@ -395,21 +395,24 @@ __global__ __launch_bounds__(KS * KT * 64) void k_gemm_ks(const GemmArgs a) {
 }
 
 // Many-row variant (batched episodes: thousands of rows, MFMA-bound).  A
-// workgroup of 8 waves owns kBigPairs weight pairs x kBigTok blocks of 16
+// workgroup of 8 waves owns kBigPairs weight pairs x 4 TW blocks of 16
 // token rows and walks the whole k range; every k step, both operands'
-// fragments for the tile (2 kBigPairs weight + kBigTok token fragments)
-// are copied straight into LDS (global_load_lds), three stages deep so one
-// step is in flight while another is read, with one workgroup barrier per
-// step.  Wave (wp, wt) multiplies pairs wp*2..wp*2+1 by token blocks
-// wt*4..wt*4+3 (16 MFMAs per k step from 8 LDS fragment reads) and runs the
-// same fused epilogue as k_gemm_ks.  Each row's sum runs over k in order, so
-// a row's result does not depend on the tile it falls in.
-constexpr int kBigWP = 2, kBigWT = 4, kBigPW = 2, kBigTW = 4;
-constexpr int kBigPairs = kBigWP * kBigPW, kBigTok = kBigWT * kBigTW;
-static_assert(kBigTok == kGemmBigTok, "token tile of the many-row kernel");
-constexpr int kBigFrags = 2 * kBigPairs + kBigTok;   // fragments per k step
+// fragments for the tile (2 kBigPairs weight + 4 TW token fragments) are
+// copied straight into LDS (global_load_lds), three stages deep so one step
+// is in flight while another is read, with one workgroup barrier per step.
+// Wave (wp, wt) multiplies pairs wp*2..wp*2+1 by token blocks
+// wt*TW..wt*TW+TW-1 (4 TW MFMAs per k step from 4 + TW LDS fragment reads)
+// and runs the same fused epilogue as k_gemm_ks.  Each row's sum runs over
+// k in order, so a row's result does not depend on the tile it falls in or
+// on the tile height (TW = 4: 256-row tiles, TW = 2: 128-row tiles; the
+// launcher picks one per launch).
+constexpr int kBigWP = 2, kBigWT = 4, kBigPW = 2;
+constexpr int kBigPairs = kBigWP * kBigPW;
 constexpr int kBigStages = 3;
-constexpr int kBigLds = kBigStages * kBigFrags * 1024;
+template <int TW>
+constexpr int big_frags() { return 2 * kBigPairs + kBigWT * TW; }   // fragments per k step
+template <int TW>
+constexpr int big_lds_bytes() { return kBigStages * big_frags<TW>() * 1024; }
 
 typedef unsigned u32x4b __attribute__((ext_vector_type(4)));
 #define GPB(p) ((const void __attribute__((address_space(1)))*)(p))
@@ -435,26 +438,31 @@ __device__ __forceinline__ void big_wait_vm() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x0F70);
 }
 
-template <int EPI>
+template <int EPI, int TW>
 __global__ __launch_bounds__(kBigWP * kBigWT * 64) void k_gemm_big(const GemmArgs a) {
   constexpr int NW = kBigWP * kBigWT;
   constexpr int WF = 2 * kBigPairs;
-  constexpr int LPW = (kBigFrags + NW - 1) / NW;   // fragment copies per wave per k step
-  extern __shared__ u32x4b big_lds[];              // [kBigStages][kBigFrags][64]
+  constexpr int FR = big_frags<TW>();
+  constexpr int LPW = (FR + NW - 1) / NW;          // fragment copies per wave per k step
+  extern __shared__ u32x4b big_lds[];              // [kBigStages][FR][64]
   const int lane = threadIdx.x & 63, wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wp = wv % kBigWP, wt = wv / kBigWP;
   // XCD-aware order: all tiles of one weight tile run on XCD (tile % 8) and
-  // share its weights in that L2
+  // share its weights in that L2; within an XCD, jobs run in groups of 8
+  // token tiles x all of the XCD's weight tiles, so the workgroups resident
+  // at one time share both operands' tiles
   const int x = blockIdx.x, xcd = x & 7, i = x >> 3;
-  const int nt = xcd + 8 * (i / a.mtiles), mt = i % a.mtiles;
   const int ntiles = (a.n_pairs + kBigPairs - 1) / kBigPairs;
+  const int nnt = (ntiles + 7) / 8, g = i / (8 * nnt), r = i % (8 * nnt);
+  const int gs = min(8, a.mtiles - g * 8);
+  const int nt = xcd + 8 * (r / gs), mt = g * 8 + r % gs;
   if (nt >= ntiles) return;
-  const int pair0 = nt * kBigPairs, tb0 = mt * kBigTok;
+  const int pair0 = nt * kBigPairs, tb0 = mt * kBigWT * TW;
   const bf16x8* src[LPW];
   int dst[LPW];
 #pragma unroll
   for (int l = 0; l < LPW; ++l) {
-    const int f = min(wv + l * NW, kBigFrags - 1);
+    const int f = min(wv + l * NW, FR - 1);
     dst[l] = f;
     if (f < WF) {
       int ma, ba, mb, bb; bool ok;
@@ -465,16 +473,16 @@ __global__ __launch_bounds__(kBigWP * kBigWT * 64) void k_gemm_big(const GemmArg
     }
   }
   auto issue = [&](int k) {   // k steps past the end re-read the last one (in bounds)
-    u32x4b* st = big_lds + (k % kBigStages) * kBigFrags * 64;
+    u32x4b* st = big_lds + (k % kBigStages) * FR * 64;
     const size_t o = (size_t)min(k, a.KB - 1) * 64;
 #pragma unroll
     for (int l = 0; l < LPW; ++l) __builtin_amdgcn_global_load_lds(GPB(src[l] + o), LPB(st + dst[l] * 64), 16, 0, 0);
   };
-  floatx4 acc[2 * kBigPW][kBigTW];
+  floatx4 acc[2 * kBigPW][TW];
 #pragma unroll
   for (int p = 0; p < 2 * kBigPW; ++p)
 #pragma unroll
-    for (int j = 0; j < kBigTW; ++j) acc[p][j] = floatx4{0, 0, 0, 0};
+    for (int j = 0; j < TW; ++j) acc[p][j] = floatx4{0, 0, 0, 0};
   issue(0);
   for (int k = 0; k < a.KB; ++k) {
     // stage (k + 1) % 3 last held step k - 2, which every wave finished
@@ -482,14 +490,14 @@ __global__ __launch_bounds__(kBigWP * kBigWT * 64) void k_gemm_big(const GemmArg
     issue(k + 1);
     big_wait_vm<LPW>();
     lds_barrier();
-    const u32x4b* st = big_lds + (k % kBigStages) * kBigFrags * 64;
-    bf16x8 wf[2 * kBigPW], xf[kBigTW];
+    const u32x4b* st = big_lds + (k % kBigStages) * FR * 64;
+    bf16x8 wf[2 * kBigPW], xf[TW];
 #pragma unroll
     for (int p = 0; p < 2 * kBigPW; ++p) wf[p] = __builtin_bit_cast(bf16x8, st[(2 * wp * kBigPW + p) * 64 + lane]);
 #pragma unroll
-    for (int j = 0; j < kBigTW; ++j) xf[j] = __builtin_bit_cast(bf16x8, st[(WF + wt * kBigTW + j) * 64 + lane]);
+    for (int j = 0; j < TW; ++j) xf[j] = __builtin_bit_cast(bf16x8, st[(WF + wt * TW + j) * 64 + lane]);
 #pragma unroll
-    for (int j = 0; j < kBigTW; ++j)
+    for (int j = 0; j < TW; ++j)
 #pragma unroll
       for (int p = 0; p < 2 * kBigPW; ++p) acc[p][j] = mfma16(wf[p], xf[j], acc[p][j]);
   }
@@ -502,30 +510,52 @@ __global__ __launch_bounds__(kBigWP * kBigWT * 64) void k_gemm_big(const GemmArg
     int ma, ba, mb, bb; bool b_ok;
     map_pair(a, pair, ma, ba, mb, bb, b_ok);
 #pragma unroll
-    for (int j = 0; j < kBigTW; ++j) {
-      const int m = (tb0 + wt * kBigTW + j) * 16 + col;
+    for (int j = 0; j < TW; ++j) {
+      const int m = (tb0 + wt * TW + j) * 16 + col;
       epilogue<EPI>(a, pair, lane, min(m, a.M - 1), acc[2 * p][j], acc[2 * p + 1][j], b_ok, m < a.M, 1.0f);
     }
   }
 }
 
-template <int EPI>
-static hipError_t launch_big_epi(const GemmArgs& a, hipStream_t s) {
+template <int EPI, int TW>
+static hipError_t launch_big_tw(GemmArgs a, hipStream_t s) {
   static bool attr = false;
   if (!attr) {
-    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_gemm_big<EPI>),
-                                             hipFuncAttributeMaxDynamicSharedMemorySize, kBigLds);
+    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_gemm_big<EPI, TW>),
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, big_lds_bytes<TW>());
     if (e != hipSuccess) return e;
     attr = true;
   }
+  a.mtiles = (a.mblocks + kBigWT * TW - 1) / (kBigWT * TW);
   const int ntiles = (a.n_pairs + kBigPairs - 1) / kBigPairs;
   const dim3 grid(8 * ((ntiles + 7) / 8) * a.mtiles);
-  hipLaunchKernelGGL(k_gemm_big<EPI>, grid, dim3(kBigWP * kBigWT * 64), kBigLds, s, a);
+  hipLaunchKernelGGL((k_gemm_big<EPI, TW>), grid, dim3(kBigWP * kBigWT * 64), big_lds_bytes<TW>(), s, a);
   return hipGetLastError();
 }
 
-// a.mtiles counts tiles of kBigTok token blocks here; pair maps only, no
-// folded norm.
+// Tile height: a launch takes about ceil(workgroups / resident) rounds of
+// one workgroup's k loop.  Two 256-row workgroups fit a CU (72 KiB of LDS
+// each), three 128-row ones (48 KiB); a round of 128-row tiles, half the
+// MFMAs of a 256-row round but shared three ways, measured 0.885 of one
+// on the 7B projections at 736-4416 rows.
+template <int EPI>
+static hipError_t launch_big_epi(const GemmArgs& a, hipStream_t s) {
+  static int cus = 0;
+  if (!cus) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return e;
+  }
+  const long long ntiles = (a.n_pairs + kBigPairs - 1) / kBigPairs;
+  const long long j4 = ntiles * ((a.mblocks + 4 * kBigWT - 1) / (4 * kBigWT));
+  const long long j2 = ntiles * ((a.mblocks + 2 * kBigWT - 1) / (2 * kBigWT));
+  const long long r4 = (j4 + 2LL * cus - 1) / (2LL * cus), r2 = (j2 + 3LL * cus - 1) / (3LL * cus);
+  if (885 * r2 < 1000 * r4) return launch_big_tw<EPI, 2>(a, s);
+  return launch_big_tw<EPI, 4>(a, s);
+}
+
+// Tiles are chosen here from a.mblocks; pair maps only, no folded norm.
 hipError_t launch_gemm_big(const GemmArgs& a, int epi, hipStream_t s) {
   if (a.map == MAP_SINGLE || a.map == MAP_QKV_SINGLE || a.e.ssq_in) return hipErrorInvalidValue;
   switch (epi) {
