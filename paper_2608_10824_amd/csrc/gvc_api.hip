@@ -546,7 +546,8 @@ int32_t run_layer(gvc_ctx* c, int l, const RowMap& rows, int M, float* src, floa
   const int k0 = GVC_K_PREFILL_QKV;   // class of this layer's QKV launch; the others follow in order
   {
     ProfScope ps(c, GVC_K_NORM);
-    HIP_TRY(launch_rmsnorm(src, mapped ? rows.idx : nullptr, M, p.d.d_model, gains, p.d.rms_eps, X, p.KBd, c->stream));
+    HIP_TRY(launch_rmsnorm(src, mapped ? rows.idx : nullptr, M, p.d.d_model, gains, p.d.rms_eps, X, p.KBd,
+                           c->big_gemm, c->stream));
   }
   {
     GemmArgs a = base_args(c);
@@ -581,7 +582,8 @@ int32_t run_layer(gvc_ctx* c, int l, const RowMap& rows, int M, float* src, floa
   }
   {
     ProfScope ps(c, GVC_K_NORM);
-    HIP_TRY(launch_rmsnorm(R, nullptr, M, p.d.d_model, gains + p.d.d_model, p.d.rms_eps, X, p.KBd, c->stream));
+    HIP_TRY(launch_rmsnorm(R, nullptr, M, p.d.d_model, gains + p.d.d_model, p.d.rms_eps, X, p.KBd, c->big_gemm,
+                           c->stream));
   }
   {
     GemmArgs a = base_args(c);
@@ -686,7 +688,7 @@ int32_t run_head(gvc_ctx* c, const RowMap& rows, const float* src, int M, float*
   {
     ProfScope ps(c, GVC_K_NORM);
     HIP_TRY(launch_rmsnorm(src, rows.idx, M, p.d.d_model, c->W<float>(p.final_gain_off), p.d.rms_eps, X, p.KBd,
-                           c->stream));
+                           c->big_gemm, c->stream));
   }
   GemmArgs a = base_args(c);
   a.w[0] = c->packed(p.lm); a.wblk[0] = p.lm.Nblk;
@@ -1072,7 +1074,7 @@ int32_t gvc_decode_actions(gvc_ctx* c, int32_t* tokens_out, float* margins_out, 
         {
           ProfScope ps(c, GVC_K_NORM);
           HIP_TRY(launch_rmsnorm(xdec, nullptr, p.B, p.d.d_model, c->W<float>(p.final_gain_off), p.d.rms_eps,
-                                 c->K<bf16>(p.x_off), p.KBd, s));
+                                 c->K<bf16>(p.x_off), p.KBd, c->big_gemm, s));
         }
       } else {
         for (int l = 0; l < p.L; ++l) {

@@ -28,8 +28,11 @@ hipError_t launch_layernorm(const float* src, int M, int d, const float* gain, c
                             bf16* x, int KB, hipStream_t s);
 hipError_t launch_gather_visual(const bf16* src, const int* idx, const int* pos, int M, int P, int N, int KB,
                                 bf16* x, hipStream_t s);
+// tiled: one workgroup per block of 16 rows (many-row sessions) instead of
+// one per row; the two sum a row's squares in different orders, so a session
+// keeps one choice.
 hipError_t launch_rmsnorm(const float* src, const int* idx, int M, int d, const float* gain, float eps,
-                          bf16* x, int KB, hipStream_t s);
+                          bf16* x, int KB, bool tiled, hipStream_t s);
 hipError_t launch_gemm_big(const GemmArgs& a, int epi, hipStream_t s);
 // Split-k prompt-pass GEMM (k_gemm_sk, then the slice sum and epilogue);
 // workgroups own groups of gemm_sk_group_blocks() weight blocks.

@@ -191,6 +191,60 @@ __global__ __launch_bounds__(256) void k_rmsnorm(const float* __restrict__ src, 
   }
 }
 
+// The same RMSNorm for one block of 16 rows per workgroup (d % 32 == 0,
+// d <= 32 * kNormWaves * kNormFrags): wave w takes k fragments w, w + 8, ...;
+// lane l holds row l % 16 and k sub-block l / 16 of each (8 values, kept in
+// registers between the sum of squares and the scaling), so every store
+// writes one whole 1 KiB fragment.  A row's sum of squares runs per lane over
+// its fragments in order, then over the four sub-blocks and the waves in a
+// fixed order.  Rows past M (the rest of the last block) repeat row M - 1.
+constexpr int kNormWaves = 8, kNormFrags = 16;
+__global__ __launch_bounds__(kNormWaves * 64) void k_rmsnorm16(const float* __restrict__ src,
+                                                               const int* __restrict__ idx, int M, int d,
+                                                               const float* __restrict__ gain, float eps,
+                                                               bf16* __restrict__ x, int KB) {
+  __shared__ float red[kNormWaves][16];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int mb = blockIdx.x, r = lane & 15, sg = lane >> 4;
+  const int m = min(mb * 16 + r, M - 1);
+  const float* row = src + (size_t)(idx ? idx[m] : m) * d;
+  const int nf = d / 32;
+  float4 v[kNormFrags][2];
+  float ss = 0.f;
+#pragma unroll
+  for (int i = 0; i < kNormFrags; ++i) {
+    const int f = w + i * kNormWaves;
+    if (f < nf) {
+      const int c = f * 32 + sg * 8;
+      v[i][0] = *(const float4*)(row + c);
+      v[i][1] = *(const float4*)(row + c + 4);
+      const float4 a = v[i][0], b = v[i][1];
+      ss += a.x * a.x + a.y * a.y + a.z * a.z + a.w * a.w + b.x * b.x + b.y * b.y + b.z * b.z + b.w * b.w;
+    }
+  }
+  ss += __shfl_xor(ss, 16);
+  ss += __shfl_xor(ss, 32);
+  if (lane < 16) red[w][lane] = ss;
+  __syncthreads();
+  float tot = 0.f;
+#pragma unroll
+  for (int j = 0; j < kNormWaves; ++j) tot += red[j][r];
+  const float inv = 1.0f / sqrtf(tot / (float)d + eps);
+#pragma unroll
+  for (int i = 0; i < kNormFrags; ++i) {
+    const int f = w + i * kNormWaves;
+    if (f < nf) {
+      const int c = f * 32 + sg * 8;
+      const float4 a = v[i][0], b = v[i][1];
+      const float4 ga = *(const float4*)(gain + c), gb = *(const float4*)(gain + c + 4);
+      const u16x8 o = {f2bf(a.x * inv * ga.x), f2bf(a.y * inv * ga.y), f2bf(a.z * inv * ga.z),
+                       f2bf(a.w * inv * ga.w), f2bf(b.x * inv * gb.x), f2bf(b.y * inv * gb.y),
+                       f2bf(b.z * inv * gb.z), f2bf(b.w * inv * gb.w)};
+      *(u16x8*)(x + ((size_t)(mb * KB + f) * 64 + lane) * 8) = o;
+    }
+  }
+}
+
 // LayerNorm of fp32 rows (ViT blocks): (x - mean) / sqrt(var + eps) * gain
 // + bias, the variance taken about the mean in a second pass over the row;
 // bf16 out in frag layout.  One workgroup of 256 threads per row; d % 8 == 0.
@@ -412,9 +466,13 @@ hipError_t launch_im2row(const uint8_t* frame, int views, int img, int patch, co
 }
 
 hipError_t launch_rmsnorm(const float* src, const int* idx, int M, int d, const float* gain, float eps, bf16* x,
-                          int KB, hipStream_t s) {
+                          int KB, bool tiled, hipStream_t s) {
   if (M == 0) return hipSuccess;
-  hipLaunchKernelGGL(k_rmsnorm, dim3(M), dim3(256), 0, s, src, idx, d, gain, eps, x, KB);
+  if (tiled && d % 32 == 0 && d <= 32 * kNormWaves * kNormFrags)
+    hipLaunchKernelGGL(k_rmsnorm16, dim3((M + 15) / 16), dim3(kNormWaves * 64), 0, s, src, idx, M, d, gain, eps, x,
+                       KB);
+  else
+    hipLaunchKernelGGL(k_rmsnorm, dim3(M), dim3(256), 0, s, src, idx, d, gain, eps, x, KB);
   return hipGetLastError();
 }
 
