@@ -480,7 +480,7 @@ int32_t run_vit(gvc_ctx* c, const uint8_t* frame_t) {
     {
       ProfScope ps(c, GVC_K_VIT);
       HIP_TRY(launch_attn_prefill(Q, Kv, Vv, rows.pos, c->K<int>(p.vepc_off), c->K<int>(p.vepo_off), p.E, p.Hv,
-                                  p.dhv, p.kvpad_v, (p.Sv + 15) / 16, O, p.KBv, 0, p.Sv - 1, s));
+                                  p.dhv, p.kvpad_v, (p.Sv + 15) / 16, O, p.KBv, 0, p.Sv - 1, false, s));
     }
     {
       GemmArgs a = vit_args(c);
@@ -562,7 +562,7 @@ int32_t run_layer(gvc_ctx* c, int l, const RowMap& rows, int M, float* src, floa
   {
     ProfScope ps(c, k0 + 1);
     HIP_TRY(launch_attn_prefill(Q, c->Kc(l), c->Vc(l), rows.pos, epc, epo, p.B, p.H, p.dh, p.kv_pad, max_tiles, O,
-                                p.KBd, p.block_first, p.block_last, c->stream));
+                                p.KBd, p.block_first, p.block_last, c->big_gemm, c->stream));
   }
   if (p.stage2 || p.stage3) {   // Stage 2 / 3 signals of this layer, for the next step's selection
     ProfScope ps(c, GVC_K_STAGE2);

@@ -48,7 +48,7 @@ hipError_t launch_text_vis(const bf16* q, const bf16* kc, const int* ep_counts, 
 hipError_t launch_attn_prefill(const bf16* q, const bf16* kc, const bf16* vc, const int* rows_pos,
                                const int* ep_counts, const int* ep_offsets, int B, int H, int head_dim,
                                int kv_pad, int max_tiles, bf16* o, int KB, int block_first, int block_last,
-                               hipStream_t s);
+                               bool grouped, hipStream_t s);
 hipError_t launch_attn_decode(const float* qraw, const float* kraw, bf16* kc, const bf16* vc, const float2* rope,
                               int B, int H, int head_dim, int kv_pad, int pos, bf16* o, int KB, hipStream_t s);
 hipError_t launch_embed_tokens(const bf16* embed, const int* tokens, int tok_stride, int B, int d,

@@ -16,6 +16,11 @@
 // contiguous bytes per lane.
 // Decode: one workgroup per (head, episode) and one query.
 #include "gvc_kernels.h"
+#include "gvc_sync.h"
+
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+#define GPA(p) ((const void __attribute__((address_space(1)))*)(p))
+#define LPA(p) ((void __attribute__((address_space(3)))*)(p))
 
 namespace gvc {
 
@@ -181,6 +186,148 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn_prefill(
       if (r < cnt) o[frag_off(off + r, h * DH + c * 16 + col, KB)] = f2bf(v[i] / lt[i]);
     }
   }
+}
+
+// Grouped variant for many-row sessions (DH = 128): one workgroup of
+// kGrpWaves waves per (episode, head, kGrpWaves query tiles of 16 rows).
+// Wave w owns query tile blockIdx.x * kGrpWaves + w and walks every key tile
+// up to its rows' last key with one online softmax (no merge across waves).
+// Each key tile's K rows and V columns (32 keys) are copied once per
+// workgroup straight into LDS (global_load_lds), three stages deep with one
+// barrier per tile; a stage is overwritten two tiles after it was read, once
+// every wave has passed the barrier in between.  The 16-byte chunks sit
+// XOR-swizzled in LDS (K: chunk ^ key % 16 within a key row; V: chunk ^
+// (dim / 4) % 4 within a dimension's 32 keys), so the 16 lanes that read one
+// MFMA operand row group hit distinct banks; each lane of a copy fetches the
+// global chunk that belongs at its LDS slot.  Per row the arithmetic is that
+// of a single wave walking all of its key tiles in order: a tile entirely
+// past a row's last key leaves its running max, sum and output unchanged, so
+// a row's result does not depend on which rows share its tile.
+constexpr int kGrpWaves = 4, kGrpStages = 3;
+constexpr int kGrpChunks = 32 * 128 * 2 / 16;           // 16-byte chunks per K (or V) tile
+constexpr int kGrpCopies = kGrpChunks / (kGrpWaves * 64);   // copies per wave per tile, each of K and V
+
+__global__ __launch_bounds__(kGrpWaves * 64) void k_attn_prefill_grp(
+    const bf16* __restrict__ q, const bf16* __restrict__ kc, const bf16* __restrict__ vc,
+    const int* __restrict__ rows_pos, const int* __restrict__ ep_counts, const int* __restrict__ ep_offsets, int H,
+    int kv_pad, bf16* __restrict__ o, int KB, int block_first, int block_last) {
+  constexpr int DH = 128, NK = DH / 32, NO = DH / 16;
+  static_assert(kGrpCopies * kGrpWaves * 64 == kGrpChunks, "tile copies");
+  __shared__ u32x4 kv_lds[kGrpStages][2][kGrpChunks];
+  __shared__ bf16 ps_all[kGrpWaves][16 * 32];
+  const int h = blockIdx.y, b = blockIdx.z;
+  const int cnt = ep_counts[b];
+  const int row0 = blockIdx.x * kGrpWaves * 16;
+  if (row0 >= cnt) return;   // uniform over the workgroup
+  const int off = ep_offsets[b];
+  const int lane = threadIdx.x & 63, wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  bf16* ps = ps_all[wv];
+  const int col = lane & 15, grp = lane >> 4;
+  const int d = H * DH;
+  auto key_last = [&](int p) { return p >= block_first ? block_last : p; };
+  // key tiles of the workgroup: up to the last key of its last row
+  const int wg_last = min(cnt, row0 + kGrpWaves * 16) - 1;
+  const int ntiles = key_last(rows_pos[off + wg_last]) / 32 + 1;
+  const int tile = blockIdx.x * kGrpWaves + wv;
+  const bool active = tile * 16 < cnt;
+  const int last = active ? min(cnt, tile * 16 + 16) - 1 : wg_last;
+  const int max_pos = active ? key_last(rows_pos[off + last]) : -1;
+  int qpos[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) qpos[i] = key_last(rows_pos[off + min(tile * 16 + grp * 4 + i, last)]);
+  bf16x8 qf[NK];
+  {
+    const int r = min(tile * 16 + col, last);
+    const bf16* qr = q + (size_t)(off + r) * d + h * DH + grp * 8;
+#pragma unroll
+    for (int kk = 0; kk < NK; ++kk) qf[kk] = *(const bf16x8*)(qr + kk * 32);
+  }
+  const bf16* kbase = kc + (size_t)(b * H + h) * kv_pad * DH;
+  const bf16* vbase = vc + (size_t)(b * H + h) * DH * kv_pad;
+  // copy n of tile t: K slots n*64 + lane (key n*4 + lane/16, chunk lane%16),
+  // V slots n*64 + lane (dimension n*16 + lane/4, chunk lane%4); tiles past
+  // the last re-read it (in bounds)
+  auto issue = [&](int t) {
+    const int j0 = min(t, ntiles - 1) * 32;
+    u32x4* st = kv_lds[t % kGrpStages][0];
+#pragma unroll
+    for (int c = 0; c < kGrpCopies; ++c) {
+      const int n = wv * kGrpCopies + c;
+      const int key = n * 4 + (lane >> 4), kch = (lane & 15) ^ (key & 15);
+      __builtin_amdgcn_global_load_lds(GPA(kbase + (size_t)(j0 + key) * DH + kch * 8), LPA(st + n * 64), 16, 0, 0);
+    }
+#pragma unroll
+    for (int c = 0; c < kGrpCopies; ++c) {
+      const int n = wv * kGrpCopies + c;
+      const int dim = n * 16 + (lane >> 2), vch = (lane & 3) ^ ((dim >> 2) & 3);
+      __builtin_amdgcn_global_load_lds(GPA(vbase + (size_t)dim * kv_pad + j0 + vch * 8),
+                                       LPA(st + kGrpChunks + n * 64), 16, 0, 0);
+    }
+  };
+  const float scale = 1.0f / sqrtf((float)DH);
+  floatx4 acc[NO];
+#pragma unroll
+  for (int c = 0; c < NO; ++c) acc[c] = floatx4{0, 0, 0, 0};
+  float m_run[4], l_run[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) { m_run[i] = -INFINITY; l_run[i] = 0.f; }
+  issue(0);
+  for (int t = 0; t < ntiles; ++t) {
+    issue(t + 1);
+    wait_vmcnt<2 * kGrpCopies>();
+    lds_barrier();
+    const int j0 = t * 32;
+    if (j0 > max_pos) continue;   // uniform per wave; the barrier of the next tile is still reached
+    const u32x4* kt = kv_lds[t % kGrpStages][0];
+    const u32x4* vt = kv_lds[t % kGrpStages][1];
+    floatx4 s0 = {0, 0, 0, 0}, s1 = {0, 0, 0, 0};
+#pragma unroll
+    for (int kk = 0; kk < NK; ++kk) {
+      const int ch = (kk * 4 + grp) ^ col;   // key col (and 16 + col): key % 16 == col
+      s0 = mfma16(qf[kk], __builtin_bit_cast(bf16x8, kt[col * 16 + ch]), s0);
+      s1 = mfma16(qf[kk], __builtin_bit_cast(bf16x8, kt[(16 + col) * 16 + ch]), s1);
+    }
+    float p0[4], p1[4], alpha[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float a0 = (j0 + col <= qpos[i]) ? s0[i] * scale : -INFINITY;
+      const float a1 = (j0 + 16 + col <= qpos[i]) ? s1[i] * scale : -INFINITY;
+      const float mx = group_max<16>(fmaxf(a0, a1));
+      const float mn = fmaxf(m_run[i], mx);
+      const float mb = mn == -INFINITY ? 0.f : mn;
+      alpha[i] = __expf(m_run[i] - mb);
+      p0[i] = __expf(a0 - mb);
+      p1[i] = __expf(a1 - mb);
+      const float sm = group_sum<16>(p0[i] + p1[i]);
+      l_run[i] = l_run[i] * alpha[i] + sm;
+      m_run[i] = mn;
+    }
+#pragma unroll
+    for (int c = 0; c < NO; ++c)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) acc[c][i] *= alpha[i];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      ps[(grp * 4 + i) * 32 + col] = f2bf(p0[i]);
+      ps[(grp * 4 + i) * 32 + 16 + col] = f2bf(p1[i]);
+    }
+    const bf16x8 pa = *(const bf16x8*)(ps + col * 32 + grp * 8);
+#pragma unroll
+    for (int c = 0; c < NO; ++c) {
+      // dimension c*16 + col, keys grp*8..: chunk grp ^ (dim / 4) % 4 = grp ^ col / 4
+      const bf16x8 vf = __builtin_bit_cast(bf16x8, vt[(c * 16 + col) * 4 + (grp ^ (col >> 2))]);
+      acc[c] = mfma16(pa, vf, acc[c]);
+    }
+  }
+  wait_vmcnt<0>();
+  if (!active) return;
+#pragma unroll
+  for (int c = 0; c < NO; ++c)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = tile * 16 + grp * 4 + i;
+      if (r < cnt) o[frag_off(off + r, h * DH + c * 16 + col, KB)] = f2bf(acc[c][i] / l_run[i]);
+    }
 }
 
 // Stage 2 signal (Sec. III-B: static patches that draw the instruction's
@@ -487,8 +634,15 @@ __global__ __launch_bounds__(512) void k_attn_decode(const float* __restrict__ q
 
 hipError_t launch_attn_prefill(const bf16* q, const bf16* kc, const bf16* vc, const int* rows_pos,
                                const int* ep_counts, const int* ep_offsets, int B, int H, int head_dim, int kv_pad,
-                               int max_tiles, bf16* o, int KB, int block_first, int block_last, hipStream_t s) {
+                               int max_tiles, bf16* o, int KB, int block_first, int block_last, bool grouped,
+                               hipStream_t s) {
   if (block_first <= block_last && block_last >= kv_pad) return hipErrorInvalidValue;
+  if (grouped && head_dim == 128) {
+    const dim3 grid_g((max_tiles + kGrpWaves - 1) / kGrpWaves, H, B);
+    hipLaunchKernelGGL(k_attn_prefill_grp, grid_g, dim3(kGrpWaves * 64), 0, s, q, kc, vc, rows_pos, ep_counts,
+                       ep_offsets, H, kv_pad, o, KB, block_first, block_last);
+    return hipGetLastError();
+  }
   dim3 grid(max_tiles, H, B);
   if (head_dim == 128)
     hipLaunchKernelGGL(k_attn_prefill<128>, grid, dim3(kAttnWaves * 64), 0, s, q, kc, vc, rows_pos, ep_counts,

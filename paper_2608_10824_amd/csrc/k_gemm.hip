@@ -16,6 +16,7 @@
 //    LDS in a fixed order, so results are bitwise reproducible and no
 //    workgroup ever waits on another.
 #include "gvc_kernels.h"
+#include "gvc_sync.h"
 
 namespace gvc {
 
@@ -417,20 +418,6 @@ constexpr int big_lds_bytes() { return kBigStages * big_frags<TW>() * 1024; }
 typedef unsigned u32x4b __attribute__((ext_vector_type(4)));
 #define GPB(p) ((const void __attribute__((address_space(1)))*)(p))
 #define LPB(p) ((void __attribute__((address_space(3)))*)(p))
-
-// Workgroup barrier for pipelines fed by direct-to-LDS loads.
-// __syncthreads() also fences memory, and that fence makes every wave wait
-// for all of its outstanding global loads (vmcnt 0), prefetches of later
-// steps included, before the barrier.  Here the caller first waits (with
-// s_waitcnt) for exactly the loads the next step reads; the empty asm
-// statements keep the compiler from moving memory accesses across the
-// barrier.  Only for LDS data written by those loads or read before the
-// previous barrier.
-__device__ __forceinline__ void lds_barrier() {
-  asm volatile("" ::: "memory");
-  __builtin_amdgcn_s_barrier();
-  asm volatile("" ::: "memory");
-}
 
 template <int N>
 __device__ __forceinline__ void big_wait_vm() {
