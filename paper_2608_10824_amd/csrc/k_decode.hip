@@ -67,6 +67,20 @@ __device__ __forceinline__ void wait_vm() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x0F70);
 }
 __device__ __forceinline__ void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(0xC07F); }
+// Block barrier without a memory fence.  __syncthreads() would also make
+// every wave wait for all of its outstanding global loads, the weight ring's
+// prefetches of the next step included, before it arrives.  Everything the
+// pass shares through a block barrier lives in LDS (each wave's LDS
+// operations complete before it arrives); global data written by one
+// workgroup and read by another passes through grid_sync / head_sync, whose
+// caller waits for its own stores and atomics first, and is read with
+// coherent loads.
+__device__ __forceinline__ void block_sync() {
+  wait_lgkm0();
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
 
 __device__ __forceinline__ rsrc_t rsrc(const void* p, size_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
@@ -181,7 +195,7 @@ __device__ __forceinline__ void stage_norm(rsrc_t src, const float* __restrict__
 ss = wave_sum(ss);
     if ((tid & 63) == 0) wred[tid >> 6] = ss;
   }
-  __syncthreads();
+  block_sync();
   if (cw) {
     float tot = 0.f;
 #pragma unroll
@@ -298,7 +312,7 @@ __device__ __forceinline__ void attn_head(int h, int pos, int d, int kv_pad, boo
       }
     }
   }
-  __syncthreads();
+  block_sync();
   // scores q . k_j / sqrt(d_h), j <= pos
   float mx = -INFINITY;
   if (!syncw) {
@@ -335,7 +349,7 @@ s = group_sum<LPK>(s);
     mx = wave_max(mx);
     if (lane == 0) wred[wv] = mx;
   }
-  __syncthreads();
+  block_sync();
   float sm = 0.f;
   if (!syncw) {
     mx = wred[0];
@@ -348,12 +362,12 @@ s = group_sum<LPK>(s);
     }
     sm = wave_sum(sm);
   }
-  __syncthreads();
+  block_sync();
   if (!syncw) {
     if (lane == 0) wred[8 + wv] = sm;
     for (int j = n_keys + tid; j < nchunk * 8; j += NT) sc[j] = 0.f;   // pad the last 8-key chunk
   }
-  __syncthreads();
+  block_sync();
   if (!syncw) {
     float tot = 0.f;
 #pragma unroll
@@ -377,7 +391,7 @@ s = group_sum<LPK>(s);
 acc = group_sum<CG>(acc);
     if (cg == 0) oact[dim] = f2bf(acc / tot);
   }
-  __syncthreads();
+  block_sync();
 }
 
 }  // namespace
@@ -523,7 +537,7 @@ __global__ __launch_bounds__(kThreads) void k_decode_pass(const DecodeArgs a) {
       const bool ok = grid_sync(a, ++nbar);
       if (lane == 0) s_ok = ok;
     }
-    __syncthreads();
+    block_sync();
     return s_ok != 0;
   };
 
@@ -546,7 +560,7 @@ __global__ __launch_bounds__(kThreads) void k_decode_pass(const DecodeArgs a) {
     bf16* const lvc = a.vc + (size_t)l * a.kv_layer_elems;
     // ---------------- 1. QKV projection (head ah's rows, published to the head's workgroups)
     stage_norm(r_x, gains + (size_t)l * 2 * d, d, a.KBd * 32, a.eps, act, wred);
-    __syncthreads();
+    block_sync();
     if (!syncw) run_step(nseg0, nkd, k0d);
     if (syncw && attn && (a.flags & kDecodeWarmKv)) {
       // share asl of head ah's cached keys (rows of DH) and values (dims of
@@ -560,7 +574,7 @@ __global__ __launch_bounds__(kThreads) void k_decode_pass(const DecodeArgs a) {
         for (int o = lane * 16; o < a.pos * 2; o += 1024)
           __builtin_amdgcn_global_load_lds(GP(vb + (size_t)dm * a.kv_pad * 2 + o), LP(sink), 16, 0, 0);
     }
-    __syncthreads();
+    block_sync();
     if (attn) {
       if (syncw) {
         for (int s0 = 0; s0 < nseg0; s0 += 4) {
@@ -573,13 +587,13 @@ __global__ __launch_bounds__(kThreads) void k_decode_pass(const DecodeArgs a) {
         const bool ok = head_sync(a, ah, (unsigned)nsl, ++nhbar);
         if (lane == 0) s_ok = ok;
       }
-      __syncthreads();
+      block_sync();
       if (!s_ok) break;
 
       // ---------------- 2. attention of head ah, times W_o's slice asl of head-ah columns
       attn_head<DH>(ah, a.pos, d, a.kv_pad, asl == 0, xl, lkc, lvc, rp, r_qkv, qs, kn, vn, wred, sc, act);
       if (!syncw) run_step(nseg_o, KH, 0);
-      __syncthreads();
+      block_sync();
       if (syncw) {
         for (int w = 0; w < kWaves; ++w) {
           const int wb0 = w * nsb / kWaves, wn = (w + 1) * nsb / kWaves - wb0;
@@ -596,9 +610,9 @@ __global__ __launch_bounds__(kThreads) void k_decode_pass(const DecodeArgs a) {
 
     // ---------------- 3. gate/up projection + SwiGLU
     stage_norm(r_r, gains + (size_t)l * 2 * d + d, d, a.KBd * 32, a.eps, act, wred);
-    __syncthreads();
+    block_sync();
     if (!syncw) run_step(nseg2, nkd, k0d);
-    __syncthreads();
+    block_sync();
     if (syncw) {
       for (int s0 = 0; s0 < nseg2 / 2; s0 += 4) {
         const int pr = s0 + (lane >> 4), t = lane & 15;
@@ -612,9 +626,9 @@ __global__ __launch_bounds__(kThreads) void k_decode_pass(const DecodeArgs a) {
 
     // ---------------- 4. down projection + residual; r = x for the next layer's step 2
     stage_copy(r_act, F, a.KBf * 32, act);
-    __syncthreads();
+    block_sync();
     if (!syncw) run_step(nseg3, nkf, k0f);
-    __syncthreads();
+    block_sync();
     if (syncw) {
       for (int s0 = 0; s0 < nseg3; s0 += 4) {
         const int s = s0 + (lane >> 4), t = lane & 15;

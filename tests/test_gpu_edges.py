@@ -40,16 +40,19 @@ def _chunk_cfg(name):
                                     reduce_min=True, action_bidir=True)
 
 
-@pytest.mark.parametrize("name", ["C4T", "C4T-bidir", "MID-bidir"])
-def test_parallel_action_chunk_complete_parity(name):
+@pytest.mark.parametrize("name", ["C4T", "C4T-bidir", "MID-bidir", "MID-bidir-big"])
+def test_parallel_action_chunk_complete_parity(name, monkeypatch):
     """Two views, a proprio row and the action-query rows decoded in one pass
     (the OFT variant, Sec. V-A), causal or with the action rows attending to
     each other both ways: state, every position's logits, tokens, margins
-    and the minimum-margin gate."""
+    and the minimum-margin gate.  MID-bidir-big runs the many-row kernels
+    (projections, 16-row norm, grouped attention) on the same case."""
     from paper_2608_10824_amd import gvc
     cfg = _chunk_cfg(name)
     w = synth.model_weights(cfg)
     si = synth.step_inputs(cfg, 90)
+    if name.endswith("-big"):
+        monkeypatch.setenv("GVC_GEMM", "big")
     s = _session(cfg, w)
     o = OracleVLA(cfg, w)
     fp, ft, ids, ex = si["frame_prev"], si["frame_t"], si["text_ids"], si["extra_rows"]
