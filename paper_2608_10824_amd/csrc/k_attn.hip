@@ -28,6 +28,11 @@ namespace gvc {
 // round robin; each keeps its own online softmax (running max, sum and
 // output), and the partial results are merged through LDS at the end.
 constexpr int kAttnWaves = 4;
+// Row stride (bf16) of a wave's 16 x 32 tile of probabilities in LDS: 80-byte
+// rows put the four row groups a store instruction writes, and the sixteen
+// rows an operand read takes, on distinct banks (64-byte rows would stack
+// them four deep).
+constexpr int kPsStride = 40;
 
 template <int DH>
 __global__ __launch_bounds__(kAttnWaves * 64) void k_attn_prefill(
@@ -37,7 +42,7 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn_prefill(
   constexpr int NK = DH / 32;   // k-steps of QK^T
   constexpr int NO = DH / 16;   // output column blocks
   static_assert(NO % kAttnWaves == 0, "output blocks per merging wave");
-  __shared__ bf16 ps_all[kAttnWaves][16 * 32];
+  __shared__ __attribute__((aligned(16))) bf16 ps_all[kAttnWaves][16 * kPsStride];
   __shared__ floatx4 m_acc[kAttnWaves][NO][64];
   __shared__ float m_ml[kAttnWaves][8][64];
   const int tile = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
@@ -132,10 +137,10 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn_prefill(
     // [16][32] -> A layout (a wave's LDS accesses complete in order)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      ps[(grp * 4 + i) * 32 + col] = f2bf(p0[i]);
-      ps[(grp * 4 + i) * 32 + 16 + col] = f2bf(p1[i]);
+      ps[(grp * 4 + i) * kPsStride + col] = f2bf(p0[i]);
+      ps[(grp * 4 + i) * kPsStride + 16 + col] = f2bf(p1[i]);
     }
-    const bf16x8 pa = *(const bf16x8*)(ps + col * 32 + grp * 8);
+    const bf16x8 pa = *(const bf16x8*)(ps + col * kPsStride + grp * 8);
 #pragma unroll
     for (int c = 0; c < NO; ++c) acc[c] = mfma16(pa, vf[c], acc[c]);
 #pragma unroll
@@ -214,7 +219,7 @@ __global__ __launch_bounds__(kGrpWaves * 64) void k_attn_prefill_grp(
   constexpr int DH = 128, NK = DH / 32, NO = DH / 16;
   static_assert(kGrpCopies * kGrpWaves * 64 == kGrpChunks, "tile copies");
   __shared__ u32x4 kv_lds[kGrpStages][2][kGrpChunks];
-  __shared__ bf16 ps_all[kGrpWaves][16 * 32];
+  __shared__ __attribute__((aligned(16))) bf16 ps_all[kGrpWaves][16 * kPsStride];
   const int h = blockIdx.y, b = blockIdx.z;
   const int cnt = ep_counts[b];
   const int row0 = blockIdx.x * kGrpWaves * 16;
@@ -308,10 +313,10 @@ __global__ __launch_bounds__(kGrpWaves * 64) void k_attn_prefill_grp(
       for (int i = 0; i < 4; ++i) acc[c][i] *= alpha[i];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      ps[(grp * 4 + i) * 32 + col] = f2bf(p0[i]);
-      ps[(grp * 4 + i) * 32 + 16 + col] = f2bf(p1[i]);
+      ps[(grp * 4 + i) * kPsStride + col] = f2bf(p0[i]);
+      ps[(grp * 4 + i) * kPsStride + 16 + col] = f2bf(p1[i]);
     }
-    const bf16x8 pa = *(const bf16x8*)(ps + col * 32 + grp * 8);
+    const bf16x8 pa = *(const bf16x8*)(ps + col * kPsStride + grp * 8);
 #pragma unroll
     for (int c = 0; c < NO; ++c) {
       // dimension c*16 + col, keys grp*8..: chunk grp ^ (dim / 4) % 4 = grp ^ col / 4
