@@ -500,7 +500,7 @@ __global__ __launch_bounds__(kTvWaves * 64) void k_text_vis(const bf16* __restri
 // slot being written.  Values: the cache is dim-major, so a lane reads 8
 // consecutive keys of one dim.
 template <int DH, int NQ>
-__global__ __launch_bounds__(512) void k_attn_decode(const float* __restrict__ qraw, const float* __restrict__ kraw,
+__global__ __launch_bounds__(512, 4) void k_attn_decode(const float* __restrict__ qraw, const float* __restrict__ kraw,
                                                      bf16* __restrict__ kc, const bf16* __restrict__ vc,
                                                      const float2* __restrict__ rope, int H, int kv_pad, int pos,
                                                      bf16* __restrict__ o, int KB) {
@@ -510,7 +510,7 @@ __global__ __launch_bounds__(512) void k_attn_decode(const float* __restrict__ q
   constexpr int NT = 512;
   constexpr int LPK = DH / 8;            // lanes per key
   constexpr int KPI = NT / LPK;          // keys per load round
-  constexpr int U = 10;                  // load rounds per batch
+  constexpr int U = 9;                   // load rounds per batch
   constexpr int DQ = DH / NQ;            // value dims of this workgroup
   constexpr int DG = NT / 16;            // dim groups
   constexpr int ND = (DQ + DG - 1) / DG; // dims per thread in the value phase
