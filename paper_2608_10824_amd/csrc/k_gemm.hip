@@ -405,8 +405,8 @@ __global__ __launch_bounds__(KS * KT * 64) void k_gemm_ks(const GemmArgs a) {
 // wt*TW..wt*TW+TW-1 (4 TW MFMAs per k step from 4 + TW LDS fragment reads)
 // and runs the same fused epilogue as k_gemm_ks.  Each row's sum runs over
 // k in order, so a row's result does not depend on the tile it falls in or
-// on the tile height (TW = 4: 256-row tiles, TW = 2: 128-row tiles; the
-// launcher picks one per launch).
+// on the tile height (TW = 4, 3, 2: 256-, 192-, 128-row tiles; the launcher
+// picks one per launch).
 constexpr int kBigWP = 2, kBigWT = 4, kBigPW = 2;
 constexpr int kBigPairs = kBigWP * kBigPW;
 constexpr int kBigStages = 3;
@@ -522,9 +522,12 @@ static hipError_t launch_big_tw(GemmArgs a, hipStream_t s) {
 
 // Tile height: a launch takes about ceil(workgroups / resident) rounds of
 // one workgroup's k loop.  Two 256-row workgroups fit a CU (72 KiB of LDS
-// each), three 128-row ones (48 KiB); a round of 128-row tiles, half the
-// MFMAs of a 256-row round but shared three ways, measured 0.885 of one
-// on the 7B projections at 736-4416 rows.
+// each), two 192-row ones (60 KiB), three 128-row ones (48 KiB); on the 7B
+// projections at 736-4416 rows a round of 128-row tiles measured 0.885 of a
+// 256-row round and, on the narrow (d-wide) ones, a round of 192-row tiles
+// 0.87.  192-row tiles are only taken for narrow launches that would give
+// more than one 128-row workgroup per CU (wider ones and smaller launches
+// measured faster on the other two).
 template <int EPI>
 static hipError_t launch_big_epi(const GemmArgs& a, hipStream_t s) {
   static int cus = 0;
@@ -537,8 +540,15 @@ static hipError_t launch_big_epi(const GemmArgs& a, hipStream_t s) {
   const long long ntiles = (a.n_pairs + kBigPairs - 1) / kBigPairs;
   const long long j4 = ntiles * ((a.mblocks + 4 * kBigWT - 1) / (4 * kBigWT));
   const long long j2 = ntiles * ((a.mblocks + 2 * kBigWT - 1) / (2 * kBigWT));
+  const long long j3 = ntiles * ((a.mblocks + 3 * kBigWT - 1) / (3 * kBigWT));
   const long long r4 = (j4 + 2LL * cus - 1) / (2LL * cus), r2 = (j2 + 3LL * cus - 1) / (3LL * cus);
-  if (885 * r2 < 1000 * r4) return launch_big_tw<EPI, 2>(a, s);
+  const long long r3 = (j3 + 2LL * cus - 1) / (2LL * cus);
+  long long best = 1000 * r4;
+  int tw = 4;
+  if (885 * r2 < best) { best = 885 * r2; tw = 2; }
+  if (ntiles <= 32 && j2 > cus && 870 * r3 < best) tw = 3;
+  if (tw == 3) return launch_big_tw<EPI, 3>(a, s);
+  if (tw == 2) return launch_big_tw<EPI, 2>(a, s);
   return launch_big_tw<EPI, 4>(a, s);
 }
 
