@@ -536,6 +536,7 @@ static hipError_t launch_big_epi(const GemmArgs& a, hipStream_t s) {
     hipError_t e = hipGetDevice(&dev);
     if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
     if (e != hipSuccess) return e;
+    if (cus <= 0) return hipErrorInvalidDevice;
   }
   const long long ntiles = (a.n_pairs + kBigPairs - 1) / kBigPairs;
   const long long j4 = ntiles * ((a.mblocks + 4 * kBigWT - 1) / (4 * kBigWT));
