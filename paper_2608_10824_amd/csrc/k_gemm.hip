@@ -524,10 +524,10 @@ static hipError_t launch_big_tw(GemmArgs a, hipStream_t s) {
 // one workgroup's k loop.  Two 256-row workgroups fit a CU (72 KiB of LDS
 // each), two 192-row ones (60 KiB), three 128-row ones (48 KiB); on the 7B
 // projections at 736-4416 rows a round of 128-row tiles measured 0.885 of a
-// 256-row round and, on the narrow (d-wide) ones, a round of 192-row tiles
-// 0.87.  192-row tiles are only taken for narrow launches that would give
-// more than one 128-row workgroup per CU (wider ones and smaller launches
-// measured faster on the other two).
+// 256-row round and, on the output, down and QKV projections, a round of
+// 192-row tiles 0.87.  192-row tiles are only taken for launches of at most
+// 96 weight tiles that would give more than one 128-row workgroup per CU
+// (gate/up and smaller launches measured faster on the other two).
 template <int EPI>
 static hipError_t launch_big_epi(const GemmArgs& a, hipStream_t s) {
   static int cus = 0;
@@ -547,7 +547,7 @@ static hipError_t launch_big_epi(const GemmArgs& a, hipStream_t s) {
   long long best = 1000 * r4;
   int tw = 4;
   if (885 * r2 < best) { best = 885 * r2; tw = 2; }
-  if (ntiles <= 32 && j2 > cus && 870 * r3 < best) tw = 3;
+  if (ntiles <= 96 && j2 > cus && 870 * r3 < best) tw = 3;
   if (tw == 3) return launch_big_tw<EPI, 3>(a, s);
   if (tw == 2) return launch_big_tw<EPI, 2>(a, s);
   return launch_big_tw<EPI, 4>(a, s);
