@@ -182,14 +182,20 @@ __device__ __forceinline__ void stage_norm(rsrc_t src, const float* __restrict__
   float4 y[4];
   float ss = 0.f;
   if (cw) {
+    // every load is issued (indices past the end re-read the last chunk, in
+    // bounds) before any is used: one memory round trip, not one per chunk
+    float4 v[4], g[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int c = tid + i * kWaves * 64;
-      if (c < n / 4) {
-        const float4 v = __builtin_bit_cast(float4, ld_b128(src, c * 16));
-        const float4 g = *(const float4*)(gain + c * 4);
-        ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
-        y[i] = float4{v.x * g.x, v.y * g.y, v.z * g.z, v.w * g.w};
+      const int c = min(tid + i * kWaves * 64, n / 4 - 1);
+      v[i] = __builtin_bit_cast(float4, ld_b128(src, c * 16));
+      g[i] = *(const float4*)(gain + c * 4);
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      if (tid + i * kWaves * 64 < n / 4) {
+        ss += v[i].x * v[i].x + v[i].y * v[i].y + v[i].z * v[i].z + v[i].w * v[i].w;
+        y[i] = float4{v[i].x * g[i].x, v[i].y * g[i].y, v[i].z * g[i].z, v[i].w * g[i].w};
       }
     }
 ss = wave_sum(ss);
@@ -217,10 +223,7 @@ __device__ __forceinline__ void stage_copy(rsrc_t src, int n, int npad, bf16* ac
   if (tid >= kWaves * 64) return;
   u32x4 v[4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int c = tid + i * kWaves * 64;
-    if (c < n / 8) v[i] = ld_b128(src, c * 16);
-  }
+  for (int i = 0; i < 4; ++i) v[i] = ld_b128(src, min(tid + i * kWaves * 64, n / 8 - 1) * 16);   // all loads first
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int c = tid + i * kWaves * 64;

@@ -172,22 +172,60 @@ __global__ __launch_bounds__(256) void k_rmsnorm(const float* __restrict__ src, 
   __shared__ float red[4];
   const int m = blockIdx.x;
   const float* row = src + (size_t)(idx ? idx[m] : m) * d;
+  // Rows of up to kRowChunks * 2048 values stay in registers with their
+  // gains, every load issued before any is used (chunks past the end re-read
+  // the last one, in bounds): one memory round trip.  Longer rows are read
+  // twice.  The sum of squares runs in the same order either way.
+  constexpr int kRowChunks = 4;
+  const int t8 = threadIdx.x * 8;
   float ss = 0.f;
-  for (int c = threadIdx.x * 8; c < d; c += 256 * 8) {
+  if (d <= kRowChunks * 256 * 8) {
+    float4 ra[kRowChunks], rb[kRowChunks], ga[kRowChunks], gb[kRowChunks];
+#pragma unroll
+    for (int i = 0; i < kRowChunks; ++i) {
+      const int c = min(t8 + i * 256 * 8, d - 8);
+      ra[i] = *(const float4*)(row + c);
+      rb[i] = *(const float4*)(row + c + 4);
+      ga[i] = *(const float4*)(gain + c);
+      gb[i] = *(const float4*)(gain + c + 4);
+    }
+#pragma unroll
+    for (int i = 0; i < kRowChunks; ++i) {
+      if (t8 + i * 256 * 8 < d) {
+        const float4 a = ra[i], b = rb[i];
+        ss += a.x * a.x + a.y * a.y + a.z * a.z + a.w * a.w + b.x * b.x + b.y * b.y + b.z * b.z + b.w * b.w;
+      }
+    }
+    for (int o = 32; o > 0; o >>= 1) ss += __shfl_xor(ss, o);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
+    __syncthreads();
+    const float inv = 1.0f / sqrtf((red[0] + red[1] + red[2] + red[3]) / (float)d + eps);
+#pragma unroll
+    for (int i = 0; i < kRowChunks; ++i) {
+      const int c = t8 + i * 256 * 8;
+      if (c < d) {
+        const float4 a = ra[i], b = rb[i], g0 = ga[i], g1 = gb[i];
+        *(u16x8*)(x + frag_off(m, c, KB)) =
+            u16x8{f2bf(a.x * inv * g0.x), f2bf(a.y * inv * g0.y), f2bf(a.z * inv * g0.z), f2bf(a.w * inv * g0.w),
+                  f2bf(b.x * inv * g1.x), f2bf(b.y * inv * g1.y), f2bf(b.z * inv * g1.z), f2bf(b.w * inv * g1.w)};
+      }
+    }
+    return;
+  }
+  for (int c = t8; c < d; c += 256 * 8) {
     const float4 a = *(const float4*)(row + c), b = *(const float4*)(row + c + 4);
     ss += a.x * a.x + a.y * a.y + a.z * a.z + a.w * a.w + b.x * b.x + b.y * b.y + b.z * b.z + b.w * b.w;
   }
   for (int o = 32; o > 0; o >>= 1) ss += __shfl_xor(ss, o);
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
   __syncthreads();
-  const float tot = red[0] + red[1] + red[2] + red[3];
-  const float inv = 1.0f / sqrtf(tot / (float)d + eps);
-  for (int c = threadIdx.x * 8; c < d; c += 256 * 8) {
+  const float inv = 1.0f / sqrtf((red[0] + red[1] + red[2] + red[3]) / (float)d + eps);
+  for (int c = t8; c < d; c += 256 * 8) {
     const float4 a = *(const float4*)(row + c), b = *(const float4*)(row + c + 4);
-    const float4 ga = *(const float4*)(gain + c), gb = *(const float4*)(gain + c + 4);
-    u16x8 o = {f2bf(a.x * inv * ga.x), f2bf(a.y * inv * ga.y), f2bf(a.z * inv * ga.z), f2bf(a.w * inv * ga.w),
-               f2bf(b.x * inv * gb.x), f2bf(b.y * inv * gb.y), f2bf(b.z * inv * gb.z), f2bf(b.w * inv * gb.w)};
-    *(u16x8*)(x + frag_off(m, c, KB)) = o;
+    const float4 g0 = *(const float4*)(gain + c), g1 = *(const float4*)(gain + c + 4);
+    *(u16x8*)(x + frag_off(m, c, KB)) =
+        u16x8{f2bf(a.x * inv * g0.x), f2bf(a.y * inv * g0.y), f2bf(a.z * inv * g0.z), f2bf(a.w * inv * g0.w),
+              f2bf(b.x * inv * g1.x), f2bf(b.y * inv * g1.y), f2bf(b.z * inv * g1.z), f2bf(b.w * inv * g1.w)};
   }
 }
 
@@ -211,13 +249,17 @@ __global__ __launch_bounds__(kNormWaves * 64) void k_rmsnorm16(const float* __re
   const int nf = d / 32;
   float4 v[kNormFrags][2];
   float ss = 0.f;
+  // every load is issued (fragments past the row's end re-read the last one,
+  // in bounds) before any is used: one memory round trip, not one per fragment
 #pragma unroll
   for (int i = 0; i < kNormFrags; ++i) {
-    const int f = w + i * kNormWaves;
-    if (f < nf) {
-      const int c = f * 32 + sg * 8;
-      v[i][0] = *(const float4*)(row + c);
-      v[i][1] = *(const float4*)(row + c + 4);
+    const int c = min(w + i * kNormWaves, nf - 1) * 32 + sg * 8;
+    v[i][0] = *(const float4*)(row + c);
+    v[i][1] = *(const float4*)(row + c + 4);
+  }
+#pragma unroll
+  for (int i = 0; i < kNormFrags; ++i) {
+    if (w + i * kNormWaves < nf) {
       const float4 a = v[i][0], b = v[i][1];
       ss += a.x * a.x + a.y * a.y + a.z * a.z + a.w * a.w + b.x * b.x + b.y * b.y + b.z * b.z + b.w * b.w;
     }
