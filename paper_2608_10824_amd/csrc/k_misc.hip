@@ -242,6 +242,7 @@ __global__ __launch_bounds__(kNormWaves * 64) void k_rmsnorm16(const float* __re
                                                                const float* __restrict__ gain, float eps,
                                                                bf16* __restrict__ x, int KB) {
   __shared__ float red[kNormWaves][16];
+  __shared__ __attribute__((aligned(16))) float gs[32 * kNormWaves * kNormFrags];   // the gains, staged once
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int mb = blockIdx.x, r = lane & 15, sg = lane >> 4;
   const int m = min(mb * 16 + r, M - 1);
@@ -256,6 +257,13 @@ __global__ __launch_bounds__(kNormWaves * 64) void k_rmsnorm16(const float* __re
     const int c = min(w + i * kNormWaves, nf - 1) * 32 + sg * 8;
     v[i][0] = *(const float4*)(row + c);
     v[i][1] = *(const float4*)(row + c + 4);
+  }
+  // the gains go to LDS in the same round trip (read back after the barrier)
+#pragma unroll
+  for (int i = 0; i < 32 * kNormWaves * kNormFrags / (kNormWaves * 64 * 4); ++i) {
+    const int c = threadIdx.x * 4 + i * kNormWaves * 64 * 4;
+    const float4 g = *(const float4*)(gain + min(c, d - 4));
+    if (c < d) *(float4*)(gs + c) = g;
   }
 #pragma unroll
   for (int i = 0; i < kNormFrags; ++i) {
@@ -278,7 +286,7 @@ __global__ __launch_bounds__(kNormWaves * 64) void k_rmsnorm16(const float* __re
     if (f < nf) {
       const int c = f * 32 + sg * 8;
       const float4 a = v[i][0], b = v[i][1];
-      const float4 ga = *(const float4*)(gain + c), gb = *(const float4*)(gain + c + 4);
+      const float4 ga = *(const float4*)(gs + c), gb = *(const float4*)(gs + c + 4);
       const u16x8 o = {f2bf(a.x * inv * ga.x), f2bf(a.y * inv * ga.y), f2bf(a.z * inv * ga.z),
                        f2bf(a.w * inv * ga.w), f2bf(b.x * inv * gb.x), f2bf(b.y * inv * gb.y),
                        f2bf(b.z * inv * gb.z), f2bf(b.w * inv * gb.w)};
