@@ -75,6 +75,6 @@ struct GemmArgs {
 };
 
 // k-steps per pipelined register chunk for a tile of NT blocks of 16 token rows.
-constexpr int gemm_pf(int NT) { return NT == 1 ? 8 : (NT <= 3 ? 4 : (NT <= 6 ? 2 : 1)); }
+constexpr int gemm_pf(int NT) { return NT == 1 ? 4 : (NT <= 3 ? 4 : (NT <= 6 ? 2 : 1)); }
 
 }  // namespace gvc
