@@ -4,8 +4,12 @@ This package is the slow, plain reference that the HIP path is checked
 against.  Only the tests, the smoke entry point and the benchmark's CPU
 baseline leg may import it; the product path never does.  It shares no code
 with the HIP library: it receives the same seeded inputs (from `synth`) and
-recomputes everything with NumPy in float64, one token row at a time, so a
-row's result never depends on which other rows are computed alongside it.
+recomputes everything with NumPy in float64, by default one token row at a
+time, so a row's result never depends on which other rows are computed
+alongside it.  At the 7B shape the tests run it in its batched mode, where
+each projection and each head's attention is one library matrix product
+over the recomputed rows (pinned against the row-at-a-time form and the
+Hugging Face forward).
 
 Contents (each function cites the passage it follows):
   patches  - Stage 1 static-patch detection (Sec. III-B) and the per-layer

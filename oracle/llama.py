@@ -79,3 +79,48 @@ def layer_rows(w: dict, h_in: np.ndarray, rows, pos, K: np.ndarray, V: np.ndarra
 def head_row(h: np.ndarray, g: np.ndarray, w_lm: np.ndarray, eps: float) -> np.ndarray:
     """Final RMSNorm then the LM head: logits of one row."""
     return w_lm @ rmsnorm(h, g, eps)
+
+
+def attend_rows(Q: np.ndarray, last, K: np.ndarray, V: np.ndarray) -> np.ndarray:
+    """attend_row for several query rows at once: Q [M][H][d_h], row i sees the
+    key slots 0..last[i]; the scores and the weighted sum are taken as batched
+    matrix products over the heads (library matmuls as the steps of the same
+    formula), keys past a row's last slot masked out."""
+    M, H, dh = Q.shape
+    last = np.asarray(last)
+    T = int(last.max()) + 1
+    Qh = Q.transpose(1, 0, 2)                        # [H][M][dh]
+    Kh = K[:T].transpose(1, 2, 0)                    # [H][dh][T]
+    Vh = V[:T].transpose(1, 0, 2)                    # [H][T][dh]
+    s = np.matmul(Qh, Kh) / np.sqrt(dh)              # [H][M][T]
+    s = np.where(np.arange(T)[None, None, :] > last[None, :, None], -np.inf, s)
+    s = s - s.max(axis=2, keepdims=True)
+    p = np.exp(s)
+    p = p / p.sum(axis=2, keepdims=True)
+    return np.matmul(p, Vh).transpose(1, 0, 2)       # [M][H][dh]
+
+
+def layer_rows_batched(w: dict, h_in: np.ndarray, rows, pos, K: np.ndarray, V: np.ndarray,
+                       n_heads: int, eps: float, base: float, key_last=None) -> np.ndarray:
+    """layer_rows with every projection taken as one matrix product over the
+    whole row set and the attention as attend_rows; the normalisation and the
+    rotation stay per row.  Same block, same arguments and effects (fresh K/V
+    written into the slots `pos` before any row attends); the values differ
+    from layer_rows only in the summation order inside the library products.
+    For the 7B shape, where the row-at-a-time form is too slow."""
+    d = h_in.shape[-1]
+    dh = d // n_heads
+    rows, pos = list(rows), list(pos)
+    X = h_in[rows]
+    Xn = np.stack([rmsnorm(x, w["attn_norm"], eps) for x in X])
+    Qp, Kp, Vp = Xn @ w["wq"].T, Xn @ w["wk"].T, Xn @ w["wv"].T
+    Q = np.empty((len(rows), n_heads, dh))
+    for i, p in enumerate(pos):
+        Q[i] = rope_row(Qp[i].reshape(n_heads, dh), p, base)
+        K[p] = rope_row(Kp[i].reshape(n_heads, dh), p, base)
+        V[p] = Vp[i].reshape(n_heads, dh)
+    last = pos if key_last is None else list(key_last)
+    O = attend_rows(Q, last, K, V).reshape(len(rows), d)
+    R = X + O @ w["wo"].T
+    Rn = np.stack([rmsnorm(r, w["ffn_norm"], eps) for r in R])
+    return R + (silu(Rn @ w["wg"].T) * (Rn @ w["wu"].T)) @ w["wd"].T

@@ -25,16 +25,18 @@ Readings (the paper does not fix them):
     rows of the prompt pass and no extra pass runs.
 """
 import numpy as np
+import torch
 
 from .patches import select_static as _select_one
-from .llama import layer_rows, head_row, rmsnorm
+from .llama import layer_rows, layer_rows_batched, head_row, rmsnorm
 from .relevance import text_vision_attention, text_attention_entropy, entropy_permille, relevant_patches
 from .margin import position_margin, reduce_margin, gate_fires
 from .vit import visual_embeddings
 
 
 def _f64(t):
-    return t.detach().to("cpu").float().numpy().astype(np.float64)
+    # exact (bf16 -> float64); torch's CPU conversion runs on all cores
+    return t.detach().to("cpu").to(torch.float64).numpy()
 
 
 def convert_weights(w: dict) -> dict:
@@ -64,8 +66,17 @@ class Layout:
 
 
 class OracleVLA:
-    def __init__(self, cfg, weights):
+    """Alg. 1 over the float64 decoder.  batched=True takes each layer's
+    projections as matrix products over the recomputed rows
+    (layer_rows_batched) instead of one row at a time: the same arithmetic
+    up to the summation order inside the products, fast enough for the 7B
+    shape.  The row-at-a-time default keeps a row's value independent of
+    which other rows a pass computes, so the invariants below hold
+    bit-exactly."""
+
+    def __init__(self, cfg, weights, batched=False):
         self.cfg = cfg
+        self.layer = layer_rows_batched if batched else layer_rows
         self.w = weights if isinstance(weights["embed"], np.ndarray) else convert_weights(weights)
         B, L, d = cfg.batch, cfg.n_layers, cfg.d_model
         self.lay = Layout(cfg)
@@ -180,7 +191,7 @@ class OracleVLA:
                 if l == 0:
                     for p in rows:
                         self.H[0, b, p] = self.embed_row(b, p, frame_t, text_ids, extra_rows)
-                out = layer_rows(self.w["layers"][l], self.H[l, b], rows, rows,
+                out = self.layer(self.w["layers"][l], self.H[l, b], rows, rows,
                                  self.K[l, b], self.V[l, b], cfg.n_heads, cfg.rms_eps, cfg.rope_theta,
                                  self.key_last(rows))
                 if stage2:
@@ -205,7 +216,7 @@ class OracleVLA:
         cfg = self.cfg
         x = self.w["embed"][int(token)][None, :].copy()
         for l in range(cfg.n_layers):
-            x = layer_rows(self.w["layers"][l], x, [0], [pos], self.K[l, b], self.V[l, b],
+            x = self.layer(self.w["layers"][l], x, [0], [pos], self.K[l, b], self.V[l, b],
                            cfg.n_heads, cfg.rms_eps, cfg.rope_theta)
         return head_row(x[0], self.w["final_norm"], self.w["lm_head"], cfg.rms_eps)
 

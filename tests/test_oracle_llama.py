@@ -141,3 +141,64 @@ def test_decode_passes_match_hf_on_extended_sequence():
     ref = out.logits[0].numpy()[o.lay.P - 1:]
     assert ref.shape == logits[0].shape
     assert _rel(logits[0], ref) < 1e-5
+
+
+# ---------------------------------------------------------------- batched mode (7B-shape tests)
+def test_attend_rows_matches_row_form_and_sdpa():
+    """attend_rows against attend_row row by row and against torch's SDPA,
+    causal and with a block of rows that see every key."""
+    rng = np.random.default_rng(5)
+    T, H, dh = 13, 3, 8
+    K, V, Q = rng.normal(size=(T, H, dh)), rng.normal(size=(T, H, dh)), rng.normal(size=(T, H, dh))
+    rows = [0, 2, 3, 7, 12]
+    out = ol.attend_rows(Q[rows], rows, K, V)
+    for i, r in enumerate(rows):
+        assert np.allclose(out[i], ol.attend_row(Q[r], r, K, V), rtol=0, atol=1e-13)
+    ref = torch.nn.functional.scaled_dot_product_attention(
+        torch.from_numpy(Q).permute(1, 0, 2), torch.from_numpy(K).permute(1, 0, 2),
+        torch.from_numpy(V).permute(1, 0, 2), is_causal=True).permute(1, 0, 2).numpy()
+    assert np.allclose(out, ref[rows], atol=1e-12)
+    last = [12, 12, 3]
+    out = ol.attend_rows(Q[[10, 11, 3]], last, K, V)
+    for i, (r, l) in enumerate(zip([10, 11, 3], last)):
+        assert np.allclose(out[i], ol.attend_row(Q[r], l, K, V), rtol=0, atol=1e-13)
+
+
+def test_batched_layer_matches_row_layer_on_a_partial_pass():
+    """layer_rows_batched over a row subset with carried-over K/V equals the
+    row-at-a-time layer (outputs and the fresh K/V slots), and leaves the
+    other slots alone."""
+    cfg = synth.config_c1()
+    w = convert_weights(synth.model_weights(cfg))["layers"][1]
+    rng = np.random.default_rng(6)
+    P, d, H = cfg.prompt_len, cfg.d_model, cfg.n_heads
+    h = rng.normal(size=(P, d))
+    K0, V0 = rng.normal(size=(P, H, d // H)), rng.normal(size=(P, H, d // H))
+    rows = [0] + list(range(5, 40, 3)) + list(range(65, P))
+    Ka, Va, Kb, Vb = K0.copy(), V0.copy(), K0.copy(), V0.copy()
+    a = ol.layer_rows(w, h, rows, rows, Ka, Va, H, cfg.rms_eps, cfg.rope_theta)
+    b = ol.layer_rows_batched(w, h, rows, rows, Kb, Vb, H, cfg.rms_eps, cfg.rope_theta)
+    assert _rel(b, a) < 1e-13
+    assert _rel(Kb, Ka) < 1e-13 and _rel(Vb, Va) < 1e-13
+    keep = [p for p in range(P) if p not in rows]
+    assert np.array_equal(Kb[keep], K0[keep]) and np.array_equal(Vb[keep], V0[keep])
+
+
+def test_batched_oracle_matches_hf_llama():
+    """The batched oracle's full prompt pass and decode passes against
+    Hugging Face's Llama forward over the pinned embeddings."""
+    cfg = synth.config_c1()
+    w = synth.model_weights(cfg)
+    o = OracleVLA(cfg, w, batched=True)
+    si = synth.step_inputs(cfg, 45)
+    o.step_prefill(si["frame_t"].numpy(), si["text_ids"].numpy(), None, None)
+    H0 = o.H[0, 0].copy()
+    tokens, margins, logits = o.decode_actions()
+    m = _hf_model(cfg, w)
+    seq = np.concatenate([H0, o.w["embed"][tokens[0, :-1]]], axis=0)
+    with torch.no_grad():
+        out = m(inputs_embeds=torch.from_numpy(seq[None]), position_ids=torch.arange(seq.shape[0])[None],
+                output_hidden_states=True, use_cache=False)
+    P = o.lay.P
+    assert _rel(o.H[1, 0], out.hidden_states[1][0].numpy()[:P]) < 1e-5
+    assert _rel(logits[0], out.logits[0].numpy()[P - 1:]) < 1e-5

@@ -131,3 +131,54 @@ def test_gate_invalidates_only_fired_episodes():
     o.valid[:] = True
     _, fire = o.margin_gate(0.1, force=[1, 0])
     assert list(fire) == [True, False] and list(o.valid) == [False, True]
+
+
+# ---------------------------------------------------------------- embeddings (Sec. III-A)
+def test_embed_row_single_pixel_closed_form():
+    """A frame that is zero except one pixel: only the embedding of the patch
+    holding it is non-zero, and it equals the patch projection's column for
+    that pixel's place in the patch's H, W, C flattening, times value / 255.
+    Pins the raster order of the patches, the view-major order, the H, W, C
+    flattening within a patch and the 1/255 scaling independently of the
+    oracle's own patch extraction."""
+    cfg = synth.config_c1().with_(n_views=2)
+    w = synth.model_weights(cfg)
+    o = OracleVLA(cfg, w)
+    p, side = cfg.patch, cfg.patches_per_side
+    ids = np.zeros((1, cfg.n_text), dtype=np.int64)
+    W = w["patch_proj"].double().numpy()
+    for (v, y, x, c, val) in [(0, 0, 0, 0, 255), (0, 13, 1, 2, 17), (1, 20, 97, 1, 200), (1, 111, 111, 2, 3)]:
+        frame = np.zeros((1, cfg.n_views, cfg.img, cfg.img, 3), dtype=np.uint8)
+        frame[0, v, y, x, c] = val
+        n_hit = v * side * side + (y // p) * side + x // p
+        col = (y % p) * p * 3 + (x % p) * 3 + c
+        for n in range(cfg.n_patches):
+            e = o.embed_row(0, 1 + n, frame, ids, None)
+            if n == n_hit:
+                assert np.allclose(e, W[:, col] * (val / 255.0), rtol=1e-15, atol=0)
+            else:
+                assert not e.any()
+
+
+def test_embed_rows_of_a_prompt(c1):
+    """Every prompt row at layer 0: visual rows are patchify(frame)/255 times
+    the patch projection (patchify is pinned on its own), text token 0 sits at
+    position 0 and tokens 1.. after the image, given extra rows after the
+    text; the prompt pass stores exactly these rows as H[0]."""
+    cfg = synth.config_c1().with_(n_proprio=1, n_action_q=2)
+    w = synth.model_weights(cfg)
+    si = synth.step_inputs(cfg, 45)
+    frame, ids = si["frame_t"].numpy(), si["text_ids"].numpy()
+    extra = si["extra_rows"].numpy()
+    o = OracleVLA(cfg, w)
+    o.step_prefill(frame, ids, extra, None)
+    N, T = cfg.n_patches, cfg.n_text
+    Wp, E = w["patch_proj"].double().numpy(), w["embed"].double().numpy()
+    vis = op.patchify(frame[0], cfg.patch).astype(np.float64) / 255.0 @ Wp.T
+    H0 = o.H[0, 0]
+    assert np.allclose(H0[1:N + 1], vis, rtol=0, atol=1e-14)
+    assert np.array_equal(H0[0], E[ids[0, 0]])
+    assert np.array_equal(H0[N + 1:N + T], E[ids[0, 1:]])
+    assert np.array_equal(H0[N + T:], extra[0].astype(np.float64))
+    for pos in (0, 1, N, N + 1, N + T):
+        assert np.array_equal(o.embed_row(0, pos, frame, ids, extra), H0[pos])
