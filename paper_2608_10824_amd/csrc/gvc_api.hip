@@ -279,6 +279,7 @@ struct gvc_ctx {
   bool prefill_done = false;
   bool decode_done = false;
   int force_splits = 0;   // GVC_FORCE_SPLITS: waves splitting each GEMM's k range (4 or 8; testing)
+  int big_tw = 0;         // GVC_BIG_TW: tile height of the many-row kernel, 2, 3 or 4 token blocks per wave (testing)
   // prompt-pass projections on the many-row kernel: sessions of at least
   // kBigRows prompt rows (B * P), for every pass of the session, so a row's
   // result never depends on how many rows a pass recomputes; GVC_GEMM=big
@@ -403,6 +404,7 @@ int32_t run_gemm(gvc_ctx* c, GemmArgs& a, int epi, int M, int cls, bool big = fa
   if (big) {
     a.M = M;
     a.mblocks = (M + 15) / 16;
+    a.big_tw = c->big_tw;
     ProfScope ps(c, cls);
     HIP_TRY(launch_gemm_big(a, epi, c->stream));
     return GVC_OK;
@@ -727,7 +729,7 @@ bool setup_persist(gvc_ctx* c) {
   if (mode && strcmp(mode, "legacy") == 0) return false;
   if (p.B != 1 || p.d.parallel_decode || p.D < 2) return false;
   const int d = p.d.d_model, F = p.F;
-  if (d % 256 || d > 8192 || F > 16384 || (p.dh != 64 && p.dh != 128) || F % 16) return false;
+  if (d % 256 || d > 4096 || F > 16384 || (p.dh != 64 && p.dh != 128) || F % 16) return false;
   const size_t u = sizeof(bf16x8);
   auto at = [&](const Packed& m) { return (long long)(m.off / u); };
   const long long qkv_stride = at(p.wk[0]) - at(p.wq[0]), gu_stride = at(p.wu[0]) - at(p.wg[0]);
@@ -750,7 +752,7 @@ bool setup_persist(gvc_ctx* c) {
     return false;
   int act = std::max({d * 4, p.KBf * 32 * 2, p.KBd * 32 * 2, decode_pass_score_offset() + p.kv_pad * 4});
   act = (act + 15) / 16 * 16;
-  const void* f = decode_pass_kernel(p.dh);
+  const void* f = decode_pass_kernel(p.dh, d);
   const size_t lds = decode_pass_lds_bytes(act);
   if (hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess) {
     (void)hipGetLastError();
@@ -770,7 +772,7 @@ bool setup_persist(gvc_ctx* c) {
   a.gains = c->W<float>(p.gains_off);
   a.rope = c->K<float2>(p.rope_off);
   a.x = c->K<float>(p.xdec_off);
-  a.r = c->K<float>(p.r_off);
+  a.racc = c->K<unsigned long long>(p.r_off);   // d int64 accumulators (the region holds Mp >= 16 rows of d floats)
   a.qkv = c->K<float>(p.qkv3_off);
   a.act = c->K<bf16>(p.act_off);
   a.bar = c->K<unsigned>(p.bar_off);
@@ -845,6 +847,7 @@ int32_t gvc_init_cache(const gvc_desc* desc, const gvc_weights* wt, void* weight
   if (const char* fs = getenv("GVC_FORCE_SPLITS")) c->force_splits = atoi(fs);
   c->big_gemm = p.B * p.P >= kBigRows;
   if (const char* sk = getenv("GVC_SK")) c->sk_gemm = atoi(sk) != 0;
+  if (const char* tw = getenv("GVC_BIG_TW")) c->big_tw = atoi(tw);
   if (const char* g = getenv("GVC_GEMM")) {
     if (!strcmp(g, "big")) c->big_gemm = true;
     if (!strcmp(g, "small")) c->big_gemm = false;
@@ -1061,7 +1064,11 @@ int32_t gvc_decode_actions(gvc_ctx* c, int32_t* tokens_out, float* margins_out, 
       hd.e.rows = rows; hd.e.store = lg; hd.e.ld_store = p.V;
       if (c->persist) {
         // all layers in one cooperative launch, then the final norm and the head
-        if (j == 1) HIP_TRY(launch_fill_u32(c->K<uint32_t>(p.bar_off), 0u, kDecodeBarWords, s));
+        if (j == 1) {   // every barrier word but the abort word, which stays set until a gate reports it
+          HIP_TRY(launch_fill_u32(c->K<uint32_t>(p.bar_off), 0u, kDecodeAbortWord, s));
+          HIP_TRY(launch_fill_u32(c->K<uint32_t>(p.bar_off) + kDecodeAbortWord + 1, 0u,
+                                  kDecodeBarWords - kDecodeAbortWord - 1, s));
+        }
         DecodeArgs a = c->dargs;
         a.pos = pos;
         a.bar_base = (unsigned)((j - 1) * decode_grid_barriers(p.L));
@@ -1111,20 +1118,27 @@ int32_t gvc_margin_gate(gvc_ctx* c, float theta, int32_t reduce, float* margin_o
   const Plan& p = c->p;
   float* m = c->K<float>(p.gate_m_off);
   int* f = c->K<int>(p.gate_f_off);
+  // The abort word of the single-launch decode pass stays set from a timed-out
+  // barrier until this gate reports it: the gate kernel then invalidates every
+  // episode instead of deciding on that decode's margins.
+  const bool check_abort = c->persist_ran;
+  uint32_t* abort_dev = c->K<uint32_t>(p.bar_off) + kDecodeAbortWord;
   HIP_TRY(launch_gate(c->S<float>(p.margins_off), p.B, p.D, theta, reduce == GVC_REDUCE_MIN, force,
-                      c->S<int>(p.valid_off), m, f, c->stream));
+                      check_abort ? abort_dev : nullptr, c->S<int>(p.valid_off), m, f, c->stream));
   std::vector<float> hm(p.B);
   std::vector<int> hf(p.B);
   HIP_TRY(hipMemcpyAsync(hm.data(), m, (size_t)p.B * 4, hipMemcpyDeviceToHost, c->stream));
   HIP_TRY(hipMemcpyAsync(hf.data(), f, (size_t)p.B * 4, hipMemcpyDeviceToHost, c->stream));
-  const bool check_abort = c->persist_ran;
   if (check_abort)
-    HIP_TRY(hipMemcpyAsync(&c->abort_word, c->K<uint32_t>(p.bar_off) + kDecodeAbortWord, 4, hipMemcpyDeviceToHost,
-                           c->stream));
+    HIP_TRY(hipMemcpyAsync(&c->abort_word, abort_dev, 4, hipMemcpyDeviceToHost, c->stream));
   HIP_TRY(hipStreamSynchronize(c->stream));
   if (check_abort) {
     c->persist_ran = false;
-    if (c->abort_word) return fail(GVC_EDEVICE, "decode pass: grid barrier timed out");
+    if (c->abort_word) {
+      c->decode_done = false;
+      HIP_TRY(launch_fill_u32(abort_dev, 0u, 1, c->stream));   // reported: later passes may run again
+      return fail(GVC_EDEVICE, "decode pass: grid barrier timed out; every episode's cache was invalidated");
+    }
   }
   for (int b = 0; b < p.B; ++b) {
     if (margin_out) margin_out[b] = hm[b];

@@ -9,9 +9,12 @@ namespace gvc {
 constexpr int kDecodeMaxSeg = 8;       // weight blocks per workgroup per step
 constexpr int kDecodeAbortWord = 512;  // barrier words: abort flag
 constexpr int kDecodeXccWord = 544;    // barrier words: set when a workgroup is not on XCD blockIdx % 8
+constexpr int kDecodePoisonWord = 576; // barrier words: set when a head contribution was not finite
 constexpr int kDecodeHeadWord = 1024;  // barrier words: per-head counters, 32 words apart
 constexpr int kDecodeMaxHeads = 64;
-constexpr int kDecodeBarWords = kDecodeHeadWord + 32 * kDecodeMaxHeads;   // zeroed before a launch sequence
+// zeroed before a launch sequence, except the abort word, which stays set
+// until the gate that follows has reported it
+constexpr int kDecodeBarWords = kDecodeHeadWord + 32 * kDecodeMaxHeads;
 // grid barriers and per-head barriers of one pass over L layers
 constexpr int decode_grid_barriers(int L) { return 1 + 3 * L; }
 constexpr int decode_head_barriers(int L) { return L; }
@@ -26,7 +29,7 @@ struct DecodeArgs {
   const float* gains;          // [L][2][d]: attention norm, FFN norm
   const float2* rope;          // [kv_pad][head_dim/2]
   float* x;                    // [d] layer input / output (in place)
-  float* r;                    // [d] residual after attention
+  unsigned long long* racc;    // [d] sum of the heads' attention-output contributions, int64 in 2^-32 units
   float* qkv;                  // [3d] q, k, v before RoPE
   bf16* act;                   // [F] SwiGLU output
   unsigned* bar;               // kDecodeBarWords barrier words

@@ -71,6 +71,7 @@ struct GemmArgs {
   // part_rows rows per slice; sk_groups weight-block groups per slice
   float* part;
   int sk_slices, sk_steps, sk_groups, part_ld, part_rows;
+  int big_tw;           // many-row kernel: token blocks per wave (2, 3 or 4), 0 = chosen per launch
   EpiArgs e;
 };
 

@@ -19,12 +19,19 @@
 //     slice of the output rows, all on one XCD) each compute the head's
 //     attention over the cache (the new key and value from the raw q, k, v
 //     with RoPE) and multiply it by their slice of W_o's head-h columns,
-//     adding the result into the residual row r (= x, set in step 1) with
-//     device-scope atomic adds.  This takes the attention output's round
-//     trip through memory and one barrier off the critical path; the order
-//     of the head contributions per output is not fixed.
-//  3. Gate/up projection of RMSNorm(r) and SwiGLU; the activation is published.
-//  4. Down projection; x = r + result.
+//     adding the result into an accumulator with device-scope atomic adds.
+//     This takes the attention output's round trip through memory and one
+//     barrier off the critical path.  The accumulator is a 64-bit integer
+//     per output in units of 2^-32: integer addition is associative, so the
+//     sum of the head contributions does not depend on the order in which
+//     the atomics land and the pass is bit-reproducible.  Quantising a
+//     contribution to 2^-32 changes it by at most 2^-33, far below the fp32
+//     rounding of the residual; a contribution that is not finite or
+//     reaches 2^24 in magnitude sets a poison word instead, and the residual
+//     then reads as NaN (the gate fires on a NaN margin).
+//  3. Gate/up projection of RMSNorm(r), r = x + accumulator, and SwiGLU;
+//     the activation is published.
+//  4. Down projection; x = r + result; the accumulator is cleared.
 //
 // Workgroup layout: 8 compute waves and 1 synchronising wave.
 //  * Compute waves stage each step's input into LDS (with the RMSNorm
@@ -36,7 +43,7 @@
 //    weight loads, so its stores and barrier loads never queue behind the
 //    ring in the in-order memory counter.
 //  * Data crossing workgroups is written and read with device-coherent (sc1)
-//    buffer accesses; the barrier and the residual adds use device-scope
+//    buffer accesses; the barrier and the accumulator adds use device-scope
 //    atomics.  No cache write-back or invalidation is needed.
 //
 // Work split over the G workgroups (weights as 16-row blocks, see
@@ -112,6 +119,28 @@ __device__ __forceinline__ void st_f32(rsrc_t r, int off, float v) {
 __device__ __forceinline__ void st_b16(rsrc_t r, int off, bf16 v) {
   __builtin_amdgcn_raw_buffer_store_b16(v, r, off, 0, kSC1);
 }
+__device__ __forceinline__ unsigned long long ld_u64(rsrc_t r, int off) {
+  typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
+  const u32x2 v = __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, kSC1);
+  return (unsigned long long)v.x | ((unsigned long long)v.y << 32);
+}
+__device__ __forceinline__ void st_u64(rsrc_t r, int off, unsigned long long v) {
+  typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
+  __builtin_amdgcn_raw_buffer_store_b64(u32x2{(unsigned)v, (unsigned)(v >> 32)}, r, off, 0, kSC1);
+}
+
+// Fixed-point accumulation of the head contributions (step 2).
+constexpr float kFixScale = 4294967296.0f;   // accumulator units per 1.0 (2^32)
+constexpr float kFixLimit = 16777216.0f;     // contributions must stay below 2^24 in magnitude
+// Residual after attention from the layer input and the accumulator; NaN
+// once a contribution was poisoned.
+__device__ __forceinline__ float res_value(float x, unsigned long long acc, bool poisoned) {
+  const double v = (double)x + (double)(long long)acc * (1.0 / 4294967296.0);
+  return poisoned ? __builtin_nanf("") : (float)v;
+}
+__device__ __forceinline__ bool poisoned_now(const unsigned* bar) {
+  return __hip_atomic_load(bar + kDecodePoisonWord, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u;
+}
 
 #define GP(p) ((const void __attribute__((address_space(1)))*)(p))
 #define LP(p) ((void __attribute__((address_space(3)))*)(p))
@@ -174,25 +203,50 @@ __device__ bool head_sync(const DecodeArgs& a, int h, unsigned n, unsigned k) {
 // beats several with one wave.
 //
 // act[0..n) = bf16(src * gain / rms(src)), src fp32 [n], n % 4 == 0,
-// n <= 8192; act[n..npad) = 0.
-__device__ __forceinline__ void stage_norm(rsrc_t src, const float* __restrict__ gain, int n, int npad, float eps,
-                                           bf16* act, float* wred) {
+// n <= NCH * 4 * 512; act[n..npad) = 0.  With RES, src is the residual
+// after attention: res_value(x, accumulator) with x = src and the
+// accumulator acc.
+template <bool RES, int NCH>
+__device__ __forceinline__ void stage_norm(rsrc_t src, rsrc_t acc, const unsigned* bar, const float* __restrict__ gain,
+                                           int n, int npad, float eps, bf16* act, float* wred) {
   const int tid = threadIdx.x;
   const bool cw = tid < kWaves * 64;
-  float4 y[4];
+  float4 y[NCH];
   float ss = 0.f;
   if (cw) {
     // every load is issued (indices past the end re-read the last chunk, in
     // bounds) before any is used: one memory round trip, not one per chunk
-    float4 v[4], g[4];
+    // (batches of two chunks with RES: 64-bit accumulators take registers)
+    float4 v[NCH], g[NCH];
+    constexpr int BATCH = RES ? 2 : NCH;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int c = min(tid + i * kWaves * 64, n / 4 - 1);
-      v[i] = __builtin_bit_cast(float4, ld_b128(src, c * 16));
-      g[i] = *(const float4*)(gain + c * 4);
+    for (int i0 = 0; i0 < NCH; i0 += BATCH) {
+      u32x4 ac[RES ? 2 * BATCH : 1];
+#pragma unroll
+      for (int i = i0; i < i0 + BATCH; ++i) {
+        const int c = min(tid + i * kWaves * 64, n / 4 - 1);
+        v[i] = __builtin_bit_cast(float4, ld_b128(src, c * 16));
+        g[i] = *(const float4*)(gain + c * 4);
+        if constexpr (RES) {
+          ac[2 * (i - i0)] = ld_b128(acc, c * 32);
+          ac[2 * (i - i0) + 1] = ld_b128(acc, c * 32 + 16);
+        }
+      }
+      if constexpr (RES) {
+        const bool poisoned = poisoned_now(bar);
+        auto u64 = [](unsigned lo, unsigned hi) { return (unsigned long long)lo | ((unsigned long long)hi << 32); };
+#pragma unroll
+        for (int i = i0; i < i0 + BATCH; ++i) {
+          const u32x4 a0 = ac[2 * (i - i0)], a1 = ac[2 * (i - i0) + 1];
+          v[i].x = res_value(v[i].x, u64(a0.x, a0.y), poisoned);
+          v[i].y = res_value(v[i].y, u64(a0.z, a0.w), poisoned);
+          v[i].z = res_value(v[i].z, u64(a1.x, a1.y), poisoned);
+          v[i].w = res_value(v[i].w, u64(a1.z, a1.w), poisoned);
+        }
+      }
     }
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < NCH; ++i) {
       if (tid + i * kWaves * 64 < n / 4) {
         ss += v[i].x * v[i].x + v[i].y * v[i].y + v[i].z * v[i].z + v[i].w * v[i].w;
         y[i] = float4{v[i].x * g[i].x, v[i].y * g[i].y, v[i].z * g[i].z, v[i].w * g[i].w};
@@ -208,7 +262,7 @@ ss = wave_sum(ss);
     for (int w = 0; w < kWaves; ++w) tot += wred[w];
     const float inv = 1.0f / sqrtf(tot / (float)n + eps);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < NCH; ++i) {
       const int c = tid + i * kWaves * 64;
       if (c < n / 4)
         *(u16x4*)(act + c * 4) = u16x4{f2bf(y[i].x * inv), f2bf(y[i].y * inv), f2bf(y[i].z * inv), f2bf(y[i].w * inv)};
@@ -399,7 +453,8 @@ acc = group_sum<CG>(acc);
 
 }  // namespace
 
-template <int DH>
+// NCH: staging chunks of 4 values per compute thread, d <= NCH * 2048.
+template <int DH, int NCH>
 __global__ __launch_bounds__(kThreads) void k_decode_pass(const DecodeArgs a) {
   extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
   u32x4* ring = reinterpret_cast<u32x4*>(lds);                  // [kWaves][kRing][64]
@@ -436,7 +491,7 @@ __global__ __launch_bounds__(kThreads) void k_decode_pass(const DecodeArgs a) {
   const int db0 = gi * nq / G, nseg3 = (gi + 1) * nq / G - db0;           // down blocks (k split)
   const int nsegs = nseg0 + nseg_o + nseg2 + nseg3;   // segments of one layer, in stream order
 
-  const rsrc_t r_x = rsrc(a.x, (size_t)d * 4), r_r = rsrc(a.r, (size_t)d * 4);
+  const rsrc_t r_x = rsrc(a.x, (size_t)d * 4), r_acc = rsrc(a.racc, (size_t)d * 8);
   const rsrc_t r_qkv = rsrc(a.qkv, (size_t)3 * d * 4);
   const rsrc_t r_act = rsrc(a.act, (size_t)F * 2);
 
@@ -544,11 +599,12 @@ __global__ __launch_bounds__(kThreads) void k_decode_pass(const DecodeArgs a) {
     return s_ok != 0;
   };
 
-  // Prologue: r = x for the first layer's step 2; check that this workgroup
-  // runs on XCD blockIdx % 8, which makes each head's workgroups share one L2.
+  // Prologue: clear the accumulator for the first layer's step 2 (each
+  // workgroup its down-projection outputs); check that this workgroup runs
+  // on XCD blockIdx % 8, which makes each head's workgroups share one L2.
   if (syncw) {
     for (int i = lane; i < DH / 2; i += 64) rp[i] = a.rope[(size_t)a.pos * (DH / 2) + i];
-    for (int e = db0 * 16 + lane; e < (db0 + nseg3) * 16; e += 64) st_f32(r_r, e * 4, ld_f32(r_x, e * 4));
+    for (int e = db0 * 16 + lane; e < (db0 + nseg3) * 16; e += 64) st_u64(r_acc, e * 8, 0ull);
     if (lane == 0 && (__builtin_amdgcn_s_getreg((31 << 11) | 20) & 0xf) != (unsigned)(gi & 7))
       __hip_atomic_store(a.bar + kDecodeXccWord, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
@@ -562,7 +618,7 @@ __global__ __launch_bounds__(kThreads) void k_decode_pass(const DecodeArgs a) {
     bf16* const lkc = a.kc + (size_t)l * a.kv_layer_elems;
     bf16* const lvc = a.vc + (size_t)l * a.kv_layer_elems;
     // ---------------- 1. QKV projection (head ah's rows, published to the head's workgroups)
-    stage_norm(r_x, gains + (size_t)l * 2 * d, d, a.KBd * 32, a.eps, act, wred);
+    stage_norm<false, NCH>(r_x, r_x, a.bar, gains + (size_t)l * 2 * d, d, a.KBd * 32, a.eps, act, wred);
     block_sync();
     if (!syncw) run_step(nseg0, nkd, k0d);
     if (syncw && attn && (a.flags & kDecodeWarmKv)) {
@@ -598,21 +654,29 @@ __global__ __launch_bounds__(kThreads) void k_decode_pass(const DecodeArgs a) {
       if (!syncw) run_step(nseg_o, KH, 0);
       block_sync();
       if (syncw) {
+        bool bad = false;
         for (int w = 0; w < kWaves; ++w) {
           const int wb0 = w * nsb / kWaves, wn = (w + 1) * nsb / kWaves - wb0;
           for (int s0 = 0; s0 < wn; s0 += 4) {
             const int s = s0 + (lane >> 4), t = lane & 15;
-            if (s < wn)
-              __hip_atomic_fetch_add(a.r + (sb0 + wb0 + s) * 16 + t, red[(w * kDecodeMaxSeg + s) * 16 + t],
-                                     __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (s < wn) {
+              const float cv = red[(w * kDecodeMaxSeg + s) * 16 + t];
+              if (fabsf(cv) < kFixLimit)
+                __hip_atomic_fetch_add(a.racc + (sb0 + wb0 + s) * 16 + t,
+                                       (unsigned long long)__float2ll_rn(cv * kFixScale), __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_AGENT);
+              else
+                bad = true;
+            }
           }
         }
+        if (bad) __hip_atomic_store(a.bar + kDecodePoisonWord, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       }
     }
     if (!barrier()) break;
 
     // ---------------- 3. gate/up projection + SwiGLU
-    stage_norm(r_r, gains + (size_t)l * 2 * d + d, d, a.KBd * 32, a.eps, act, wred);
+    stage_norm<true, NCH>(r_x, r_acc, a.bar, gains + (size_t)l * 2 * d + d, d, a.KBd * 32, a.eps, act, wred);
     block_sync();
     if (!syncw) run_step(nseg2, nkd, k0d);
     block_sync();
@@ -627,19 +691,22 @@ __global__ __launch_bounds__(kThreads) void k_decode_pass(const DecodeArgs a) {
     }
     if (!barrier()) break;
 
-    // ---------------- 4. down projection + residual; r = x for the next layer's step 2
+    // ---------------- 4. down projection + residual; the accumulator is
+    // cleared for the next layer's step 2 (every workgroup staged r in step 3,
+    // before the last barrier)
     stage_copy(r_act, F, a.KBf * 32, act);
     block_sync();
     if (!syncw) run_step(nseg3, nkf, k0f);
     block_sync();
     if (syncw) {
+      const bool poisoned = poisoned_now(a.bar);
       for (int s0 = 0; s0 < nseg3; s0 += 4) {
         const int s = s0 + (lane >> 4), t = lane & 15;
         if (s < nseg3) {
           const int e = (db0 + s) * 16 + t;
-          const float xn = ld_f32(r_r, e * 4) + sum_partials(red, s, t);
-          st_f32(r_x, e * 4, xn);
-          st_f32(r_r, e * 4, xn);
+          const float rv = res_value(ld_f32(r_x, e * 4), ld_u64(r_acc, e * 8), poisoned);
+          st_f32(r_x, e * 4, rv + sum_partials(red, s, t));
+          st_u64(r_acc, e * 8, 0ull);
         }
       }
     }
@@ -654,14 +721,18 @@ int decode_pass_threads() { return kThreads; }
 
 int decode_pass_score_offset() { return kScoreOffset; }
 
-const void* decode_pass_kernel(int head_dim) {
-  if (head_dim == 128) return reinterpret_cast<const void*>(&k_decode_pass<128>);
-  if (head_dim == 64) return reinterpret_cast<const void*>(&k_decode_pass<64>);
+// d <= 4096: two staging chunks per compute thread (a 4-chunk variant for
+// d <= 8192 would spill registers around the 64-bit accumulator loads;
+// larger models take the per-step launches).
+const void* decode_pass_kernel(int head_dim, int d) {
+  if (d > 2 * 4 * kWaves * 64) return nullptr;
+  if (head_dim == 128) return reinterpret_cast<const void*>(&k_decode_pass<128, 2>);
+  if (head_dim == 64) return reinterpret_cast<const void*>(&k_decode_pass<64, 2>);
   return nullptr;
 }
 
 hipError_t launch_decode_pass(const DecodeArgs& a, int n_wg, hipStream_t s) {
-  const void* f = decode_pass_kernel(a.head_dim);
+  const void* f = decode_pass_kernel(a.head_dim, a.d);
   if (!f) return hipErrorInvalidValue;
   DecodeArgs args = a;
   void* params[] = {&args};

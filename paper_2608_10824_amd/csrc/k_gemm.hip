@@ -548,6 +548,7 @@ static hipError_t launch_big_epi(const GemmArgs& a, hipStream_t s) {
   int tw = 4;
   if (885 * r2 < best) { best = 885 * r2; tw = 2; }
   if (ntiles <= 96 && j2 > cus && 870 * r3 < best) tw = 3;
+  if (a.big_tw >= 2 && a.big_tw <= 4) tw = a.big_tw;   // fixed by the caller (testing)
   if (tw == 3) return launch_big_tw<EPI, 3>(a, s);
   if (tw == 2) return launch_big_tw<EPI, 2>(a, s);
   return launch_big_tw<EPI, 4>(a, s);

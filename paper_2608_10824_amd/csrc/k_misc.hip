@@ -453,9 +453,16 @@ struct Force { signed char f[64]; };
 // the D positions; fire = !(m >= theta) unless forced; a fired episode's
 // cache becomes invalid.
 __global__ void k_gate(const float* __restrict__ margins, int B, int D, float theta, int use_min, Force force,
-                       int* __restrict__ valid, float* __restrict__ m_out, int* __restrict__ fire_out) {
+                       const unsigned* __restrict__ abort_word, int* __restrict__ valid, float* __restrict__ m_out,
+                       int* __restrict__ fire_out) {
   const int b = threadIdx.x;
   if (b >= B) return;
+  if (abort_word && *abort_word) {   // the decode that produced the margins did not finish
+    valid[b] = 0;                    // invalidation is always safe: the next pass is full
+    m_out[b] = __builtin_nanf("");
+    fire_out[b] = 1;
+    return;
+  }
   const float* mr = margins + (size_t)b * D;
   float m;
   if (use_min) {
@@ -555,11 +562,12 @@ hipError_t launch_logits_reduce(const float* logits, int rows, int V, int bin_lo
   return hipGetLastError();
 }
 
-hipError_t launch_gate(const float* margins, int B, int D, float theta, int use_min, const int8_t* force, int* valid,
-                       float* m_out, int* fire_out, hipStream_t s) {
+hipError_t launch_gate(const float* margins, int B, int D, float theta, int use_min, const int8_t* force,
+                       const unsigned* abort_word, int* valid, float* m_out, int* fire_out, hipStream_t s) {
   Force f;
   for (int b = 0; b < 64; ++b) f.f[b] = (force && b < B) ? force[b] : -1;
-  hipLaunchKernelGGL(k_gate, dim3(1), dim3(64), 0, s, margins, B, D, theta, use_min, f, valid, m_out, fire_out);
+  hipLaunchKernelGGL(k_gate, dim3(1), dim3(64), 0, s, margins, B, D, theta, use_min, f, abort_word, valid, m_out,
+                     fire_out);
   return hipGetLastError();
 }
 
