@@ -115,3 +115,17 @@ def check_layer_sampled(cfg, wl, h_in, h_out, K, V, sample_pos):
     sp = list(sample_pos)
     errs = {"k": rel_err(K[sp], Ko[sp]), "v": rel_err(V[sp], Vo[sp]), "out": rel_err(h_out[sp], out)}
     return errs
+
+
+def rel_err_slices(g, o, n_lead) -> float:
+    """Largest per-slice relative error: the arrays are cut into the slices
+    indexed by their first n_lead axes (a row of H, a (row, head) of K or V)
+    and each slice's max |g - o| is divided by that slice's own max |o|, so a
+    wrong low-magnitude row or head cannot hide under the tensor's maximum."""
+    g = np.asarray(g, dtype=np.float64)
+    o = np.asarray(o, dtype=np.float64)
+    lead = int(np.prod(o.shape[:n_lead]))
+    g, o = g.reshape(lead, -1), o.reshape(lead, -1)
+    den = np.abs(o).max(axis=1)
+    den = np.where(den > 0, den, 1.0)
+    return float((np.abs(g - o).max(axis=1) / den).max())

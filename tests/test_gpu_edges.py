@@ -292,8 +292,10 @@ def test_sixteen_episodes_prompt_and_decode():
     2176 prompt rows (the many-row projection kernel) and a batched decode
     whose attention takes one value slice per (head, episode) (16 x 16 = 256
     pairs).  Episodes are independent, so episodes 0 and 15 are checked
-    against a one-episode oracle each: the prompt state, and the decode
-    logits with the oracle fed the GPU's own tokens."""
+    against a one-episode oracle each: the prompt state, and the decode with
+    every GPU episode fed the oracle's greedy tokens (episode 0's where the
+    episode is not checked); the GPU's own argmax tokens and margins against
+    the oracle's."""
     from paper_2608_10824_amd import gvc
     cfg = synth.config_mid().with_(batch=16)
     w = synth.model_weights(cfg)
@@ -302,18 +304,54 @@ def test_sixteen_episodes_prompt_and_decode():
     fp, ids = si["frame_prev"], si["text_ids"]
     s.step_prefill(fp.to(DEV), ids.to(DEV))
     H, K, V, z = _state(s, cfg)
-    tok, mg, lg = s.decode_actions(logits=True)
-    torch.cuda.synchronize()
-    tok, lgn = tok.cpu().numpy(), lg.cpu().numpy()
     one = cfg.with_(batch=1)
+    oracles = {}
     for b in (0, cfg.batch - 1):
         o = OracleVLA(one, w)
         o.step_prefill(fp.numpy()[b:b + 1], ids.numpy()[b:b + 1])
         for l in range(cfg.n_layers + 1):
             assert rel_err(H[l][b:b + 1], o.H[l]) <= TOL, (b, l)
-        _, _, lg_o = o.decode_actions(forced_tokens=tok[b:b + 1])
+        oracles[b] = o.decode_actions()
+    forced = np.repeat(oracles[0][0], cfg.batch, axis=0)
+    forced[cfg.batch - 1] = oracles[cfg.batch - 1][0][0]
+    tok, mg, lg = s.decode_actions(logits=True, forced_tokens=torch.from_numpy(forced.astype(np.int32)).to(DEV))
+    torch.cuda.synchronize()
+    tok, mg, lgn = tok.cpu().numpy(), mg.cpu().numpy(), lg.cpu().numpy()
+    for b, (tok_o, m_o, lg_o) in oracles.items():
         err = rel_err(lgn[b:b + 1], lg_o)
         print("episode %d decode logits rel err %.2e" % (b, err))
         assert err <= TOL
-        check_tokens(tok[b:b + 1], lgn[b:b + 1], tok[b:b + 1], lg_o, cfg.bin_lo)
+        check_tokens(tok[b:b + 1], lgn[b:b + 1], tok_o, lg_o, cfg.bin_lo)
+        check_margins(mg[b:b + 1], m_o, lgn[b:b + 1], lg_o, cfg.bin_lo)
     s.close()
+
+
+def test_many_row_tile_height_does_not_change_a_row():
+    """The many-row kernel sums each row over k in the same order whatever
+    its tile height (128-, 192- or 256-row tiles), so the same 16-episode
+    full and partial steps run with each height forced give bit-identical
+    hidden states, K/V caches and head logits."""
+    import os
+    cfg = synth.config_mid().with_(batch=16)
+    w = synth.model_weights(cfg)
+    si = synth.step_inputs(cfg, 90)
+    ref = None
+    for tw in ("2", "3", "4"):
+        os.environ["GVC_BIG_TW"] = tw
+        try:
+            s = _session(cfg, w)
+        finally:
+            os.environ.pop("GVC_BIG_TW", None)
+        fp, ft, ids = si["frame_prev"].to(DEV), si["frame_t"].to(DEV), si["text_ids"].to(DEV)
+        s.step_prefill(fp, ids)
+        s.decode_actions()
+        s.margin_gate(force=[0] * cfg.batch)
+        mask, _ = s.select_static(ft, fp)
+        s.step_prefill(ft, ids, None, mask)
+        got = _state(s, cfg)
+        s.close()
+        flat = got[0] + got[1] + got[2] + [got[3]]
+        if ref is None:
+            ref = flat
+        else:
+            assert all(np.array_equal(a, b) for a, b in zip(flat, ref)), "tile height %s" % tw
