@@ -226,6 +226,25 @@ int32_t gvc_select_static(gvc_ctx* ctx, const uint8_t* frame_t, const uint8_t* f
                           int32_t tau_num, int32_t tau_den, const int32_t* reuse_permille,
                           uint8_t* reuse_mask, int32_t* n_static);
 
+/* Allocation-free Stage 1 + applied Stage 3 selection, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation) and hold no context.  Same masks and counts
+ * as gvc_select_static with fixed proportions, computed from desc's batch,
+ * n_layers, img, patch and n_views only (the other fields are ignored, but
+ * task_topk and entropy_reuse must be 0: Stages 2 and 3 need a context's last
+ * prompt pass).  frame_t, frame_prev, reuse_permille, reuse_mask and n_static
+ * as in gvc_select_static; stream: a hipStream_t (NULL = the null stream) on
+ * the current GPU, on which the two kernels are enqueued (asynchronous).
+ * Scratch: the per-patch statistics live in a fixed array of 16 x 1024 x 3
+ * int32 (192 KiB) that each GPU holds for the life of the process; calls
+ * that overlap on one GPU (concurrent streams or threads) race on it.
+ * Nothing is allocated.  Errors: GVC_EINVAL (null pointer, bad shape, more
+ * than 16 episodes or 1024 patches per frame, tau or permille out of range,
+ * Stage 2/3 requested), GVC_EDEVICE. */
+int32_t gvc_select_static_noalloc(const gvc_desc* desc, const uint8_t* frame_t, const uint8_t* frame_prev,
+                                  int32_t tau_num, int32_t tau_den, const int32_t* reuse_permille,
+                                  uint8_t* reuse_mask, int32_t* n_static, void* stream);
+
 /* The prompt pass (Alg. 1, full or partial forward).  frame_t: dev uint8
  * [B][n_views][img][img][3]; text_ids: dev int32 [B][n_text] (ids < V);
  * extra_rows: dev fp32 [B][n_proprio + n_action_q][d] given embeddings, or

@@ -971,6 +971,37 @@ int32_t gvc_select_static(gvc_ctx* c, const uint8_t* frame_t, const uint8_t* fra
   return GVC_OK;
 }
 
+int32_t gvc_select_static_noalloc(const gvc_desc* desc, const uint8_t* frame_t, const uint8_t* frame_prev,
+                                  int32_t tau_num, int32_t tau_den, const int32_t* reuse_permille,
+                                  uint8_t* reuse_mask, int32_t* n_static, void* stream) {
+  if (!desc || !frame_t || !frame_prev || !reuse_mask) return fail(GVC_EINVAL, "null argument");
+  const gvc_desc& d = *desc;
+  if (d.batch < 1 || d.n_layers < 1 || d.n_layers > 128) return fail(GVC_EINVAL, "batch >= 1 and n_layers in [1, 128]");
+  if (d.patch < 1 || d.img < d.patch || d.img % d.patch) return fail(GVC_EINVAL, "img must be a multiple of patch");
+  if (d.n_views < 1) return fail(GVC_EINVAL, "n_views must be >= 1");
+  if (d.task_topk != 0 || d.entropy_reuse != 0)
+    return fail(GVC_EINVAL, "Stages 2 and 3 need the previous prompt pass: use gvc_select_static");
+  const long long side = d.img / d.patch, N = (long long)d.n_views * side * side;
+  if (d.batch > kSelectScratchEpisodes || N > kSelectScratchPatches)
+    return fail(GVC_EINVAL, "the allocation-free selection takes at most " + std::to_string(kSelectScratchEpisodes) +
+                                " episodes of " + std::to_string(kSelectScratchPatches) + " patches");
+  if (!(tau_num > 0 && tau_num <= tau_den && tau_den <= (1 << 20)))
+    return fail(GVC_EINVAL, "tau must satisfy 0 < num <= den <= 2^20");
+  std::vector<int> q(d.n_layers, 1000);
+  if (reuse_permille)
+    for (int l = 0; l < d.n_layers; ++l) {
+      if (reuse_permille[l] < 0 || reuse_permille[l] > 1000) return fail(GVC_EINVAL, "permille out of [0, 1000]");
+      q[l] = reuse_permille[l];
+    }
+  int* stats = nullptr;
+  HIP_TRY(select_scratch(&stats));
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  HIP_TRY(launch_patch_stats(frame_t, frame_prev, d.batch, d.n_views, d.img, d.patch, stats, s));
+  HIP_TRY(launch_rank_mask(stats, d.batch, (int)N, d.n_layers, tau_num, tau_den, q.data(), reuse_mask, n_static,
+                           nullptr, 0, 0, nullptr, 0, 0, nullptr, s));
+  return GVC_OK;
+}
+
 int32_t gvc_step_prefill(gvc_ctx* c, const uint8_t* frame_t, const int32_t* text_ids, const float* extra_rows,
                          const uint8_t* reuse_mask) {
   if (!c || !frame_t || !text_ids) return fail(GVC_EINVAL, "null argument");

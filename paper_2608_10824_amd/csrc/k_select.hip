@@ -9,7 +9,16 @@
 // unsigned arithmetic, so the masks are exact.
 #include "gvc_kernels.h"
 
+#include <mutex>
+#include <vector>
+
 namespace gvc {
+
+// Patch statistics of the allocation-free selection (select_scratch): the
+// [B][N][3] int32 buffer between k_patch_stats and k_rank_mask for at most
+// kSelectScratchEpisodes episodes of kSelectScratchPatches patches.  Each GPU
+// the library runs on holds its own copy until the process ends.
+static __device__ __align__(256) int scratch[kSelectScratchEpisodes * kSelectScratchPatches * 3];
 
 // One wave per patch: stats[(b*N + n)*3 + {0,1,2}] = dot, |u|^2, |v|^2.
 __global__ __launch_bounds__(64) void k_patch_stats(const uint8_t* __restrict__ ft, const uint8_t* __restrict__ fp,
@@ -126,6 +135,28 @@ __global__ __launch_bounds__(512) void k_rank_mask(const int* __restrict__ stats
     }
   }
   if (threadIdx.x == 0 && n_static) n_static[b] = S;
+}
+
+// Device address of this GPU's copy of `scratch`, looked up once per device
+// with hipGetSymbolAddress while that device is current (the array's name is
+// a host-side stand-in and must never reach a kernel).
+hipError_t select_scratch(int** out) {
+  static std::mutex mu;
+  static std::vector<int*> ptrs;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  std::lock_guard<std::mutex> lock(mu);
+  if ((int)ptrs.size() <= dev) ptrs.resize(dev + 1, nullptr);
+  if (!ptrs[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    ptrs[dev] = static_cast<int*>(p);
+  }
+  *out = ptrs[dev];
+  return hipSuccess;
 }
 
 hipError_t launch_patch_stats(const uint8_t* ft, const uint8_t* fp, int B, int views, int img, int patch,

@@ -19,7 +19,8 @@ REDUCE_MEAN, REDUCE_MIN = 0, 1
  K_PREFILL_ATTN, K_PREFILL_O, K_PREFILL_GU, K_PREFILL_DOWN, K_PREFILL_HEAD, K_EMBED, K_NORM, K_SELECT,
  K_DECODE_PASS, K_STAGE2, K_VIT) = range(18)
 
-EXPORTED = ("gvc_sizes", "gvc_init_cache", "gvc_select_static", "gvc_step_prefill", "gvc_decode_actions",
+EXPORTED = ("gvc_sizes", "gvc_init_cache", "gvc_select_static", "gvc_select_static_noalloc", "gvc_step_prefill",
+            "gvc_decode_actions",
             "gvc_margin_gate", "gvc_invalidate", "gvc_read_state", "gvc_state_item_bytes", "gvc_profile_begin",
             "gvc_profile_end", "gvc_destroy", "gvc_last_error")
 
@@ -79,6 +80,8 @@ def lib():
         L.gvc_init_cache.argtypes = [ctypes.POINTER(Desc), ctypes.POINTER(Weights), vp, sz, vp, sz, vp, sz, vp,
                                      ctypes.POINTER(vp)]
         L.gvc_select_static.argtypes = [vp, vp, vp, i32, i32, ctypes.POINTER(i32), vp, vp]
+        L.gvc_select_static_noalloc.argtypes = [ctypes.POINTER(Desc), vp, vp, i32, i32, ctypes.POINTER(i32), vp, vp,
+                                                vp]
         L.gvc_step_prefill.argtypes = [vp, vp, vp, vp, vp]
         L.gvc_decode_actions.argtypes = [vp, vp, vp, vp, vp]
         L.gvc_margin_gate.argtypes = [vp, ctypes.c_float, i32, ctypes.POINTER(ctypes.c_float),
@@ -127,6 +130,15 @@ def select_static(ctx: int, frame_t: int, frame_prev: int, tau_num: int, tau_den
     if reuse_permille is not None:
         q = (ctypes.c_int32 * len(reuse_permille))(*[int(v) for v in reuse_permille])
     _check(lib().gvc_select_static(ctx, frame_t, frame_prev, tau_num, tau_den, q, reuse_mask, n_static))
+
+
+def select_static_noalloc(desc: Desc, frame_t: int, frame_prev: int, tau_num: int, tau_den: int, reuse_permille,
+                          reuse_mask: int, n_static: int, stream: int):
+    q = None
+    if reuse_permille is not None:
+        q = (ctypes.c_int32 * len(reuse_permille))(*[int(v) for v in reuse_permille])
+    _check(lib().gvc_select_static_noalloc(ctypes.byref(desc), frame_t, frame_prev, tau_num, tau_den, q, reuse_mask,
+                                           n_static, stream))
 
 
 def step_prefill(ctx: int, frame_t: int, text_ids: int, extra_rows, reuse_mask):

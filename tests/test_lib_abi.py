@@ -87,3 +87,26 @@ def test_null_context_calls_fail_cleanly():
         gvc.invalidate(None, -1)
     with pytest.raises(gvc.GvcError):
         gvc.step_prefill(None, 0, 0, None, None)
+
+
+@pytest.mark.parametrize("field,value", [("img", 462), ("batch", 17), ("batch", 0), ("n_views", 2),
+                                         ("task_topk", 1), ("entropy_reuse", 1), ("patch", 15)])
+def test_noalloc_selection_rejects_sizes_beyond_its_scratch(field, value):
+    """The allocation-free selection validates its sizes on the host before
+    any device work: at most 16 episodes of 1024 patches (here 33^2 = 1089
+    patches, or two views of 1024), no Stage 2 or 3; bad pointers fail the
+    same way (nothing is launched, so this runs without a GPU)."""
+    from paper_2608_10824_amd import gvc
+    from paper_2608_10824_amd.session import desc_from
+    d = desc_from(synth.config_c1().with_(img=448))
+    setattr(d, field, value)
+    with pytest.raises(gvc.GvcError) as e:
+        gvc.select_static_noalloc(d, 256, 256, 99, 100, None, 256, 256, None)
+    assert e.value.code == gvc.GVC_EINVAL and gvc.last_error()
+    d = desc_from(synth.config_c1())
+    with pytest.raises(gvc.GvcError) as e:
+        gvc.select_static_noalloc(d, 256, 256, 99, 100, None, None, 256, None)
+    assert e.value.code == gvc.GVC_EINVAL
+    with pytest.raises(gvc.GvcError) as e:
+        gvc.select_static_noalloc(d, 256, 256, 101, 100, None, 256, 256, None)
+    assert e.value.code == gvc.GVC_EINVAL
