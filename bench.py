@@ -45,6 +45,9 @@ def parse():
     ap.add_argument("--no-c5", action="store_true", help="skip the batch-16 prompt passes")
     ap.add_argument("--no-stage2", action="store_true",
                     help="skip the Stage 2 (top-k = 120) and Stage 2 + entropy Stage 3 steps")
+    ap.add_argument("--no-fired", action="store_true", help="skip the C2 steps whose gate fires (full recompute)")
+    ap.add_argument("--c5-static", default="0,64,128,192,230",
+                    help="static patches per episode of the C5 passes to time (comma-separated)")
     return ap.parse_args()
 
 
@@ -53,45 +56,65 @@ def layer_weight_bytes(cfg):
     return (4 * d * d + 3 * d * F) * 2
 
 
-def cpu_baseline(cfg, w_cpu, si, n_static, min_s=10.0, max_reps=20):
-    """The oracle on a one-layer slice of the same step, repeated until about
-    min_s seconds of CPU work, per-layer time scaled to 32 layers."""
+def _blas_info():
+    """BLAS library and thread count NumPy uses (threadpoolctl's view)."""
+    try:
+        from threadpoolctl import threadpool_info
+        for i in threadpool_info():
+            if i.get("user_api") == "blas":
+                return {"blas": "%s %s" % (i.get("internal_api"), i.get("version")), "blas_threads": i.get("num_threads")}
+    except Exception:   # pragma: no cover - threadpoolctl missing
+        pass
+    return {"blas": "unknown", "blas_threads": None}
+
+
+def cpu_baseline(cfg, oracle, si):
+    """The oracle timed over one whole C2 control step on the host cores:
+    Stage 1, the 148-row partial prompt pass through all 32 layers, the 6
+    single-token decode passes and the gate, after an untimed full step that
+    fills its cache (its batched float64 mode, the one the 7B parity tests
+    use).  Also the tiny C1 control step with BLAS on every core and on one
+    thread, for scale."""
     import numpy as np
+    from threadpoolctl import threadpool_limits
     from oracle.vla import OracleVLA
-    from oracle.llama import head_row
-    cfg1 = cfg.with_(n_layers=1)
-    o = OracleVLA(cfg1, w_cpu)
-    ft, fp = si["frame_t"].numpy(), si["frame_prev"].numpy()
-    ids = si["text_ids"].numpy()
-    t_sel = t_slice = t_head = 0.0
-    reps = 0
-    t_all = time.perf_counter()
-    while reps < max_reps and (reps == 0 or time.perf_counter() - t_all < min_s):
-        t0 = time.perf_counter()
-        masks, ns = o.select_static(ft, fp)
-        t_sel += time.perf_counter() - t0
-        o.valid[:] = True
-        t0 = time.perf_counter()
-        o.step_prefill(ft, ids, None, masks)
-        o.decode_actions()
-        t_slice += time.perf_counter() - t0
-        t0 = time.perf_counter()
-        for _ in range(cfg.n_decode):
-            head_row(o.H[1, 0, cfg.prompt_len - 1], o.w["final_norm"], o.w["lm_head"], cfg.rms_eps)
-        t_head += time.perf_counter() - t0
-        reps += 1
-    t_sel, t_slice, t_head = t_sel / reps, t_slice / reps, t_head / reps
-    t_step = t_sel + cfg.n_layers * (t_slice - t_head) + t_head
+    import synth
+    ft, fp, ids = si["frame_t"].numpy(), si["frame_prev"].numpy(), si["text_ids"].numpy()
+    t0 = time.perf_counter()
+    oracle.step_prefill(fp, ids)
+    oracle.decode_actions()
+    t_full = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    oracle.margin_gate(force=[0])
+    masks, _ = oracle.select_static(ft, fp)
+    oracle.step_prefill(ft, ids, None, masks)
+    oracle.decode_actions()
+    t_step = time.perf_counter() - t0
+    c1 = synth.config_c1()
+    o1 = OracleVLA(c1, synth.model_weights(c1))
+    s1 = synth.step_inputs(c1, 45)
+    o1.step_prefill(s1["frame_prev"].numpy(), s1["text_ids"].numpy())
+    o1.decode_actions()
+
+    def c1_step():
+        t = time.perf_counter()
+        o1.margin_gate(force=[0])
+        m1, _ = o1.select_static(s1["frame_t"].numpy(), s1["frame_prev"].numpy())
+        o1.step_prefill(s1["frame_t"].numpy(), s1["text_ids"].numpy(), None, m1)
+        o1.decode_actions()
+        return time.perf_counter() - t
+
+    c1_all = min(c1_step() for _ in range(3))
+    with threadpool_limits(limits=1, user_api="blas"):
+        c1_one = min(c1_step() for _ in range(3))
     cores = len(os.sched_getaffinity(0))
-    omp = os.environ.get("OMP_NUM_THREADS")
-    if omp and omp.isdigit():
-        cores = min(cores, int(omp))
+    info = _blas_info()
     return {"value": 1.0 / t_step, "unit": "control steps/s", "cores": cores, "kind": "oracle",
-            "sample": "float64 oracle on 1 of the 32 decoder layers (Stage 1, the prompt pass over the %d "
-                      "recomputed rows, the 6 single-token decode passes and the 7 LM-head rows), run %d times "
-                      "(%.1f s of CPU work); per-layer time scaled to 32 layers"
-                      % (int(o.recomputed[0, 0]), reps, time.perf_counter() - t_all),
-            "seconds_per_step": t_step}
+            "sample": "one whole C2 control step of the float64 oracle in its batched mode (Stage 1, the 148-row "
+                      "partial prompt pass through 32 layers, 6 single-token decode passes, the gate; %.1f s) after "
+                      "an untimed full step (%.1f s) that fills its cache" % (t_step, t_full),
+            "seconds_per_step": t_step, "full_step_s": t_full, **info,
+            "c1_ms_per_step_all_threads": c1_all * 1e3, "c1_ms_per_step_one_thread": c1_one * 1e3}
 
 
 def c3_episode(dev):
@@ -116,27 +139,57 @@ def c3_episode(dev):
     s.step_prefill(frames[0:1], ids)
     s.decode_actions()
     n = frames.shape[0]
-    fired, rows = [], []
+    stream = s.stream
+
+    def run(trace):
+        """Steps 1..n-1 with the gate applied; with trace, a record per step
+        (and a synchronisation per step to read the static count and rows)."""
+        fired, rows, out = [], [], []
+        for t in range(1, n):
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)] if trace else None
+            if ev:
+                ev[0].record(stream)
+            m, fire = s.margin_gate()
+            fired.append(bool(fire[0]))
+            mask, n_static = s.select_static(frames[t:t + 1], frames[t - 1:t])
+            if ev:
+                ev[1].record(stream)
+            s.step_prefill(frames[t:t + 1], ids, None, mask)
+            if ev:
+                ev[2].record(stream)
+            s.decode_actions()
+            if ev:
+                ev[3].record(stream)
+                torch.cuda.synchronize()
+                r = s.read(gvc.STATE_ROWS).cpu().tolist()
+                rows.append(r)
+                out.append({"step": t, "fired": bool(fire[0]), "margin_prev": round(float(m[0]), 6),
+                            "static": int(n_static[0].item()), "rows_per_layer": r,
+                            "us_gate_select": round(ev[0].elapsed_time(ev[1]) * 1e3, 1),
+                            "us_prefill": round(ev[1].elapsed_time(ev[2]) * 1e3, 1),
+                            "us_decode": round(ev[2].elapsed_time(ev[3]) * 1e3, 1)})
+            if t % 10 == 0:
+                note("C3 frame %d of %d%s" % (t, n - 1, " (trace)" if trace else ""))
+        return fired, rows, out
+
+    # timed episode (no per-step synchronisation), then the same episode traced
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for t in range(1, n):
-        _, fire = s.margin_gate()
-        fired.append(bool(fire[0]))
-        mask, _ = s.select_static(frames[t:t + 1], frames[t - 1:t])
-        s.step_prefill(frames[t:t + 1], ids, None, mask)
-        s.decode_actions()
-        rows.append(s.read(gvc.STATE_ROWS).cpu().tolist())
-        if t % 10 == 0:
-            note("C3 frame %d of %d" % (t, n - 1))
+    fired, _, _ = run(False)
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
+    s.invalidate()
+    s.step_prefill(frames[0:1], ids)
+    s.decode_actions()
+    fired2, rows, trace = run(True)
     s.close()
     L = cfg.n_layers
     return {"frames": n, "gated_steps": n - 1, "fired": sum(fired), "recompute_rate": sum(fired) / (n - 1),
+            "traced_run_same_decisions": fired == fired2,
             "mean_recomputed_rows_per_layer": sum(sum(r) for r in rows) / (len(rows) * L),
             "prompt_len": cfg.prompt_len, "ms_per_step": dt * 1e3 / (n - 1),
             "reuse_permille": "%d -> %d over the layers" % (cfg.permille()[0], cfg.permille()[-1]),
-            "tau": "%d/%d" % cfg.tau, "theta": cfg.theta}
+            "tau": "%d/%d" % cfg.tau, "theta": cfg.theta, "trace": trace}
 
 
 def c4_chunk(dev, steps, warmup):
@@ -208,6 +261,7 @@ def c5_prefill(dev, reps, ks=(0, 64, 128, 192, 230)):
     d, F, V, L, P, B = cfg.d_model, cfg.ffn, cfg.vocab, cfg.n_layers, cfg.prompt_len, cfg.batch
     out = []
     for k in ks:
+        note("C5 k=%d: full step, then %d timed partial passes" % (k, reps))
         si = synth.step_inputs(cfg, k, stream=k + 1)
         fp, ft = si["frame_prev"].to(dev), si["frame_t"].to(dev)
         ids = si["text_ids"].to(dev)
@@ -351,6 +405,45 @@ def staged_steps(cfg, w, si, dev, steps, warmup, entropy=False):
     return out
 
 
+def fired_steps(s, cfg, si, dev, steps):
+    """C2 control steps whose gate fires (Alg. 1, invalidate branch): the
+    cache is invalidated, so the prompt pass recomputes all 276 rows, then
+    the 7-token decode.  Reports the time per control step and the full
+    prompt pass's time, TFLOP/s and MFMA utilisation."""
+    import torch
+    from paper_2608_10824_amd import gvc
+    d, F, V, L, P = cfg.d_model, cfg.ffn, cfg.vocab, cfg.n_layers, cfg.prompt_len
+    fp, ft, ids = si["frame_prev"].to(dev), si["frame_t"].to(dev), si["text_ids"].to(dev)
+    stream = s.stream
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(steps)]
+
+    def step(ev=None):
+        s.margin_gate(force=[1])                # the gate fires: the next pass is full
+        mask, _ = s.select_static(ft, fp)
+        if ev:
+            ev[0].record(stream)
+        s.step_prefill(ft, ids, None, mask)
+        if ev:
+            ev[1].record(stream)
+        s.decode_actions()
+
+    step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        step(evs[i])
+    torch.cuda.synchronize()
+    dt = (time.perf_counter() - t0) / steps
+    rows = s.read(gvc.STATE_ROWS).cpu().tolist()
+    pms = sum(e[0].elapsed_time(e[1]) for e in evs) / steps
+    flops = 2 * V * d + L * (2 * P * (4 * d * d + 3 * d * F) + 2 * sum(2 * (p + 1) * d for p in range(P)))
+    tf = flops / (pms / 1e3) / 1e12
+    return {"ms_per_step": dt * 1e3, "control_steps_per_s": 1.0 / dt, "recomputed_rows_per_layer": rows[0],
+            "prefill_ms": pms, "prefill_tflops": tf, "prefill_mfma_util_pct": 100.0 * tf / BF16_PEAK_TFLOPS,
+            "prefill_hbm_frac": (L * layer_weight_bytes(cfg) + V * d * 2) / (pms / 1e3) / 1e9 / HBM_PEAK_GBS,
+            "steps": steps}
+
+
 def stored_traffic(kernel_sources):
     """HBM bytes per launch of the dominant kernel from the committed rocprofv3
     counter summary, or None when the kernel sources changed since."""
@@ -393,10 +486,11 @@ def main():
     si = synth.step_inputs(cfg, n_static)
     note("weights and inputs generated")
     w_stage2 = w if not args.no_stage2 else None
-    w_cpu = None
-    if not args.no_cpu_baseline:
-        w_cpu = {k: v.cpu() for k, v in w.items() if k != "layers"}
-        w_cpu["layers"] = [{k: v.cpu() for k, v in w["layers"][0].items()}]
+    oracle = None
+    if not args.no_cpu_baseline:   # float64 host copy for the oracle's timed step (test infrastructure)
+        from oracle.vla import OracleVLA
+        oracle = OracleVLA(cfg, w, batched=True)
+        note("oracle weights converted to float64 on the host")
     s = Session(cfg, w, device=dev)
     torch.cuda.synchronize()
     del w
@@ -512,13 +606,16 @@ def main():
                      "bytes_per_launch": dk_bytes, "avg_launch_us": dk_avg_s * 1e6, "launches": dk_n,
                      "region_ms_per_step": dt2 * 1e3 / args.steps},
     }
-    if not args.no_cpu_baseline:
-        cb = cpu_baseline(cfg, w_cpu, si, n_static)
-        out["cpu_baseline"] = cb
-        note("cpu baseline done")
+    if not args.no_fired:
+        out["c2_fired"] = fired_steps(s, cfg, si, dev, min(args.steps, 10))
+        note("C2 fired steps done: %.2f ms per step" % out["c2_fired"]["ms_per_step"])
     s.close()
     del s
     torch.cuda.empty_cache()
+    if oracle is not None:
+        out["cpu_baseline"] = cpu_baseline(cfg, oracle, si)
+        del oracle
+        note("cpu baseline done")
     if w_stage2 is not None:
         out["stage2"] = staged_steps(cfg, w_stage2, si, dev, min(args.steps, 10), 2)
         note("Stage 2 steps done: %d static patches left" % out["stage2"]["static_patches"])
@@ -527,7 +624,8 @@ def main():
         del w_stage2
         torch.cuda.empty_cache()
     if not args.no_c5:
-        out["c5_prefill"] = c5_prefill(dev, min(args.steps, 5))
+        ks = tuple(int(k) for k in args.c5_static.split(",") if k.strip())
+        out["c5_prefill"] = c5_prefill(dev, min(args.steps, 5), ks)
     if not args.no_vit:
         out["c2_vit"] = vit_steps(dev, min(args.steps, 10), 2)
         note("C2 + ViT steps done: %.2f ms per step" % out["c2_vit"]["ms_per_step"])
@@ -537,7 +635,11 @@ def main():
     if not args.no_c3:
         out["c3"] = c3_episode(dev)
         note("C3 episode done: recompute rate %.3f" % out["c3"]["recompute_rate"])
-    print(json.dumps(out))
+    # explicit teardown before the interpreter exits: every session is closed
+    # above; wait for the device, then return the cached blocks
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    print(json.dumps(out), flush=True)
     return 0
 
 
