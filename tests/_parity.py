@@ -129,3 +129,74 @@ def rel_err_slices(g, o, n_lead) -> float:
     den = np.abs(o).max(axis=1)
     den = np.where(den > 0, den, 1.0)
     return float((np.abs(g - o).max(axis=1) / den).max())
+
+
+# ---------------------------------------------------------------- Stage 2 / 3 decisions
+# The selection turns floating-point signals into integers (which patches
+# are task-relevant, each layer's per-mille proportion).  Both sides take
+# those decisions in the kernel's precision: the oracle's own float64
+# signals go through the same fp32 steps the GPU applies to its signals.
+# The two decisions may differ only where the oracle's value lies within the
+# measured signal error of a decision boundary (several answers are correct).
+
+def fp32_scores(tv):
+    """Per-patch Stage 2 scores [B][N] as the kernel forms them: fp32 sums
+    over the (layer, head) columns of tv [B][L][H][N], in order."""
+    B, L, H, N = tv.shape
+    flat = np.asarray(tv).reshape(B, L * H, N).astype(np.float32)
+    acc = np.zeros((B, N), dtype=np.float32)
+    for c in range(L * H):
+        acc = (acc + flat[:, c, :]).astype(np.float32)
+    return acc
+
+
+def fp32_layer_q(ent, n_instr):
+    """Stage 3 per-layer proportions from ent [L][H], taking the kernel's fp32
+    steps in its order: E_l summed over heads, u_l = 1 - E_l / (H n_instr),
+    s_l = s_{l-1} + (u_l - s_{l-1}) / 2, q_l = floor(1000 clamp(s_l))."""
+    f = np.float32
+    L, H = ent.shape
+    out, sl = [], f(0)
+    for l in range(L):
+        e = f(0)
+        for h in range(H):
+            e = f(e + f(ent[l, h]))
+        u = f(f(1) - f(e / f(H * n_instr)))
+        sl = u if l == 0 else f(sl + f(f(u - sl) * f(0.5)))
+        c = min(max(sl, f(0)), f(1))
+        out.append(int(np.floor(f(f(1000) * c))))
+    return out
+
+
+def layer_q_near_ties(ent_o, ent_g, n_instr, q_o, q_g):
+    """Layers whose proportions differ; each must be a near tie: the oracle's
+    1000 s_l within 1000 max|dE| (+1e-3 for fp32 rounding) of the boundary
+    between the two values (s_l is a convex mix of the u_j, so its error is at
+    most max|dE|)."""
+    L, H = ent_o.shape
+    dE = np.abs(np.asarray(ent_g, np.float64).sum(axis=1) - np.asarray(ent_o).sum(axis=1)).max() / (H * n_instr)
+    s, out = 0.0, []
+    for l in range(L):
+        u = 1.0 - ent_o[l].sum() / (H * n_instr)
+        s = u if l == 0 else s + (u - s) / 2
+        if q_o[l] != q_g[l]:
+            boundary = max(q_o[l], q_g[l])
+            assert abs(q_o[l] - q_g[l]) == 1 and abs(1000 * min(max(s, 0.0), 1.0) - boundary) <= 1000 * dE + 1e-3, \
+                "layer %d proportion %d vs %d beyond the signal error" % (l, q_o[l], q_g[l])
+            out.append(l)
+    return out
+
+
+def relevant_near_ties(score_o, score_g, k, rel_o, rel_g):
+    """Patches selected as task-relevant by one side only; each must sit
+    within twice the measured score error of the k-th / (k+1)-th boundary of
+    the oracle's scores."""
+    diff = np.nonzero(rel_o != rel_g)[0]
+    if len(diff) == 0:
+        return []
+    eps = np.abs(np.asarray(score_g, np.float64) - np.asarray(score_o, np.float64)).max()
+    srt = np.sort(np.asarray(score_o, np.float64))[::-1]
+    lo, hi = srt[min(k, len(srt) - 1)], srt[k - 1]
+    for n in diff:
+        assert lo - 2 * eps <= score_o[n] <= hi + 2 * eps, "patch %d selected beyond the score error" % n
+    return diff.tolist()

@@ -216,6 +216,54 @@ def test_c2v_front_end_full_and_partial_step_every_element():
     s.close()
 
 
+def test_c2_stage2_stage3_every_element():
+    """The benchmark's Stage 2 (k = 120) + Stage 3 (entropy) configuration:
+    after the full step, the recorded signals of every layer and head
+    against the oracle's own; each side's selection on its own signal
+    (decided in fp32 on both sides; equal except for near ties); then the
+    partial step on the (equal) masks, every element."""
+    from paper_2608_10824_amd import gvc
+    from oracle.relevance import relevant_patches
+    from tests._parity import fp32_scores, fp32_layer_q, layer_q_near_ties, relevant_near_ties
+    cfg = synth.config_c2().with_(task_topk=120, entropy_reuse=True)
+    o, s = _pair(cfg)
+    si = synth.step_inputs(cfg, 128)
+    fp, ft, ids = si["frame_prev"].numpy(), si["frame_t"].numpy(), si["text_ids"].numpy()
+    o.step_prefill(fp, ids)
+    s.step_prefill(si["frame_prev"].to(DEV), si["text_ids"].to(DEV))
+    tv, ent = s.read(gvc.STATE_TV).cpu().numpy(), s.read(gvc.STATE_ENTROPY).cpu().numpy()
+    e_tv, e_ent = rel_err(tv, o.tv), rel_err(ent, o.ent)
+    e_tv_s = rel_err_slices(tv, o.tv, 3)   # per (layer, head)
+    print("signals: attention %.2e (per layer and head %.2e), entropy %.2e" % (e_tv, e_tv_s, e_ent))
+    print("attention signal error per layer 0, 1, 2, 4, 8, 16, 31: %s; layer-input error: %s" % (
+        " ".join("%.1e" % rel_err(tv[0, l], o.tv[0, l]) for l in (0, 1, 2, 4, 8, 16, 31)),
+        " ".join("%.1e" % rel_err(s.read(gvc.STATE_H, l).cpu().numpy()[0], o.H[l, 0]) for l in (0, 1, 2, 4, 8, 16, 31))))
+    # The attention signal is a softmax over products of two projections of
+    # the layer input, so its relative error is about twice that input's:
+    # 3e-3 at layer 0 (exact input) and up to ~2.7e-2 where the 32-layer bf16
+    # error of the input is ~1.5e-2; hence twice the state tolerances.
+    assert e_tv <= 2 * TOL and e_ent <= TOL and e_tv_s <= 2 * TOL_SLICE
+    n_instr = cfg.n_text - 1
+    mask_g, n_g = s.select_static(si["frame_t"].to(DEV), si["frame_prev"].to(DEV))
+    q_g = s.read(gvc.STATE_LAYER_Q).cpu().numpy()[0].tolist()
+    q_o = fp32_layer_q(o.ent[0], n_instr)
+    q_ties = layer_q_near_ties(o.ent[0], ent[0], n_instr, q_o, q_g)
+    sc_o, sc_g = fp32_scores(o.tv)[0].astype(np.float64), fp32_scores(tv)[0].astype(np.float64)
+    r_ties = relevant_near_ties(sc_o, sc_g, 120, relevant_patches(sc_o, 120), relevant_patches(sc_g, 120))
+    masks, n_o = o.select_static(ft, fp, scores=sc_o[None], layer_q=[q_o])
+    print("proportions %s..., static after Stage 2: %d; near ties: %d layers, %d patches"
+          % (q_o[:4], n_o[0], len(q_ties), len(r_ties)))
+    if not (q_ties or r_ties):
+        assert np.array_equal(mask_g.cpu().numpy().astype(bool), masks) and n_g.cpu().tolist() == n_o.tolist()
+    # the oracle's selection decides; the GPU's partial step takes its masks
+    o.step_prefill(ft, ids, None, masks)
+    s.step_prefill(si["frame_t"].to(DEV), si["text_ids"].to(DEV), None,
+                   torch.from_numpy(masks.astype(np.uint8)).to(DEV))
+    assert s.read(gvc.STATE_ROWS).cpu().tolist() == o.recomputed[0].tolist()
+    _compare_state(s, o, 0, "C2 Stage 2+3 partial step")
+    s.close()
+
+
 # Steps 1..C3_STEPS of the moving-rectangle episode; the gate decisions on
 # them include a fired and a kept step.
 C3_STEPS = 6
