@@ -602,7 +602,7 @@ def main():
         "gate_fired_steps": sum(fired),
         "roofline": {"bound": "hbm", "achieved": dk_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": dk_gbs / HBM_PEAK_GBS, "traffic": traffic,
-                     "kernel": "k_decode_pass<128> (one decode pass over all 32 layers, cooperative grid)",
+                     "kernel": "k_decode_pass<128, 2> (one decode pass over all 32 layers, cooperative grid)",
                      "bytes_per_launch": dk_bytes, "avg_launch_us": dk_avg_s * 1e6, "launches": dk_n,
                      "region_ms_per_step": dt2 * 1e3 / args.steps},
     }
