@@ -46,6 +46,8 @@ def parse():
     ap.add_argument("--no-stage2", action="store_true",
                     help="skip the Stage 2 (top-k = 120) and Stage 2 + entropy Stage 3 steps")
     ap.add_argument("--no-fired", action="store_true", help="skip the C2 steps whose gate fires (full recompute)")
+    ap.add_argument("--trace-jsonl", default="",
+                    help="also write the C3 episode's per-step trace to this file, one JSON object per line")
     ap.add_argument("--c5-static", default="0,64,128,192,230",
                     help="static patches per episode of the C5 passes to time (comma-separated)")
     return ap.parse_args()
@@ -635,6 +637,11 @@ def main():
     if not args.no_c3:
         out["c3"] = c3_episode(dev)
         note("C3 episode done: recompute rate %.3f" % out["c3"]["recompute_rate"])
+        if args.trace_jsonl:
+            with open(args.trace_jsonl, "w") as f:
+                for rec in out["c3"]["trace"]:
+                    f.write(json.dumps(rec) + "\n")
+            note("C3 trace written to %s" % args.trace_jsonl)
     # explicit teardown before the interpreter exits: every session is closed
     # above; wait for the device, then return the cached blocks
     torch.cuda.synchronize()

@@ -294,6 +294,23 @@ int32_t gvc_read_state(gvc_ctx* ctx, int32_t item, int32_t layer, void* dst, siz
 /* Size in bytes of a state item (see gvc_read_state). */
 size_t gvc_state_item_bytes(const gvc_ctx* ctx, int32_t item);
 
+/* Host-side check of the compacted row lists of a prompt pass (Alg. 1,
+ * partial forward pass: which rows each layer recomputes).  Row r = b*P + pos
+ * is recomputed at layer l unless valid[b] != 0, mask != NULL, 1 <= pos <= N
+ * and mask[(b*L + l)*N + pos - 1] != 0.  All pointers are host memory:
+ * mask uint8 [B][L][N] or NULL; valid int32 [B]; rows int32 [L][3][B*P]
+ * (per layer the row index b*P + pos, the episode b and the position pos of
+ * each recomputed row, in increasing row order); counts int32 [L];
+ * ep_counts, ep_offsets int32 [L][B] (rows of episode b and the index of its
+ * first row in the layer's list).  Returns GVC_OK when every list, count and
+ * per-episode entry is exactly what the rule gives; otherwise GVC_EINVAL with
+ * the first difference in gvc_last_error.  With GVC_VALIDATE=1 in the
+ * environment at gvc_init_cache, gvc_step_prefill copies its lists to the host
+ * and runs this check (GVC_EDEVICE on a difference). */
+int32_t gvc_check_rows(int32_t B, int32_t L, int32_t N, int32_t P, const uint8_t* mask, const int32_t* valid,
+                       const int32_t* rows, const int32_t* counts, const int32_t* ep_counts,
+                       const int32_t* ep_offsets);
+
 /* Kernel classes for gvc_profile_begin: the launches of one class are
  * bracketed by HIP events on the context's stream. */
 enum gvc_kernel_class {

@@ -280,6 +280,9 @@ struct gvc_ctx {
   bool decode_done = false;
   int force_splits = 0;   // GVC_FORCE_SPLITS: waves splitting each GEMM's k range (4 or 8; testing)
   int big_tw = 0;         // GVC_BIG_TW: tile height of the many-row kernel, 2, 3 or 4 token blocks per wave (testing)
+  bool poison = false;    // GVC_POISON: arenas start as 0xFF bytes instead of zeros (testing)
+  int validate = 0;       // GVC_VALIDATE: 1 = every prompt pass checks its row lists on the host, 2 = also
+                          // alters the host copy first, so the check must fail (tests that it runs)
   // prompt-pass projections on the many-row kernel: sessions of at least
   // kBigRows prompt rows (B * P), for every pass of the session, so a row's
   // result never depends on how many rows a pass recomputes; GVC_GEMM=big
@@ -852,8 +855,29 @@ int32_t gvc_init_cache(const gvc_desc* desc, const gvc_weights* wt, void* weight
     if (!strcmp(g, "big")) c->big_gemm = true;
     if (!strcmp(g, "small")) c->big_gemm = false;
   }
-  INIT_TRY(launch_fill_u32(reinterpret_cast<uint32_t*>(c->st), 0u, p.state_bytes / 4, s));
-  INIT_TRY(launch_fill_u32(reinterpret_cast<uint32_t*>(c->ws), 0u, p.ws_bytes / 4, s));
+  // GVC_POISON=1 (testing): every state and workspace byte starts as 0xFF
+  // (NaN in fp32 and bf16, -1 in int32) instead of 0, except what the library
+  // relies on starting at zero: the cache-valid flags, the decode barrier
+  // words, the key/value positions past the prompt (the prompt attention's
+  // last key tile reads them with zero weight) and, when the FFN width is not
+  // a multiple of 32, the activation fragments' padding columns.  A step that
+  // reads anything else before writing it then yields NaN.
+  if (const char* pz = getenv("GVC_POISON")) c->poison = atoi(pz) != 0;
+  if (const char* va = getenv("GVC_VALIDATE")) c->validate = atoi(va);
+  const uint32_t fill = c->poison ? 0xFFFFFFFFu : 0u;
+  INIT_TRY(launch_fill_u32(reinterpret_cast<uint32_t*>(c->st), fill, p.state_bytes / 4, s));
+  INIT_TRY(launch_fill_u32(reinterpret_cast<uint32_t*>(c->ws), fill, p.ws_bytes / 4, s));
+  if (c->poison) {
+    INIT_TRY(launch_fill_u32(c->S<uint32_t>(p.valid_off), 0u, p.B, s));
+    INIT_TRY(launch_fill_u32(c->K<uint32_t>(p.bar_off), 0u, kDecodeBarWords, s));
+    INIT_TRY(launch_zero_kv_tail(c->S<bf16>(p.K_off), c->S<bf16>(p.V_off), (size_t)p.L * p.B * p.H, p.kv_pad, p.dh,
+                                 p.P, s));
+    if (p.d.ffn % 32)
+      INIT_TRY(launch_fill_u32(c->K<uint32_t>(p.act_off), 0u, (size_t)p.Mp * p.KBf * 32 / 2, s));
+    if (p.vit)
+      INIT_TRY(launch_zero_kv_tail(c->K<bf16>(p.vk_off), c->K<bf16>(p.vv_off), (size_t)p.E * p.Hv, p.kvpad_v, p.dhv,
+                                   p.Sv, s));
+  }
   for (int l = 0; l < p.L; ++l) {
     const gvc_layer_weights& lw = wt->layers[l];
     const Packed* mats[7] = {&p.wq[l], &p.wk[l], &p.wv[l], &p.wo[l], &p.wg[l], &p.wu[l], &p.wd[l]};
@@ -1002,6 +1026,44 @@ int32_t gvc_select_static_noalloc(const gvc_desc* desc, const uint8_t* frame_t, 
   return GVC_OK;
 }
 
+int32_t gvc_check_rows(int32_t B, int32_t L, int32_t N, int32_t P, const uint8_t* mask, const int32_t* valid,
+                       const int32_t* rows, const int32_t* counts, const int32_t* ep_counts,
+                       const int32_t* ep_offsets) {
+  if (B < 1 || L < 1 || N < 0 || P < 1 || N >= P) return fail(GVC_EINVAL, "bad shape");
+  if (!valid || !rows || !counts || !ep_counts || !ep_offsets) return fail(GVC_EINVAL, "null argument");
+  const size_t tot = (size_t)B * P;
+  for (int l = 0; l < L; ++l) {
+    const int32_t* idx = rows + (size_t)l * 3 * tot;
+    const int32_t* ep = idx + tot;
+    const int32_t* pos = ep + tot;
+    auto bad = [&](const std::string& what) {
+      return fail(GVC_EINVAL, "layer " + std::to_string(l) + ": " + what);
+    };
+    size_t n = 0;   // rows the rule recomputes so far
+    for (int b = 0; b < B; ++b) {
+      const size_t first = n;
+      for (int q = 0; q < P; ++q) {
+        const bool reused = valid[b] && mask && q >= 1 && q <= N && mask[((size_t)b * L + l) * N + q - 1];
+        if (reused) continue;
+        if (n >= (size_t)counts[l] || counts[l] > (int32_t)tot)
+          return bad("count " + std::to_string(counts[l]) + " misses row " + std::to_string(b * P + q));
+        if (idx[n] != b * P + q || ep[n] != b || pos[n] != q)
+          return bad("entry " + std::to_string(n) + " is (" + std::to_string(idx[n]) + ", " + std::to_string(ep[n]) +
+                     ", " + std::to_string(pos[n]) + "), expected (" + std::to_string(b * P + q) + ", " +
+                     std::to_string(b) + ", " + std::to_string(q) + ")");
+        ++n;
+      }
+      if (ep_offsets[l * B + b] != (int32_t)first || ep_counts[l * B + b] != (int32_t)(n - first))
+        return bad("episode " + std::to_string(b) + " has offset " + std::to_string(ep_offsets[l * B + b]) +
+                   " and count " + std::to_string(ep_counts[l * B + b]) + ", expected " + std::to_string(first) +
+                   " and " + std::to_string(n - first));
+    }
+    if (counts[l] != (int32_t)n)
+      return bad("count " + std::to_string(counts[l]) + ", expected " + std::to_string(n));
+  }
+  return GVC_OK;
+}
+
 int32_t gvc_step_prefill(gvc_ctx* c, const uint8_t* frame_t, const int32_t* text_ids, const float* extra_rows,
                          const uint8_t* reuse_mask) {
   if (!c || !frame_t || !text_ids) return fail(GVC_EINVAL, "null argument");
@@ -1018,6 +1080,21 @@ int32_t gvc_step_prefill(gvc_ctx* c, const uint8_t* frame_t, const int32_t* text
   HIP_TRY(hipStreamSynchronize(s));
   for (int l = 0; l < p.L; ++l)
     if (c->counts[l] < 1 || c->counts[l] > p.B * p.P) return fail(GVC_EDEVICE, "corrupt row count");
+  if (c->validate) {
+    const size_t tot = (size_t)p.B * p.P;
+    std::vector<int32_t> rows((size_t)p.L * 3 * tot), valid(p.B), epcs((size_t)p.L * p.B), epos((size_t)p.L * p.B);
+    std::vector<uint8_t> mask(reuse_mask ? (size_t)p.B * p.L * p.N : 0);
+    HIP_TRY(hipMemcpyAsync(rows.data(), c->K<int>(p.rows_off), rows.size() * 4, hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipMemcpyAsync(valid.data(), c->S<int>(p.valid_off), valid.size() * 4, hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipMemcpyAsync(epcs.data(), epc, epcs.size() * 4, hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipMemcpyAsync(epos.data(), epo, epos.size() * 4, hipMemcpyDeviceToHost, s));
+    if (reuse_mask) HIP_TRY(hipMemcpyAsync(mask.data(), reuse_mask, mask.size(), hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipStreamSynchronize(s));
+    if (c->validate == 2) rows[0] += 1;
+    if (gvc_check_rows(p.B, p.L, p.N, p.P, reuse_mask ? mask.data() : nullptr, valid.data(), rows.data(),
+                       c->counts.data(), epcs.data(), epos.data()) != GVC_OK)
+      return fail(GVC_EDEVICE, "row lists fail the host check: " + std::string(gvc_last_error()));
+  }
 
   // layer-0 embeddings of the rows recomputed at layer 0
   if (p.vit) {

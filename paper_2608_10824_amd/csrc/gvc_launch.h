@@ -11,6 +11,9 @@ hipError_t launch_pack(const bf16* src, int N, int K, bf16* dst, int Nblk, int K
 hipError_t launch_convert_gain(const bf16* src, float* dst, int n, hipStream_t s);
 hipError_t launch_rope_table(float2* tab, int kv_pad, int head_dim, float theta, hipStream_t s);
 hipError_t launch_fill_u32(uint32_t* p, uint32_t v, size_t n, hipStream_t s);
+// Zeroes positions [from, kv_pad) of n_blk key blocks ([kv_pad][dh]) and value
+// blocks ([dh][kv_pad]).
+hipError_t launch_zero_kv_tail(bf16* k, bf16* v, size_t n_blk, int kv_pad, int dh, int from, hipStream_t s);
 
 hipError_t launch_patch_stats(const uint8_t* ft, const uint8_t* fp, int B, int views, int img, int patch,
                               int* stats, hipStream_t s);

@@ -48,6 +48,23 @@ __global__ void k_fill_u32(uint32_t* p, uint32_t v, size_t n) {
   for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) p[i] = v;
 }
 
+// Zeroes positions [from, kv_pad) of n_blk caches of one key layout
+// ([kv_pad][dh] per block) and one value layout ([dh][kv_pad] per block).
+__global__ void k_zero_kv_tail(bf16* __restrict__ k, bf16* __restrict__ v, size_t n_blk, int kv_pad, int dh,
+                               int from) {
+  const int tail = kv_pad - from;
+  const size_t nk = n_blk * (size_t)tail * dh, nv = n_blk * (size_t)dh * tail;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < nk + nv; i += (size_t)gridDim.x * blockDim.x) {
+    if (i < nk) {
+      const size_t blk = i / ((size_t)tail * dh), r = i % ((size_t)tail * dh);
+      k[blk * kv_pad * dh + (size_t)from * dh + r] = 0;
+    } else {
+      const size_t j = i - nk, row = j / tail, c = j % tail;   // row = block * dh + dim
+      v[row * kv_pad + from + c] = 0;
+    }
+  }
+}
+
 // ------------------------------------------------------------------ row lists
 // One workgroup per layer.  Row r = b*P + pos of the batched prompt is
 // recomputed at layer l unless episode b has a valid cache, a mask is given,
@@ -504,6 +521,14 @@ hipError_t launch_fill_u32(uint32_t* p, uint32_t v, size_t n, hipStream_t s) {
   if (n == 0) return hipSuccess;
   const int blocks = (int)std::min<size_t>((n + 255) / 256, 65536);
   hipLaunchKernelGGL(k_fill_u32, dim3(blocks), dim3(256), 0, s, p, v, n);
+  return hipGetLastError();
+}
+
+hipError_t launch_zero_kv_tail(bf16* k, bf16* v, size_t n_blk, int kv_pad, int dh, int from, hipStream_t s) {
+  if (from >= kv_pad || n_blk == 0) return hipSuccess;
+  const size_t n = 2 * n_blk * (size_t)(kv_pad - from) * dh;
+  const int blocks = (int)std::min<size_t>((n + 255) / 256, 65536);
+  hipLaunchKernelGGL(k_zero_kv_tail, dim3(blocks), dim3(256), 0, s, k, v, n_blk, kv_pad, dh, from);
   return hipGetLastError();
 }
 

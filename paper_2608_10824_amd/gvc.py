@@ -8,7 +8,9 @@ the library has not been built.
 import ctypes
 import os
 
-_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libgvc.so")
+# GVC_LIBRARY selects another build of the same library (the host-code
+# AddressSanitizer build, libgvc_asan.so); there is no other implementation.
+_LIB_PATH = os.environ.get("GVC_LIBRARY") or os.path.join(os.path.dirname(os.path.abspath(__file__)), "libgvc.so")
 
 GVC_OK, GVC_EINVAL, GVC_ESTATE, GVC_ENOMEM, GVC_EDEVICE = 0, 1, 2, 3, 4
 REDUCE_MEAN, REDUCE_MIN = 0, 1
@@ -22,7 +24,7 @@ REDUCE_MEAN, REDUCE_MIN = 0, 1
 EXPORTED = ("gvc_sizes", "gvc_init_cache", "gvc_select_static", "gvc_select_static_noalloc", "gvc_step_prefill",
             "gvc_decode_actions",
             "gvc_margin_gate", "gvc_invalidate", "gvc_read_state", "gvc_state_item_bytes", "gvc_profile_begin",
-            "gvc_profile_end", "gvc_destroy", "gvc_last_error")
+            "gvc_profile_end", "gvc_destroy", "gvc_last_error", "gvc_check_rows")
 
 
 class GvcError(RuntimeError):
@@ -93,6 +95,7 @@ def lib():
         L.gvc_profile_begin.argtypes = [vp, i32, i32]
         L.gvc_profile_end.argtypes = [vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i32)]
         L.gvc_destroy.argtypes = [vp]
+        L.gvc_check_rows.argtypes = [i32, i32, i32, i32, vp, vp, vp, vp, vp, vp]
         L.gvc_last_error.restype = ctypes.c_char_p
         for n in EXPORTED:
             if n not in ("gvc_state_item_bytes", "gvc_last_error"):
@@ -122,6 +125,13 @@ def init_cache(desc: Desc, weights: Weights, weight_arena: int, weight_bytes: in
     _check(lib().gvc_init_cache(ctypes.byref(desc), ctypes.byref(weights), weight_arena, weight_bytes, state,
                                 state_bytes, workspace, workspace_bytes, stream, ctypes.byref(ctx)))
     return ctx.value
+
+
+def check_rows(B: int, L: int, N: int, P: int, mask: int, valid: int, rows: int, counts: int, ep_counts: int,
+               ep_offsets: int) -> int:
+    """Host-side row-list check (all arguments host addresses, mask may be 0);
+    returns the status code (GVC_OK or GVC_EINVAL, message in last_error())."""
+    return lib().gvc_check_rows(B, L, N, P, mask or None, valid, rows, counts, ep_counts, ep_offsets)
 
 
 def select_static(ctx: int, frame_t: int, frame_prev: int, tau_num: int, tau_den: int, reuse_permille,
