@@ -50,6 +50,8 @@
 // gvc_kernels.h): QKV blocks [i*3d/16/G, (i+1)*3d/16/G); down projection
 // block i; gate/up pairs [i*F/16/G, (i+1)*F/16/G); step 2: head i % H,
 // output slice i / H of min(G/H, d/16) slices.
+#include <type_traits>
+
 #include "gvc_kernels.h"
 
 namespace gvc {
@@ -64,6 +66,9 @@ constexpr int kSC0 = 1;                        // buffer cache policy: coherent 
 constexpr int kRingBytes = kWaves * kRing * 1024;
 constexpr int kRedBytes = kWaves * kDecodeMaxSeg * 16 * 4;
 constexpr int kScoreOffset = 256;              // attention scores follow the head output in the act region
+// ring fragments consumed per round in each step (see run_step)
+constexpr std::integral_constant<int, 1> kUnQkv{}, kUnGu{}, kUnDown{};
+constexpr std::integral_constant<int, 2> kUnO{};
 
 typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 typedef __amdgpu_buffer_rsrc_t rsrc_t;
@@ -566,13 +571,41 @@ __global__ __launch_bounds__(kThreads) void k_decode_pass(const DecodeArgs a) {
   }
 
   // Compute waves: nseg blocks of nk k steps each over the staged activation
-  // (k steps k0.. of act); partial sums to red[wave][block].
-  auto run_step = [&](int nseg, int nk, int k0) {
+  // (k steps k0.. of act); partial sums to red[wave][block].  Fragments are
+  // consumed UN at a time: the UN oldest ring loads have landed, their LDS
+  // reads overlap, then their slots are refilled.  A step whose fragments
+  // are already in the ring (the output projection after the attention) is
+  // bound by this loop, not by HBM.
+  auto run_step = [&](auto un, int nseg, int nk, int k0) {
+    constexpr int UN = decltype(un)::value;
     const bf16* abase = act + (lane >> 4) * 8;
     const bool row0 = (lane & 15) == 0;
     for (int s = 0; s < nseg; ++s) {
       floatx4 acc = {0.f, 0.f, 0.f, 0.f};
-      for (int j = 0; j < nk; ++j) {
+      int j = 0;
+      if constexpr (UN > 1) {
+        for (; j + UN <= nk; j += UN) {
+          wait_vm<kRing - UN>();
+          u32x4 wf[UN], xf[UN];
+#pragma unroll
+          for (int u = 0; u < UN; ++u) {
+            const int sl = slot + u < kRing ? slot + u : slot + u - kRing;
+            wf[u] = myring[sl * 64 + lane];
+            xf[u] = *(const u32x4*)(abase + (k0 + j + u) * 32);
+            if (!row0) xf[u] = u32x4{0u, 0u, 0u, 0u};
+          }
+#pragma unroll
+          for (int u = 0; u < UN; ++u)
+            acc = mfma16(__builtin_bit_cast(bf16x8, xf[u]), __builtin_bit_cast(bf16x8, wf[u]), acc);
+          wait_lgkm0();
+#pragma unroll
+          for (int u = 0; u < UN; ++u) {
+            issue(slot);
+            slot = slot + 1 == kRing ? 0 : slot + 1;
+          }
+        }
+      }
+      for (; j < nk; ++j) {
         wait_vm<kRing - 1>();
         const u32x4 wf = myring[slot * 64 + lane];
         u32x4 xf = *(const u32x4*)(abase + (k0 + j) * 32);
@@ -620,7 +653,7 @@ __global__ __launch_bounds__(kThreads) void k_decode_pass(const DecodeArgs a) {
     // ---------------- 1. QKV projection (head ah's rows, published to the head's workgroups)
     stage_norm<false, NCH>(r_x, r_x, a.bar, gains + (size_t)l * 2 * d, d, a.KBd * 32, a.eps, act, wred);
     block_sync();
-    if (!syncw) run_step(nseg0, nkd, k0d);
+    if (!syncw) run_step(kUnQkv, nseg0, nkd, k0d);
     if (syncw && attn && (a.flags & kDecodeWarmKv)) {
       // share asl of head ah's cached keys (rows of DH) and values (dims of
       // kv_pad), read once now so that step 2 finds them in this XCD's L2
@@ -651,7 +684,7 @@ __global__ __launch_bounds__(kThreads) void k_decode_pass(const DecodeArgs a) {
 
       // ---------------- 2. attention of head ah, times W_o's slice asl of head-ah columns
       attn_head<DH>(ah, a.pos, d, a.kv_pad, asl == 0, xl, lkc, lvc, rp, r_qkv, qs, kn, vn, wred, sc, act);
-      if (!syncw) run_step(nseg_o, KH, 0);
+      if (!syncw) run_step(kUnO, nseg_o, KH, 0);
       block_sync();
       if (syncw) {
         bool bad = false;
@@ -678,7 +711,7 @@ __global__ __launch_bounds__(kThreads) void k_decode_pass(const DecodeArgs a) {
     // ---------------- 3. gate/up projection + SwiGLU
     stage_norm<true, NCH>(r_x, r_acc, a.bar, gains + (size_t)l * 2 * d + d, d, a.KBd * 32, a.eps, act, wred);
     block_sync();
-    if (!syncw) run_step(nseg2, nkd, k0d);
+    if (!syncw) run_step(kUnGu, nseg2, nkd, k0d);
     block_sync();
     if (syncw) {
       for (int s0 = 0; s0 < nseg2 / 2; s0 += 4) {
@@ -696,7 +729,7 @@ __global__ __launch_bounds__(kThreads) void k_decode_pass(const DecodeArgs a) {
     // before the last barrier)
     stage_copy(r_act, F, a.KBf * 32, act);
     block_sync();
-    if (!syncw) run_step(nseg3, nkf, k0f);
+    if (!syncw) run_step(kUnDown, nseg3, nkf, k0f);
     block_sync();
     if (syncw) {
       const bool poisoned = poisoned_now(a.bar);
