@@ -372,26 +372,21 @@ __global__ void k_gather_visual(const bf16* __restrict__ src, const int* __restr
 // ------------------------------------------------------------------ logits
 // One workgroup per head row: greedy bin token (ties to the lower id) and
 // margin p1 - p2 with the softmax normaliser over the whole vocabulary (Eq. 1).
-struct Top2 { float v1; int i1; float v2; int i2; };
-
 __device__ __forceinline__ bool better(float va, int ia, float vb, int ib) {
   return va > vb || (va == vb && ia < ib);
 }
 
-__device__ __forceinline__ Top2 merge2(const Top2& a, const Top2& b) {
-  Top2 r;
-  if (better(a.v1, a.i1, b.v1, b.i1)) {
-    r.v1 = a.v1; r.i1 = a.i1;
-    if (better(a.v2, a.i2, b.v1, b.i1)) { r.v2 = a.v2; r.i2 = a.i2; } else { r.v2 = b.v1; r.i2 = b.i1; }
-  } else {
-    r.v1 = b.v1; r.i1 = b.i1;
-    if (better(a.v1, a.i1, b.v2, b.i2)) { r.v2 = a.v1; r.i2 = a.i1; } else { r.v2 = b.v2; r.i2 = b.i2; }
-  }
-  return r;
-}
-
-__device__ __forceinline__ Top2 shfl_top2(const Top2& t, int m) {
-  return Top2{__shfl_xor(t.v1, m), __shfl_xor(t.i1, m), __shfl_xor(t.v2, m), __shfl_xor(t.i2, m)};
+// Adds candidate (v, i) to a running top-2 (v1, i1) >= (v2, i2) under `better`,
+// a total order (value, then lower id), so the result does not depend on the
+// order of the additions.
+__device__ __forceinline__ void top2_add(float& v1, int& i1, float& v2, int& i2, float v, int i) {
+  const bool b1 = better(v, i, v1, i1), b2 = better(v, i, v2, i2);
+  const float nv2 = b1 ? v1 : (b2 ? v : v2);
+  const int ni2 = b1 ? i1 : (b2 ? i : i2);
+  v1 = b1 ? v : v1;
+  i1 = b1 ? i : i1;
+  v2 = nv2;
+  i2 = ni2;
 }
 
 // Running (max, sum of exp(z - max)) pair; a term at -inf contributes 0.
@@ -412,6 +407,7 @@ __device__ __forceinline__ void lse_merge(float& mx, float& sum, float mo, float
 }
 
 constexpr int kReduceThreads = 1024;
+constexpr int kReducePer = 8;   // chunks of 4 logits per thread loaded together
 
 // One pass over the row: every thread keeps its own running maximum, sum of
 // exponentials and bin top-2 over a strided set of float4 columns; the
@@ -420,45 +416,63 @@ __global__ __launch_bounds__(kReduceThreads) void k_logits_reduce(const float* _
                                                                   int bin_lo, int full_vocab, int* __restrict__ tok_out,
                                                                   float* __restrict__ margin_out, int out_stride,
                                                                   int out_col, int rows_per_ep) {
-  __shared__ float s_m[kReduceThreads / 64], s_s[kReduceThreads / 64];
-  __shared__ Top2 s_t[kReduceThreads / 64];
+  constexpr int NW = kReduceThreads / 64;
+  __shared__ float s_m[NW], s_s[NW], s_v1[NW], s_v2[NW];
+  __shared__ int s_i1[NW], s_i2[NW];
   const int r = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const float4* z4 = (const float4*)(logits + (size_t)r * V);
   const int lo = full_vocab ? 0 : bin_lo;
   const float NEG = -INFINITY;
   float mx = NEG, sum = 0.f;
-  Top2 t = {NEG, 0x7fffffff, NEG, 0x7fffffff};
-  for (int c = tid; c < V / 4; c += kReduceThreads) {
-    const float4 q = z4[c];
-    const float v[4] = {q.x, q.y, q.z, q.w};
+  // running top-2 of the bins under `better` (a total order: value, then
+  // lower id), kept as scalars so that nothing goes to private memory
+  float v1 = NEG, v2 = NEG;
+  int i1 = 0x7fffffff, i2 = 0x7fffffff;
+  // each thread takes chunks tid, tid + T, ... in order; the loads of a batch
+  // of kReducePer chunks are all issued before any is used (one round trip)
+  const int n4 = V / 4;
+  for (int c0 = 0; c0 < n4; c0 += kReduceThreads * kReducePer) {
+    float4 q[kReducePer];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int i = c * 4 + j;
-      if (i >= lo) lse_add(mx, sum, v[j]);
-      if (i >= bin_lo) t = merge2(t, Top2{v[j], i, NEG, 0x7fffffff});
+    for (int u = 0; u < kReducePer; ++u) q[u] = z4[min(c0 + u * kReduceThreads + tid, n4 - 1)];
+#pragma unroll
+    for (int u = 0; u < kReducePer; ++u) {
+      const int c = c0 + u * kReduceThreads + tid;
+      if (c < n4) {
+        const int i = c * 4;
+        const float e[4] = {q[u].x, q[u].y, q[u].z, q[u].w};
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          if (i + j >= lo) lse_add(mx, sum, e[j]);
+          if (i + j >= bin_lo) top2_add(v1, i1, v2, i2, e[j], i + j);
+        }
+      }
     }
   }
 #pragma unroll
   for (int m = 1; m < 64; m <<= 1) {
     lse_merge(mx, sum, __shfl_xor(mx, m), __shfl_xor(sum, m));
-    t = merge2(t, shfl_top2(t, m));
+    const float w1 = __shfl_xor(v1, m), w2 = __shfl_xor(v2, m);
+    const int j1 = __shfl_xor(i1, m), j2 = __shfl_xor(i2, m);
+    top2_add(v1, i1, v2, i2, w1, j1);
+    top2_add(v1, i1, v2, i2, w2, j2);
   }
   if (lane == 0) {
-    s_m[wv] = mx;
-    s_s[wv] = sum;
-    s_t[wv] = t;
+    s_m[wv] = mx; s_s[wv] = sum;
+    s_v1[wv] = v1; s_i1[wv] = i1; s_v2[wv] = v2; s_i2[wv] = i2;
   }
   __syncthreads();
   if (tid == 0) {
     float M = s_m[0], S = s_s[0];
-    Top2 best = s_t[0];
-    for (int w = 1; w < kReduceThreads / 64; ++w) {
+    v1 = s_v1[0]; i1 = s_i1[0]; v2 = s_v2[0]; i2 = s_i2[0];
+    for (int w = 1; w < NW; ++w) {
       lse_merge(M, S, s_m[w], s_s[w]);
-      best = merge2(best, s_t[w]);
+      top2_add(v1, i1, v2, i2, s_v1[w], s_i1[w]);
+      top2_add(v1, i1, v2, i2, s_v2[w], s_i2[w]);
     }
-    const float m = (__expf(best.v1 - M) - __expf(best.v2 - M)) / S;
+    const float m = (__expf(v1 - M) - __expf(v2 - M)) / S;
     const int o = (r / rows_per_ep) * out_stride + out_col + r % rows_per_ep;
-    tok_out[o] = best.i1;
+    tok_out[o] = i1;
     margin_out[o] = m;
   }
 }
