@@ -291,6 +291,7 @@ struct gvc_ctx {
   // the other sessions' gate/up projection on the split-k kernel (GVC_SK=0
   // turns it off: testing)
   bool sk_gemm = true;
+  int sk_dx = 1;          // GVC_SK_CORE: split-k core, 1 = k_gemm_dx (decoupled streams), 0 = k_gemm_sk
   // persistent decode pass (k_decode.hip): eligible shape, its grid and LDS
   bool persist = false;
   int persist_wg = 0;
@@ -394,6 +395,7 @@ int32_t run_gemm_sk(gvc_ctx* c, GemmArgs& a, int epi, int M, int cls, int slices
   const int gb = gemm_sk_group_blocks();
   a.sk_groups = (nblk + gb - 1) / gb;
   a.part = c->K<float>(p.part_off);
+  a.sk_dx = c->sk_dx;
   a.part_ld = nblk * 16;
   a.part_rows = a.mblocks * 16;
   if ((size_t)a.sk_slices * a.part_rows * a.part_ld * 4 > p.part_bytes) return fail(GVC_EINVAL, "split-k buffer");
@@ -850,6 +852,7 @@ int32_t gvc_init_cache(const gvc_desc* desc, const gvc_weights* wt, void* weight
   if (const char* fs = getenv("GVC_FORCE_SPLITS")) c->force_splits = atoi(fs);
   c->big_gemm = p.B * p.P >= kBigRows;
   if (const char* sk = getenv("GVC_SK")) c->sk_gemm = atoi(sk) != 0;
+  if (const char* sc = getenv("GVC_SK_CORE")) c->sk_dx = atoi(sc) != 0;
   if (const char* tw = getenv("GVC_BIG_TW")) c->big_tw = atoi(tw);
   if (const char* g = getenv("GVC_GEMM")) {
     if (!strcmp(g, "big")) c->big_gemm = true;

@@ -72,6 +72,7 @@ struct GemmArgs {
   float* part;
   int sk_slices, sk_steps, sk_groups, part_ld, part_rows;
   int big_tw;           // many-row kernel: token blocks per wave (2, 3 or 4), 0 = chosen per launch
+  int sk_dx;            // split-k core: 0 = k_gemm_sk, 1 = k_gemm_dx (decoupled weight and token streams)
   EpiArgs e;
 };
 

@@ -355,3 +355,29 @@ def test_many_row_tile_height_does_not_change_a_row():
             ref = flat
         else:
             assert all(np.array_equal(a, b) for a, b in zip(flat, ref)), "tile height %s" % tw
+
+
+def test_split_k_cores_agree_bit_for_bit(monkeypatch):
+    """The two split-k cores of the gate/up projection (decoupled weight and
+    token streams, the default, and the register-fed one, GVC_SK_CORE=0) sum
+    each k slice in the same order, so a full and a partial step give the
+    same state bit for bit (MID: 136 rows, 2 k slices)."""
+    cfg = synth.config_mid()
+    w = synth.model_weights(cfg)
+    si = synth.step_inputs(cfg, 64)
+    states = []
+    for core in ("1", "0"):
+        monkeypatch.setenv("GVC_SK_CORE", core)
+        s = _session(cfg, w)
+        monkeypatch.delenv("GVC_SK_CORE")
+        fp, ft, ids = si["frame_prev"].to(DEV), si["frame_t"].to(DEV), si["text_ids"].to(DEV)
+        s.step_prefill(fp, ids)
+        s.decode_actions()
+        s.margin_gate(force=[0])
+        mask, _ = s.select_static(ft, fp)
+        s.step_prefill(ft, ids, None, mask)
+        states.append(_state(s, cfg))
+        s.close()
+    a, b = states
+    for x, y in zip(a[0] + a[1] + a[2] + [a[3]], b[0] + b[1] + b[2] + [b[3]]):
+        assert np.array_equal(x, y)
