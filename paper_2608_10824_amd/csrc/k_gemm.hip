@@ -795,12 +795,15 @@ __global__ __launch_bounds__((8 + NXW) * 64) void k_gemm_dx(const GemmArgs a) {
 
 // Sums the k slices of k_gemm_sk in order and runs the epilogue: one wave
 // per (work pair, block of 16 rows), in the lane layout of the MFMA result.
+// The 4 waves of a workgroup take 4 consecutive pairs of one row block, so
+// each row's partial sums are read as whole cache lines by one CU (C2
+// gate/up: prompt pass 6.56 -> 6.48 ms against row-block-minor order).
 template <int EPI>
 __global__ __launch_bounds__(256) void k_gemm_sk_epi(const GemmArgs a) {
   const int lane = threadIdx.x & 63;
   const int w = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (w >= a.n_pairs * a.mblocks) return;
-  const int pair = w / a.mblocks, mb = w % a.mblocks;
+  const int pair = w % a.n_pairs, mb = w / a.n_pairs;
   int ma, ba, mb2, bb; bool b_ok;
   map_pair(a, pair, ma, ba, mb2, bb, b_ok);
   const int m = mb * 16 + (lane & 15), sub = (lane >> 4) * 4;
