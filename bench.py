@@ -563,6 +563,12 @@ def main():
     # averaged over the passes (pass j attends over P + j keys)
     n_pass = cfg.n_decode - 1
     dk_bytes = L * layer_weight_bytes(cfg) + sum(L * 2 * (P + j) * d * 2 for j in range(1, n_pass + 1)) / n_pass
+    # the pass also runs the final norm, the LM head and the token choice
+    # (unless GVC_DECODE_FLAGS masks the head bit): V x d head weights read,
+    # V logits written
+    head_fused = (int(os.environ.get("GVC_DECODE_FLAGS", "7")) & 4) != 0
+    if head_fused:
+        dk_bytes += V * d * 2 + V * 4
     dk_avg_s = dk_ms / 1e3 / max(dk_n, 1)
     dk_gbs = dk_bytes / dk_avg_s / 1e9
     # prompt pass algorithmic work: the recomputed rows of every layer, their
@@ -604,7 +610,8 @@ def main():
         "gate_fired_steps": sum(fired),
         "roofline": {"bound": "hbm", "achieved": dk_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": dk_gbs / HBM_PEAK_GBS, "traffic": traffic,
-                     "kernel": "k_decode_pass<128, 2> (one decode pass over all 32 layers, cooperative grid)",
+                     "kernel": "k_decode_pass<128, 2> (one decode pass over all 32 layers%s, cooperative grid)"
+                               % (", the final norm, the LM head and the token choice" if head_fused else ""),
                      "bytes_per_launch": dk_bytes, "avg_launch_us": dk_avg_s * 1e6, "launches": dk_n,
                      "region_ms_per_step": dt2 * 1e3 / args.steps},
     }

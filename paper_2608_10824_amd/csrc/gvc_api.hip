@@ -78,7 +78,7 @@ struct Plan {
   size_t rows_off, counts_off, epc_off, epo_off, stats_off, x_off, q_off, o_off, r_off, act_off, xdec_off, xf_off,
       ssq_a_off, ssq_f_off, qraw_off, kraw_off, part_off, part_bytes,
       logits_off, rope_off, decrows_off, headrows_off, tokens_off, gate_m_off, gate_f_off, qkv3_off, bar_off,
-      ws_bytes;
+      hpart_off, ws_bytes;
 };
 
 Packed plan_packed(Bump& a, int N, int K) {
@@ -243,6 +243,7 @@ int32_t make_plan(const gvc_desc* dsc, Plan& p) {
   p.gate_f_off = k.take((size_t)p.B * 4);
   p.qkv3_off = k.take((size_t)3 * p.B * d.d_model * 4);
   p.bar_off = k.take((size_t)kDecodeBarWords * 4);
+  p.hpart_off = k.take((size_t)kDecodeMaxGrid * 8 * 4);
   {   // split-k partial sums of the gate/up projection: slices x rows x features
     const int kps = (p.KBd + kSkGuSlices - 1) / kSkGuSlices;
     const size_t slices = (p.KBd + kps - 1) / kps;
@@ -750,7 +751,7 @@ bool setup_persist(gvc_ctx* c) {
   if (hipDeviceGetAttribute(&G, hipDeviceAttributeMultiprocessorCount, c->device) != hipSuccess) return false;
   if (hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, c->device) != hipSuccess || !coop) return false;
   auto ceil_div = [](int a, int b) { return (a + b - 1) / b; };
-  if (G < 1 || p.H > G || p.H > kDecodeMaxHeads) return false;
+  if (G < 1 || G > kDecodeMaxGrid || p.H > G || p.H > kDecodeMaxHeads) return false;
   const int n_slices = std::min(G / p.H, d / 16);
   if (3 * ceil_div(p.dh / 16, n_slices) > kDecodeMaxSeg || 2 * ceil_div(F / 16, G) > kDecodeMaxSeg ||
       ceil_div(d / 16, G) > kDecodeMaxSeg || ceil_div(ceil_div(d / 16, n_slices), 8) > kDecodeMaxSeg)
@@ -789,8 +790,17 @@ bool setup_persist(gvc_ctx* c) {
   // the activations, barrier words and key/value lines from L2 (7B: 2.93
   // instead of 3.09 ms per pass; warming the keys and values adds 1%).
   // GVC_DECODE_FLAGS overrides the flags (measurement).
-  a.flags = kDecodeNtWeights | kDecodeWarmKv;
-  if (const char* e = getenv("GVC_DECODE_FLAGS")) a.flags = atoi(e) & (kDecodeNtWeights | kDecodeWarmKv);
+  // The LM head and the token choice join the pass when its blocks fit
+  // kDecodeMaxSeg per workgroup.
+  const bool head = ceil_div(p.lm.Nblk, G) <= kDecodeMaxSeg;
+  a.flags = kDecodeNtWeights | kDecodeWarmKv | (head ? kDecodeHead : 0);
+  if (const char* e = getenv("GVC_DECODE_FLAGS"))
+    a.flags = atoi(e) & (kDecodeNtWeights | kDecodeWarmKv | (head ? kDecodeHead : 0));
+  a.wlm = c->packed(p.lm); a.nlm = p.lm.Nblk;
+  a.final_gain = c->W<float>(p.final_gain_off);
+  a.logits = c->K<float>(p.logits_off);
+  a.head_part = c->K<float>(p.hpart_off);
+  a.V = p.V; a.bin_lo = p.bin_lo; a.full_vocab = p.d.norm_full_vocab ? 1 : 0;
   c->persist_wg = G;
   return true;
 }
@@ -1168,6 +1178,7 @@ int32_t gvc_decode_actions(gvc_ctx* c, int32_t* tokens_out, float* margins_out, 
                                   c->W<float>(p.gains_off), c->K<bf16>(p.x_off), p.KBd, c->K<float>(p.ssq_a_off), s));
       const RowMap rows = c->dec_rows(j);
       const int pos = p.P + j - 1;
+      bool fused = false;   // the decode pass also ran the LM head and the token choice
       GemmArgs hd = base_args(c);
       hd.w[0] = c->packed(p.lm); hd.wblk[0] = p.lm.Nblk;
       hd.map = MAP_PLAIN; hd.n_pairs = (p.lm.Nblk + 1) / 2; hd.n_out = p.V; hd.KB = p.KBd;
@@ -1181,15 +1192,18 @@ int32_t gvc_decode_actions(gvc_ctx* c, int32_t* tokens_out, float* margins_out, 
                                   kDecodeBarWords - kDecodeAbortWord - 1, s));
         }
         DecodeArgs a = c->dargs;
+        fused = (a.flags & kDecodeHead) != 0;
         a.pos = pos;
-        a.bar_base = (unsigned)((j - 1) * decode_grid_barriers(p.L));
+        a.bar_base = (unsigned)((j - 1) * decode_grid_barriers(p.L, fused));
         a.hbar_base = (unsigned)((j - 1) * decode_head_barriers(p.L));
+        a.tok_out = tok + j;   // B = 1: token j of the episode
+        a.margin_out = mg + j;
         {
           ProfScope ps(c, GVC_K_DECODE_PASS);
           HIP_TRY(launch_decode_pass(a, c->persist_wg, s));
         }
         c->persist_ran = true;
-        {
+        if (!fused) {
           ProfScope ps(c, GVC_K_NORM);
           HIP_TRY(launch_rmsnorm(xdec, nullptr, p.B, p.d.d_model, c->W<float>(p.final_gain_off), p.d.rms_eps,
                                  c->K<bf16>(p.x_off), p.KBd, c->big_gemm, s));
@@ -1203,11 +1217,11 @@ int32_t gvc_decode_actions(gvc_ctx* c, int32_t* tokens_out, float* margins_out, 
         hd.e.ssq_in = c->K<float>(p.ssq_a_off); hd.e.ssq_parts = p.d.d_model / 16;
         hd.e.norm_eps = p.d.rms_eps; hd.e.norm_dim = p.d.d_model;
       }
-      {
+      if (!fused) {
         int32_t r = run_gemm(c, hd, EPI_STORE, p.B, GVC_K_DECODE_HEAD);
         if (r) return r;
+        HIP_TRY(launch_logits_reduce(lg, p.B, p.V, p.bin_lo, full, tok, mg, p.D, j, 1, s));
       }
-      HIP_TRY(launch_logits_reduce(lg, p.B, p.V, p.bin_lo, full, tok, mg, p.D, j, 1, s));
       if (logits_out)
         HIP_TRY(hipMemcpy2DAsync(logits_out + (size_t)j * p.V, (size_t)p.D * p.V * 4, lg, (size_t)p.V * 4,
                                  (size_t)p.V * 4, p.B, hipMemcpyDeviceToDevice, s));

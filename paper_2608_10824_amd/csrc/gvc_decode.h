@@ -12,11 +12,13 @@ constexpr int kDecodeXccWord = 544;    // barrier words: set when a workgroup is
 constexpr int kDecodePoisonWord = 576; // barrier words: set when a head contribution was not finite
 constexpr int kDecodeHeadWord = 1024;  // barrier words: per-head counters, 32 words apart
 constexpr int kDecodeMaxHeads = 64;
+constexpr int kDecodeMaxGrid = 1024;   // workgroups of one pass (per-workgroup head records)
 // zeroed before a launch sequence, except the abort word, which stays set
 // until the gate that follows has reported it
 constexpr int kDecodeBarWords = kDecodeHeadWord + 32 * kDecodeMaxHeads;
-// grid barriers and per-head barriers of one pass over L layers
-constexpr int decode_grid_barriers(int L) { return 1 + 3 * L; }
+// grid barriers and per-head barriers of one pass over L layers (one more
+// grid barrier when the pass also runs the LM head and the token choice)
+constexpr int decode_grid_barriers(int L, bool head) { return 1 + 3 * L + (head ? 1 : 0); }
 constexpr int decode_head_barriers(int L) { return L; }
 
 struct DecodeArgs {
@@ -38,9 +40,19 @@ struct DecodeArgs {
   long long timeout_ticks;     // barrier wait limit in wall-clock ticks (100 MHz)
   int L, d, F, H, head_dim, KBd, KBf, kv_pad, pos, act_bytes;
   float eps;
-  int flags;                   // kDecodeNtWeights | kDecodeWarmKv
+  int flags;                   // kDecodeNtWeights | kDecodeWarmKv | kDecodeHead
+  // with kDecodeHead: final norm, LM head and the greedy token and margin of
+  // this pass (Eq. 1) after the last layer
+  const bf16x8* wlm;           // packed LM head, nlm blocks of KBd fragments
+  const float* final_gain;     // [d]
+  float* logits;               // [V] this pass's logits
+  float* head_part;            // [gridDim <= kDecodeMaxGrid][8] per workgroup: max, sum, v1, i1, v2, i2
+  int* tok_out;                // the token of this pass (one int)
+  float* margin_out;           // its margin (one float)
+  int nlm, V, bin_lo, full_vocab;
 };
 constexpr int kDecodeNtWeights = 1;   // weight loads marked non-temporal
 constexpr int kDecodeWarmKv = 2;      // step 1 pulls the head's cached keys and values into L2
+constexpr int kDecodeHead = 4;        // the pass ends with the LM head and the token choice
 
 }  // namespace gvc

@@ -92,6 +92,44 @@ __device__ __forceinline__ float group_max(float v) {
   return v;
 }
 
+// ------------------------------------------------------------------ logits
+// Greedy-token and margin helpers (Eq. 1) shared by the logits reduction and
+// the decode pass: a total order on (logit, id) -- higher logit first, then
+// the lower id -- and a running top-2 and (max, sum of exp) under it.
+__device__ __forceinline__ bool better(float va, int ia, float vb, int ib) {
+  return va > vb || (va == vb && ia < ib);
+}
+
+// Adds candidate (v, i) to a running top-2 (v1, i1) >= (v2, i2) under `better`,
+// a total order (value, then lower id), so the result does not depend on the
+// order of the additions.
+__device__ __forceinline__ void top2_add(float& v1, int& i1, float& v2, int& i2, float v, int i) {
+  const bool b1 = better(v, i, v1, i1), b2 = better(v, i, v2, i2);
+  const float nv2 = b1 ? v1 : (b2 ? v : v2);
+  const int ni2 = b1 ? i1 : (b2 ? i : i2);
+  v1 = b1 ? v : v1;
+  i1 = b1 ? i : i1;
+  v2 = nv2;
+  i2 = ni2;
+}
+
+// Running (max, sum of exp(z - max)) pair; a term at -inf contributes 0.
+__device__ __forceinline__ void lse_add(float& mx, float& sum, float v) {
+  if (v > mx) {
+    sum = sum * __expf(mx - v) + 1.f;
+    mx = v;
+  } else if (v != -INFINITY) {
+    sum += __expf(v - mx);
+  }
+}
+
+__device__ __forceinline__ void lse_merge(float& mx, float& sum, float mo, float so) {
+  const float m = fmaxf(mx, mo);
+  if (m == -INFINITY) return;
+  sum = (mx == -INFINITY ? 0.f : sum * __expf(mx - m)) + (mo == -INFINITY ? 0.f : so * __expf(mo - m));
+  mx = m;
+}
+
 }  // namespace gvc
 
 #include "gvc_gemm.h"

@@ -495,6 +495,11 @@ __global__ __launch_bounds__(kThreads) void k_decode_pass(const DecodeArgs a) {
   const int gp0 = gi * nf / G, nseg2 = 2 * ((gi + 1) * nf / G - gp0);     // gate, up, gate, up, ...
   const int db0 = gi * nq / G, nseg3 = (gi + 1) * nq / G - db0;           // down blocks (k split)
   const int nsegs = nseg0 + nseg_o + nseg2 + nseg3;   // segments of one layer, in stream order
+  // step 5 (kDecodeHead): LM head blocks [hb0, hb0 + nh) (k split), streamed
+  // as one more "layer" after the last one
+  const bool head = (a.flags & kDecodeHead) != 0;
+  const int hb0 = head ? gi * a.nlm / G : 0, nh = head ? (gi + 1) * a.nlm / G - hb0 : 0;
+  const int Lend = a.L + (head ? 1 : 0);
 
   const rsrc_t r_x = rsrc(a.x, (size_t)d * 4), r_acc = rsrc(a.racc, (size_t)d * 8);
   const rsrc_t r_qkv = rsrc(a.qkv, (size_t)3 * d * 4);
@@ -506,6 +511,7 @@ __global__ __launch_bounds__(kThreads) void k_decode_pass(const DecodeArgs a) {
   // into indexed private memory.
   const bf16x8* const wq = a.wq;
   const long long off_o = a.wo - a.wq, off_g = a.wg - a.wq, off_d = a.wd - a.wq;
+  const bf16x8* const lm0 = head ? a.wlm + ((long long)hb0 * a.KBd + k0d) * 64 : wq;   // head block hb0, k step k0d
   const long long qkv_stride = (long long)a.qkv_stride, gu_stride = (long long)a.gu_stride;
   const long long KBd = a.KBd, KBf = a.KBf;
   auto seg_off = [=](int sg) -> long long {
@@ -534,28 +540,30 @@ __global__ __launch_bounds__(kThreads) void k_decode_pass(const DecodeArgs a) {
   int slot = 0;
   u32x4* myring = ring + wv * kRing * 64;
   const bool nt_w = (a.flags & kDecodeNtWeights) != 0;
-  const bool streams = !syncw && (nseg0 + nseg2) * nkd + nseg_o * KH + nseg3 * nkf > 0;
+  const bool streams = !syncw && (nseg0 + nseg2 + nh) * nkd + nseg_o * KH + nseg3 * nkf > 0;
   const long long layer_stride = (long long)a.layer_stride;
-  // moves to the next non-empty segment at or after (p_l, p_sg)
+  // moves to the next non-empty segment at or after (p_l, p_sg); layer
+  // a.L (with the head step) holds the LM head blocks
   auto settle = [&]() {
-    while (p_l < a.L) {
-      const int len = seg_len(p_sg);
+    while (p_l < Lend) {
+      const bool hl = p_l == a.L;
+      const int len = hl ? (p_sg < nh ? nkd : 0) : (p_sg < nsegs ? seg_len(p_sg) : 0);   // a layer may have no segments
       if (len > 0) {
-        p_ptr = wq + seg_off(p_sg) + p_l * layer_stride;
+        p_ptr = hl ? lm0 + p_sg * KBd * 64 : wq + seg_off(p_sg) + p_l * layer_stride;
         p_left = len;
         return;
       }
-      if (++p_sg == nsegs) { p_sg = 0; ++p_l; }
+      if (++p_sg >= (hl ? nh : nsegs)) { p_sg = 0; ++p_l; }
     }
   };
   auto issue = [&](int sl) {
     const bf16x8* ptr = last;   // past the end: re-read the final fragment (in bounds, cached)
-    if (p_l < a.L) {
+    if (p_l < Lend) {
       ptr = p_ptr;
       last = ptr;
       p_ptr += 64;
       if (--p_left == 0) {
-        if (++p_sg == nsegs) { p_sg = 0; ++p_l; }
+        if (++p_sg >= (p_l == a.L ? nh : nsegs)) { p_sg = 0; ++p_l; }
         settle();
       }
     }
@@ -647,6 +655,7 @@ __global__ __launch_bounds__(kThreads) void k_decode_pass(const DecodeArgs a) {
   unsigned nhbar = 0;
 
   const float* gains = a.gains;
+  int layers_done = 0;
   for (int l = 0; l < a.L && run; ++l) {
     bf16* const lkc = a.kc + (size_t)l * a.kv_layer_elems;
     bf16* const lvc = a.vc + (size_t)l * a.kv_layer_elems;
@@ -744,6 +753,68 @@ __global__ __launch_bounds__(kThreads) void k_decode_pass(const DecodeArgs a) {
       }
     }
     if (!barrier()) break;
+    layers_done = l + 1;
+  }
+
+  // ---------------- 5. final RMSNorm, LM head, and this pass's greedy token
+  // and margin (Eq. 1): each workgroup writes its logits and one partial
+  // record (max, sum of exp, top two bins) of them; after a grid barrier
+  // workgroup 0 merges the records in workgroup order (the merge is the same
+  // on every run) and writes the token and the margin.
+  if (head && layers_done == a.L) {
+    stage_norm<false, NCH>(r_x, r_x, a.bar, a.final_gain, d, a.KBd * 32, a.eps, act, wred);
+    block_sync();
+    if (!syncw) run_step(kUnQkv, nh, nkd, k0d);
+    block_sync();
+    const rsrc_t r_hp = rsrc(a.head_part, (size_t)G * 8 * 4);
+    if (syncw) {
+      const rsrc_t r_lg = rsrc(a.logits, (size_t)a.V * 4);
+      const int lo = a.full_vocab ? 0 : a.bin_lo;
+      float mx = -INFINITY, sm = 0.f, v1 = -INFINITY, v2 = -INFINITY;
+      int i1 = 0x7fffffff, i2 = 0x7fffffff;
+      for (int s0 = 0; s0 < nh; s0 += 4) {
+        const int s = s0 + (lane >> 4), t = lane & 15, idx = (hb0 + s) * 16 + t;
+        if (s < nh && idx < a.V) {
+          const float z = sum_partials(red, s, t);
+          st_f32(r_lg, idx * 4, z);
+          if (idx >= lo) lse_add(mx, sm, z);
+          if (idx >= a.bin_lo) top2_add(v1, i1, v2, i2, z, idx);
+        }
+      }
+#pragma unroll
+      for (int m = 1; m < 64; m <<= 1) {
+        lse_merge(mx, sm, __shfl_xor(mx, m), __shfl_xor(sm, m));
+        const float w1 = __shfl_xor(v1, m), w2 = __shfl_xor(v2, m);
+        const int j1 = __shfl_xor(i1, m), j2 = __shfl_xor(i2, m);
+        top2_add(v1, i1, v2, i2, w1, j1);
+        top2_add(v1, i1, v2, i2, w2, j2);
+      }
+      if (lane < 6) {
+        const float rec[6] = {mx, sm, v1, __int_as_float(i1), v2, __int_as_float(i2)};
+        st_f32(r_hp, (gi * 8 + lane) * 4, rec[lane]);
+      }
+    }
+    if (barrier() && gi == 0 && syncw) {
+      float mx = -INFINITY, sm = 0.f, v1 = -INFINITY, v2 = -INFINITY;
+      int i1 = 0x7fffffff, i2 = 0x7fffffff;
+      for (int w = lane; w < G; w += 64) {
+        lse_merge(mx, sm, ld_f32(r_hp, (w * 8) * 4), ld_f32(r_hp, (w * 8 + 1) * 4));
+        top2_add(v1, i1, v2, i2, ld_f32(r_hp, (w * 8 + 2) * 4), __float_as_int(ld_f32(r_hp, (w * 8 + 3) * 4)));
+        top2_add(v1, i1, v2, i2, ld_f32(r_hp, (w * 8 + 4) * 4), __float_as_int(ld_f32(r_hp, (w * 8 + 5) * 4)));
+      }
+#pragma unroll
+      for (int m = 1; m < 64; m <<= 1) {
+        lse_merge(mx, sm, __shfl_xor(mx, m), __shfl_xor(sm, m));
+        const float w1 = __shfl_xor(v1, m), w2 = __shfl_xor(v2, m);
+        const int j1 = __shfl_xor(i1, m), j2 = __shfl_xor(i2, m);
+        top2_add(v1, i1, v2, i2, w1, j1);
+        top2_add(v1, i1, v2, i2, w2, j2);
+      }
+      if (lane == 0) {
+        *a.tok_out = i1;
+        *a.margin_out = (__expf(v1 - mx) - __expf(v2 - mx)) / sm;
+      }
+    }
   }
   wait_vm<0>();   // direct-to-LDS loads must land before the workgroup ends
 }

@@ -210,37 +210,50 @@ def test_largest_frame_selection():
     s.close()
 
 
-@pytest.mark.parametrize("cfg_fn", [synth.config_c1, synth.config_mid])
+def _mid_bins_normaliser():
+    return synth.config_mid().with_(norm_full_vocab=False)
+
+
+@pytest.mark.parametrize("cfg_fn", [synth.config_c1, synth.config_mid, _mid_bins_normaliser])
 def test_decode_pass_matches_per_step_launches(cfg_fn, monkeypatch):
     """The single-launch decode pass (one episode) and the per-step launches
     compute the same passes: with the same fed-back tokens their logits agree
-    to the bf16 tolerance, and the single-launch path is the one that ran."""
+    to the bf16 tolerance, and the single-launch path is the one that ran.
+    The pass runs with the LM head and the token choice inside it (the
+    default) and with them as separate launches (decode flags 3): both give
+    the oracle's tokens and margins to the bound their logit error implies,
+    and each token is the argmax of that run's own logits."""
     from paper_2608_10824_amd import gvc
     cfg = cfg_fn()
     w = synth.model_weights(cfg)
     si = synth.step_inputs(cfg, cfg.n_patches // 2)
     o = OracleVLA(cfg, w)
     o.step_prefill(si["frame_prev"].numpy(), si["text_ids"].numpy())
-    tok_o, _, lg_o = o.decode_actions()
+    tok_o, m_o, lg_o = o.decode_actions()
     forced = torch.from_numpy(tok_o.astype(np.int32)).to(DEV)
     got = {}
-    for mode in ("legacy", "single"):
+    for mode in ("legacy", "split", "fused"):
+        monkeypatch.delenv("GVC_DECODE", raising=False)
+        monkeypatch.delenv("GVC_DECODE_FLAGS", raising=False)
         if mode == "legacy":
             monkeypatch.setenv("GVC_DECODE", "legacy")
-        else:
-            monkeypatch.delenv("GVC_DECODE", raising=False)
+        elif mode == "split":
+            monkeypatch.setenv("GVC_DECODE_FLAGS", "3")
         s = _session(cfg, w)
         s.step_prefill(si["frame_prev"].to(DEV), si["text_ids"].to(DEV))
         gvc.profile_begin(s.ctx, gvc.K_DECODE_PASS, 64)
-        _, _, lg = s.decode_actions(logits=True, forced_tokens=forced)
+        tok, mg, lg = s.decode_actions(logits=True, forced_tokens=forced)
         _, n = gvc.profile_end(s.ctx)
         assert n == (0 if mode == "legacy" else cfg.n_decode - 1)
         s.margin_gate()   # surfaces a barrier timeout of the single-launch path
-        got[mode] = lg.cpu().numpy()
+        got[mode] = (tok.cpu().numpy(), mg.cpu().numpy(), lg.cpu().numpy())
         s.close()
-    assert rel_err(got["single"], lg_o) <= TOL
-    assert rel_err(got["legacy"], lg_o) <= TOL
-    assert rel_err(got["single"], got["legacy"]) <= TOL
+    for mode, (tok, mg, lg) in got.items():
+        assert rel_err(lg, lg_o) <= TOL, mode
+        check_tokens(tok, lg, tok_o.reshape(tok.shape), lg_o.reshape(lg.shape), cfg.bin_lo)
+        check_margins(mg, m_o.reshape(mg.shape), lg, lg_o.reshape(lg.shape), cfg.bin_lo, cfg.norm_full_vocab)
+    assert rel_err(got["fused"][2], got["legacy"][2]) <= TOL
+    assert rel_err(got["fused"][2], got["split"][2]) <= TOL
 
 
 @pytest.mark.parametrize("name", ["C1V-B2", "C4T-bidir-B2"])
