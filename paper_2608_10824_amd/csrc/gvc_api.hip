@@ -30,12 +30,16 @@ int32_t fail(int32_t code, const std::string& msg) {
 constexpr size_t kAlign = 256;
 constexpr int kMaxNT = 5;   // token blocks per GEMM workgroup (best of 2..16 on the 7B prompt pass)
 constexpr int kBigRows = 1024;  // sessions with at least this many prompt rows use k_gemm_big
-// Split-k prompt-pass GEMM (k_gemm_sk) of the other sessions: kernel variant
-// and k slices, fixed per matrix shape.  Measured inside the 7B prompt pass
-// at 148 rows (median per launch): gate/up 58 µs + 11 for the slice sum,
-// against 85 for the per-pair kernel; QKV 44 + 11 against 50 and down 34 + 12
-// against 46, so only the gate/up projection takes it.
+// Split-k prompt-pass GEMMs (k_gemm_dx, or k_gemm_sk with GVC_SK_CORE=0) of
+// the sessions below kBigRows: k slices fixed per matrix shape.  Gate/up in 2
+// slices of 12-block groups, QKV in 4 slices of 12-block groups, the down
+// projection in 8 slices of 8-block groups (one weight block per compute
+// wave): at the 7B shape 230, 256 and 256 workgroups.  Inside the 7B prompt
+// pass at 148 rows this took the pass from 6.48 ms (per-pair kernels for QKV
+// and down, 16-block gate/up groups: 172 workgroups) to 5.72 ms; the output
+// projection stays on the per-pair kernel (8 slices measured 0.1 ms slower).
 constexpr int kSkGuSlices = 2;
+constexpr int kSkQkvSlices = 4, kSkDownSlices = 8;
 
 struct Bump {
   size_t off = 0;
@@ -244,10 +248,13 @@ int32_t make_plan(const gvc_desc* dsc, Plan& p) {
   p.qkv3_off = k.take((size_t)3 * p.B * d.d_model * 4);
   p.bar_off = k.take((size_t)kDecodeBarWords * 4);
   p.hpart_off = k.take((size_t)kDecodeMaxGrid * 8 * 4);
-  {   // split-k partial sums of the gate/up projection: slices x rows x features
-    const int kps = (p.KBd + kSkGuSlices - 1) / kSkGuSlices;
-    const size_t slices = (p.KBd + kps - 1) / kps;
-    p.part_bytes = (size_t)p.Mp * slices * 2 * (size_t)((d.ffn + 15) / 16 * 16) * 4;
+  {   // split-k partial sums (slices x rows x features) of the largest user:
+      // gate/up, QKV or the down projection
+    auto nsl = [](int KB, int want) { const int kps = (KB + want - 1) / want; return (size_t)((KB + kps - 1) / kps); };
+    const size_t gu = nsl(p.KBd, kSkGuSlices) * 2 * (size_t)((d.ffn + 15) / 16 * 16);
+    const size_t qkv = nsl(p.KBd, kSkQkvSlices) * 3 * (size_t)d.d_model;
+    const size_t down = nsl(p.KBf, kSkDownSlices) * (size_t)d.d_model;
+    p.part_bytes = (size_t)p.Mp * std::max({gu, qkv, down}) * 4;
     p.part_off = k.take(p.part_bytes);
   }
   if (p.vit) {
@@ -293,6 +300,10 @@ struct gvc_ctx {
   // turns it off: testing)
   bool sk_gemm = true;
   int sk_dx = 1;          // GVC_SK_CORE: split-k core, 1 = k_gemm_dx (decoupled streams), 0 = k_gemm_sk
+  // QKV and down projections of those sessions on the one-block-per-wave
+  // split-k shapes of the decoupled core (GVC_SK_QKV=0, GVC_SK_DOWN=0 turn
+  // them off)
+  bool sk_qkv = true, sk_down = true;
   // persistent decode pass (k_decode.hip): eligible shape, its grid and LDS
   bool persist = false;
   int persist_wg = 0;
@@ -384,7 +395,7 @@ GemmArgs base_args(const gvc_ctx* c) {
 
 // Split-k launch of a prompt-pass projection (k_gemm_sk + slice sum and
 // epilogue); the slices depend only on the matrix shape.
-int32_t run_gemm_sk(gvc_ctx* c, GemmArgs& a, int epi, int M, int cls, int slices) {
+int32_t run_gemm_sk(gvc_ctx* c, GemmArgs& a, int epi, int M, int cls, int slices, int shape = SK_GU) {
   if (M <= 0) return GVC_OK;
   const Plan& p = c->p;
   a.M = M;
@@ -393,10 +404,11 @@ int32_t run_gemm_sk(gvc_ctx* c, GemmArgs& a, int epi, int M, int cls, int slices
   a.sk_steps = kps;
   a.sk_slices = (a.KB + kps - 1) / kps;
   const int nblk = a.wblk[0] * (a.map == MAP_QKV ? 3 : (a.map == MAP_GU ? 2 : 1));
-  const int gb = gemm_sk_group_blocks();
+  const int gb = gemm_sk_group_blocks(shape);
   a.sk_groups = (nblk + gb - 1) / gb;
   a.part = c->K<float>(p.part_off);
   a.sk_dx = c->sk_dx;
+  a.sk_shape = shape;
   a.part_ld = nblk * 16;
   a.part_rows = a.mblocks * 16;
   if ((size_t)a.sk_slices * a.part_rows * a.part_ld * 4 > p.part_bytes) return fail(GVC_EINVAL, "split-k buffer");
@@ -564,7 +576,8 @@ int32_t run_layer(gvc_ctx* c, int l, const RowMap& rows, int M, float* src, floa
     a.map = MAP_QKV; a.n_pairs = 3 * p.wq[l].Nblk / 2; a.n_out = p.d.d_model; a.KB = p.KBd;
     a.x = reinterpret_cast<const bf16x8*>(X);
     a.e.rows = rows; a.e.q = Q; a.e.kc = c->Kc(l); a.e.vc = c->Vc(l);
-    int32_t r = run_gemm(c, a, EPI_QKV, M, k0, c->big_gemm);
+    int32_t r = c->sk_qkv && c->sk_dx && !c->big_gemm ? run_gemm_sk(c, a, EPI_QKV, M, k0, kSkQkvSlices, SK_WIDE)
+                                                       : run_gemm(c, a, EPI_QKV, M, k0, c->big_gemm);
     if (r) return r;
   }
   {
@@ -600,7 +613,7 @@ int32_t run_layer(gvc_ctx* c, int l, const RowMap& rows, int M, float* src, floa
     a.map = MAP_GU; a.n_pairs = p.wg[l].Nblk; a.n_out = p.F; a.KB = p.KBd;
     a.x = reinterpret_cast<const bf16x8*>(X);
     a.e.rows = rows; a.e.act = A; a.e.kb_act = p.KBf; a.e.n_feat = p.F;
-    int32_t r = c->sk_gemm && !c->big_gemm ? run_gemm_sk(c, a, EPI_SILU, M, k0 + 3, kSkGuSlices)
+    int32_t r = c->sk_gemm && !c->big_gemm ? run_gemm_sk(c, a, EPI_SILU, M, k0 + 3, kSkGuSlices, c->sk_dx ? SK_WIDE : SK_GU)
                                            : run_gemm(c, a, EPI_SILU, M, k0 + 3, c->big_gemm);
     if (r) return r;
   }
@@ -610,7 +623,9 @@ int32_t run_layer(gvc_ctx* c, int l, const RowMap& rows, int M, float* src, floa
     a.map = MAP_PLAIN; a.n_pairs = (p.wd[l].Nblk + 1) / 2; a.n_out = p.d.d_model; a.KB = p.KBf;
     a.x = reinterpret_cast<const bf16x8*>(A);
     a.e.rows = rows; a.e.resid = R; a.e.resid_mapped = 0; a.e.out = dst; a.e.out_mapped = mapped;
-    int32_t r = run_gemm(c, a, EPI_RESID, M, k0 + 4, c->big_gemm);
+    int32_t r = c->sk_down && c->sk_dx && !c->big_gemm
+                    ? run_gemm_sk(c, a, EPI_RESID, M, k0 + 4, kSkDownSlices, SK_NARROW)
+                    : run_gemm(c, a, EPI_RESID, M, k0 + 4, c->big_gemm);
     if (r) return r;
   }
   return GVC_OK;
@@ -863,6 +878,8 @@ int32_t gvc_init_cache(const gvc_desc* desc, const gvc_weights* wt, void* weight
   c->big_gemm = p.B * p.P >= kBigRows;
   if (const char* sk = getenv("GVC_SK")) c->sk_gemm = atoi(sk) != 0;
   if (const char* sc = getenv("GVC_SK_CORE")) c->sk_dx = atoi(sc) != 0;
+  if (const char* e = getenv("GVC_SK_QKV")) c->sk_qkv = atoi(e) != 0;
+  if (const char* e = getenv("GVC_SK_DOWN")) c->sk_down = atoi(e) != 0;
   if (const char* tw = getenv("GVC_BIG_TW")) c->big_tw = atoi(tw);
   if (const char* g = getenv("GVC_GEMM")) {
     if (!strcmp(g, "big")) c->big_gemm = true;

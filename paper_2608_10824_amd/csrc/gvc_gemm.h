@@ -8,6 +8,7 @@ namespace gvc {
 // Work units of a GEMM launch.  Pair maps give a workgroup two 16-row weight
 // blocks whose epilogue partners share lanes; single maps give it one block.
 enum { MAP_PLAIN = 0, MAP_QKV = 1, MAP_GU = 2, MAP_SINGLE = 3, MAP_QKV_SINGLE = 4 };
+enum { SK_GU = 0, SK_WIDE = 1, SK_NARROW = 2 };
 enum { EPI_QKV = 0, EPI_RESID = 1, EPI_SILU = 2, EPI_STORE = 3, EPI_EMBED = 4, EPI_QKV_RAW = 5, EPI_PATCH = 6,
        EPI_GELU = 7 };
 
@@ -73,6 +74,8 @@ struct GemmArgs {
   int sk_slices, sk_steps, sk_groups, part_ld, part_rows;
   int big_tw;           // many-row kernel: token blocks per wave (2, 3 or 4), 0 = chosen per launch
   int sk_dx;            // split-k core: 0 = k_gemm_sk, 1 = k_gemm_dx (decoupled weight and token streams)
+  int sk_shape;         // k_gemm_dx work split: SK_GU (8 waves x 2 blocks), SK_WIDE (12 x 1),
+                        // SK_NARROW (8 x 1); see gemm_sk_group_blocks()
   EpiArgs e;
 };
 

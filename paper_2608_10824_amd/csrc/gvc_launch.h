@@ -37,10 +37,11 @@ hipError_t launch_gather_visual(const bf16* src, const int* idx, const int* pos,
 hipError_t launch_rmsnorm(const float* src, const int* idx, int M, int d, const float* gain, float eps,
                           bf16* x, int KB, bool tiled, hipStream_t s);
 hipError_t launch_gemm_big(const GemmArgs& a, int epi, hipStream_t s);
-// Split-k prompt-pass GEMM (k_gemm_sk, then the slice sum and epilogue);
-// workgroups own groups of gemm_sk_group_blocks() weight blocks.
+// Split-k prompt-pass GEMM (k_gemm_sk or k_gemm_dx, then the slice sum and
+// epilogue); workgroups own groups of gemm_sk_group_blocks(a.sk_shape)
+// weight blocks.
 hipError_t launch_gemm_sk(const GemmArgs& a, int epi, hipStream_t s);
-int gemm_sk_group_blocks();
+int gemm_sk_group_blocks(int sk_shape);
 hipError_t launch_gemm(const GemmArgs& a, int epi, int NT, hipStream_t s);
 // Stage 2 signal of one layer: tv[b * tv_bstride + h * N + n] = sum over the
 // T1 instruction rows after the image of their softmax probability on visual

@@ -679,9 +679,9 @@ __global__ __launch_bounds__(8 * 64) void k_gemm_sk(const GemmArgs a) {
   }
 }
 
-// Split-k core with decoupled operand streams (same work split and partial
-// layout as k_gemm_sk, selected at init): 8 compute waves each stream their
-// PB weight blocks through a private LDS ring of RW fragments (non-temporal
+// Split-k core with decoupled operand streams (the partial layout of
+// k_gemm_sk; with NCW = 8, PB = 2 also its work split): NCW compute waves each
+// stream their PB weight blocks through a private LDS ring of RW fragments (non-temporal
 // direct-to-LDS loads, in k order), and NXW loader waves copy the tile's
 // token fragments into DX LDS stages of KC k steps.  Weight loads then never
 // queue behind token loads in a wave's in-order memory counter, and a
@@ -689,12 +689,12 @@ __global__ __launch_bounds__(8 * 64) void k_gemm_sk(const GemmArgs a) {
 // barrier per chunk hands the token stages over (the stage refilled after
 // the barrier of chunk c last held chunk c - 1, which every compute wave
 // finished before arriving).
-template <int T, int PB, int KC, int DX, int NXW, int RW>
-__global__ __launch_bounds__((8 + NXW) * 64) void k_gemm_dx(const GemmArgs a) {
+template <int T, int NCW, int PB, int KC, int DX, int NXW, int RW>
+__global__ __launch_bounds__((NCW + NXW) * 64) void k_gemm_dx(const GemmArgs a) {
   constexpr int NF = KC * T, ITOK = (NF + NXW - 1) / NXW;
   static_assert((DX - 2) * ITOK < 64 && RW < 64, "vmcnt range");
-  extern __shared__ u32x4b dx_lds[];                 // [8][RW][64] rings, then [DX][NF][64] token stages
-  u32x4b* const xst = dx_lds + 8 * RW * 64;
+  extern __shared__ u32x4b dx_lds[];                 // [NCW][RW][64] rings, then [DX][NF][64] token stages
+  u32x4b* const xst = dx_lds + NCW * RW * 64;
   const int lane = threadIdx.x & 63, wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   int id = blockIdx.x;
   const int g = id % a.sk_groups;
@@ -705,8 +705,8 @@ __global__ __launch_bounds__((8 + NXW) * 64) void k_gemm_dx(const GemmArgs a) {
   const int nch = (nk + KC - 1) / KC;
   const int mb0 = mt * T, nT = min(T, a.mblocks - mb0);
   const int nblk = a.wblk[0] * (a.map == MAP_QKV ? 3 : (a.map == MAP_GU ? 2 : 1));
-  if (wv >= 8) {   // token loader
-    const int x = wv - 8;
+  if (wv >= NCW) {   // token loader
+    const int x = wv - NCW;
     auto issue = [&](int c) {   // chunks past the end re-read the last k step (in bounds)
       u32x4b* st = xst + (c % DX) * NF * 64;
 #pragma unroll
@@ -731,7 +731,7 @@ __global__ __launch_bounds__((8 + NXW) * 64) void k_gemm_dx(const GemmArgs a) {
   int vbs[PB];
 #pragma unroll
   for (int p = 0; p < PB; ++p) {
-    const int vb = (g * 8 + wv) * PB + p;
+    const int vb = (g * NCW + wv) * PB + p;
     vbs[p] = vb;
     const int vc = min(vb, nblk - 1), mat = vc / a.wblk[0], blk = vc % a.wblk[0];
     wp[p] = a.w[mat] + ((size_t)blk * a.KB + kb0) * 64 + lane;
@@ -849,29 +849,45 @@ constexpr int kSkT = 10, kSkNBW = 2, kSkKC = 4, kSkD = 1;
 // 4-step chunks: within 0.05 ms).  On QKV (2 or 4 slices) and the down
 // projection (8 or 16) it does not beat the per-pair kernel.
 constexpr int kDxKC = 2, kDxD = 4, kDxNXW = 2, kDxRW = 8;
+// Wide and narrow projections (QKV; down): one weight block per compute wave,
+// so that a launch of whole k slices fills the 256 compute units with one
+// workgroup each -- QKV 64 groups of 12 blocks x 4 slices, down 32 groups of
+// 8 blocks x 8 slices.  The wide core has 12 compute waves and 3 token stages
+// (156 KiB of LDS).
+constexpr int kDxWideW = 12, kDxWideD = 4, kDxWideR = 6, kDxNarrowW = 8;
 
-template <int T, int PB, int KC, int DX, int NXW, int RW>
+template <int T, int NCW, int PB, int KC, int DX, int NXW, int RW>
 static hipError_t launch_dx_core(const GemmArgs& a, hipStream_t s) {
-  constexpr int lds = (8 * RW + DX * KC * T) * 1024;
+  constexpr int lds = (NCW * RW + DX * KC * T) * 1024;
+  static_assert(lds <= 160 * 1024, "LDS");
   static bool attr = false;
   if (!attr) {
-    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_gemm_dx<T, PB, KC, DX, NXW, RW>),
+    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_gemm_dx<T, NCW, PB, KC, DX, NXW, RW>),
                                              hipFuncAttributeMaxDynamicSharedMemorySize, lds);
     if (e != hipSuccess) return e;
     attr = true;
   }
   const int mtiles = (a.mblocks + T - 1) / T;
-  hipLaunchKernelGGL((k_gemm_dx<T, PB, KC, DX, NXW, RW>), dim3(a.sk_groups * a.sk_slices * mtiles),
-                     dim3((8 + NXW) * 64), lds, s, a);
+  hipLaunchKernelGGL((k_gemm_dx<T, NCW, PB, KC, DX, NXW, RW>), dim3(a.sk_groups * a.sk_slices * mtiles),
+                     dim3((NCW + NXW) * 64), lds, s, a);
   return hipGetLastError();
 }
 
-int gemm_sk_group_blocks() { return 8 * kSkNBW; }
+int gemm_sk_group_blocks(int sk_shape) {
+  return sk_shape == SK_WIDE ? kDxWideW : (sk_shape == SK_NARROW ? kDxNarrowW : 8 * kSkNBW);
+}
 
 hipError_t launch_gemm_sk(const GemmArgs& a, int epi, hipStream_t s) {
   if (a.map == MAP_SINGLE || a.map == MAP_QKV_SINGLE || a.e.ssq_in || !a.part) return hipErrorInvalidValue;
-  const hipError_t e = a.sk_dx ? launch_dx_core<kSkT, kSkNBW, kDxKC, kDxD, kDxNXW, kDxRW>(a, s)
-                               : launch_sk_core<kSkT, kSkNBW, kSkKC, kSkD>(a, s);
+  if (a.sk_shape != SK_GU && !a.sk_dx) return hipErrorInvalidValue;   // one-block shapes exist for k_gemm_dx only
+  hipError_t e;
+  if (a.sk_shape == SK_WIDE)
+    e = launch_dx_core<kSkT, kDxWideW, 1, kDxKC, kDxWideD, kDxNXW, kDxWideR>(a, s);
+  else if (a.sk_shape == SK_NARROW)
+    e = launch_dx_core<kSkT, kDxNarrowW, 1, kDxKC, kDxD, kDxNXW, kDxRW>(a, s);
+  else
+    e = a.sk_dx ? launch_dx_core<kSkT, 8, kSkNBW, kDxKC, kDxD, kDxNXW, kDxRW>(a, s)
+                : launch_sk_core<kSkT, kSkNBW, kSkKC, kSkD>(a, s);
   if (e != hipSuccess) return e;
   switch (epi) {
     case EPI_QKV: return launch_sk_epi<EPI_QKV>(a, s);

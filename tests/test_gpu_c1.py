@@ -7,7 +7,9 @@ blocks, the last one partial), each also with the ViT front end (C1V: one
 view, heads of 64; MIDV: two views, heads of 128), whose visual embeddings
 then enter every compared state, and each with the prompt-pass projections
 on the many-row kernel (C1-big, MID-big) that sessions of 1024 or more
-prompt rows use.  Every call goes through the C ABI."""
+prompt rows use, and on the per-pair kernel (C1-pair, MID-pair) in place of
+the split-k shapes that the other sessions use by default.  Every call goes
+through the C ABI."""
 import os
 
 import numpy as np
@@ -26,11 +28,14 @@ def _config_midv():
     return synth.config_mid().with_(name="MIDV", vit_layers=2, vit_dim=256, vit_heads=2, vit_ffn=1024)
 
 
-@pytest.fixture(scope="module", params=["C1", "MID", "C1V", "MIDV", "C1-big", "MID-big"])
+_PER_PAIR = {"GVC_SK": "0", "GVC_SK_QKV": "0", "GVC_SK_DOWN": "0"}
+
+
+@pytest.fixture(scope="module", params=["C1", "MID", "C1V", "MIDV", "C1-big", "MID-big", "C1-pair", "MID-pair"])
 def c1(request):
     from paper_2608_10824_amd.session import Session
     from paper_2608_10824_amd import gvc
-    name = request.param.replace("-big", "")
+    name = request.param.replace("-big", "").replace("-pair", "")
     cfg = {"C1": synth.config_c1, "MID": synth.config_mid, "C1V": synth.config_c1v, "MIDV": _config_midv}[name]()
     w = synth.model_weights(cfg)
     si = synth.step_inputs(cfg, 45 * cfg.n_views)
@@ -39,10 +44,16 @@ def c1(request):
     # sessions of at least 1024 prompt rows use
     if request.param.endswith("-big"):
         os.environ["GVC_GEMM"] = "big"
+    # "-pair": every prompt-pass projection on the per-pair kernel instead of
+    # the split-k shapes (QKV, gate/up, down) that these sessions default to
+    if request.param.endswith("-pair"):
+        os.environ.update(_PER_PAIR)
     try:
         s = Session(cfg, to_dev(w, dev), device=dev)
     finally:
         os.environ.pop("GVC_GEMM", None)
+        for k in _PER_PAIR:
+            os.environ.pop(k, None)
     o = OracleVLA(cfg, w)
     yield cfg, w, si, s, o, dev
     s.close()

@@ -372,13 +372,16 @@ def test_many_row_tile_height_does_not_change_a_row():
 
 def test_split_k_cores_agree_bit_for_bit(monkeypatch):
     """The two split-k cores of the gate/up projection (decoupled weight and
-    token streams, the default, and the register-fed one, GVC_SK_CORE=0) sum
-    each k slice in the same order, so a full and a partial step give the
-    same state bit for bit (MID: 136 rows, 2 k slices)."""
+    token streams in 12-block groups, the default, and the register-fed one
+    in 16-block groups, GVC_SK_CORE=0) sum each k slice in the same order, so
+    a full and a partial step give the same state bit for bit (MID: 136 rows,
+    2 k slices; QKV and down on the per-pair kernel in both runs)."""
     cfg = synth.config_mid()
     w = synth.model_weights(cfg)
     si = synth.step_inputs(cfg, 64)
     states = []
+    monkeypatch.setenv("GVC_SK_QKV", "0")
+    monkeypatch.setenv("GVC_SK_DOWN", "0")
     for core in ("1", "0"):
         monkeypatch.setenv("GVC_SK_CORE", core)
         s = _session(cfg, w)
