@@ -18,7 +18,7 @@ import torch
 
 import synth
 from oracle.vla import OracleVLA
-from tests._parity import TOL, rel_err, to_dev, gpu_k, gpu_v, check_tokens, check_margins
+from tests._parity import TOL, TOL_SLICE, rel_err, rel_err_slices, to_dev, gpu_k, gpu_v, check_tokens, check_margins
 
 pytestmark = pytest.mark.gpu
 
@@ -63,15 +63,20 @@ def _compare_state(cfg, s, o, label, kv_len=None):
     from paper_2608_10824_amd import gvc
     P = cfg.prompt_len
     kv_len = kv_len or P
-    errs = {}
+    errs, slices = {}, {}
     for l in range(cfg.n_layers + 1):
-        errs["H%d" % l] = rel_err(s.read(gvc.STATE_H, l).cpu().numpy(), o.H[l])
+        g, r = s.read(gvc.STATE_H, l).cpu().numpy(), o.H[l]
+        errs["H%d" % l], slices["H%d/row" % l] = rel_err(g, r), rel_err_slices(g, r, 2)
     for l in range(cfg.n_layers):
-        errs["K%d" % l] = rel_err(gpu_k(s, l, kv_len), o.K[l][:, :kv_len])
-        errs["V%d" % l] = rel_err(gpu_v(s, l, kv_len), o.V[l][:, :kv_len])
-    errs["logits"] = rel_err(s.read(gvc.STATE_HEAD_LOGITS).cpu().numpy(), o.head_logits)
+        for name, g, r in (("K", gpu_k(s, l, kv_len), o.K[l][:, :kv_len]),
+                           ("V", gpu_v(s, l, kv_len), o.V[l][:, :kv_len])):
+            errs["%s%d" % (name, l)], slices["%s%d/head" % (name, l)] = rel_err(g, r), rel_err_slices(g, r, 3)
+    g, r = s.read(gvc.STATE_HEAD_LOGITS).cpu().numpy(), o.head_logits
+    errs["logits"], slices["logits/pos"] = rel_err(g, r), rel_err_slices(g, r, g.ndim - 1)
     print(label, {k: "%.2e" % v for k, v in errs.items()})
+    print(label, "per row / head:", {k: "%.2e" % v for k, v in slices.items()})
     bad = {k: v for k, v in errs.items() if not v <= TOL}
+    bad.update({k: v for k, v in slices.items() if not v <= TOL_SLICE})
     assert not bad, "%s: %s" % (label, bad)
 
 

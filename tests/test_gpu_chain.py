@@ -30,11 +30,10 @@ import torch
 import synth
 from oracle.vla import OracleVLA
 from oracle.margin import gate_fires
-from tests._parity import TOL, rel_err, rel_err_slices, check_tokens, check_margins, state64
+from tests._parity import TOL, TOL_SLICE, rel_err, rel_err_slices, check_tokens, check_margins, state64
 
 pytestmark = pytest.mark.gpu
 DEV = torch.device("cuda:0")
-TOL_SLICE = 5e-2
 
 
 def _pair(cfg, oracle_cfg=None):
