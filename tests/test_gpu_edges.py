@@ -214,7 +214,13 @@ def _mid_bins_normaliser():
     return synth.config_mid().with_(norm_full_vocab=False)
 
 
-@pytest.mark.parametrize("cfg_fn", [synth.config_c1, synth.config_mid, _mid_bins_normaliser])
+def _c1_odd_head_blocks():
+    # 1008 logits: 63 LM-head blocks (an odd count), the bins starting at id
+    # 808, inside a block
+    return synth.config_c1().with_(vocab=1008, n_bins=200)
+
+
+@pytest.mark.parametrize("cfg_fn", [synth.config_c1, synth.config_mid, _mid_bins_normaliser, _c1_odd_head_blocks])
 def test_decode_pass_matches_per_step_launches(cfg_fn, monkeypatch):
     """The single-launch decode pass (one episode) and the per-step launches
     compute the same passes: with the same fed-back tokens their logits agree
