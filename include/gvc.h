@@ -267,7 +267,8 @@ int32_t gvc_step_prefill(gvc_ctx* ctx, const uint8_t* frame_t, const int32_t* te
  * (or forced_tokens[b][j] when given); parallel mode reads the action-query
  * rows of the prompt pass.  tokens_out: dev int32 [B][D]; margins_out: dev
  * fp32 [B][D]; logits_out: dev fp32 [B][D][V] or NULL; forced_tokens: dev
- * int32 [B][D] or NULL.  The margins are also kept in the state for
+ * int32 [B][D] or NULL (a fed-back id outside [0, V) is clamped into it
+ * before its embedding row is read).  The margins are also kept in the state for
  * gvc_margin_gate.  Errors: GVC_ESTATE if no prompt pass ran since the last
  * decode, GVC_EINVAL, GVC_EDEVICE. */
 int32_t gvc_decode_actions(gvc_ctx* ctx, int32_t* tokens_out, float* margins_out,

@@ -1191,7 +1191,7 @@ int32_t gvc_decode_actions(gvc_ctx* c, int32_t* tokens_out, float* margins_out, 
     float* lg = c->K<float>(p.logits_off);
     for (int j = 1; j < p.D; ++j) {
       const int* src = forced_tokens ? forced_tokens + (j - 1) : tok + (j - 1);
-      HIP_TRY(launch_embed_tokens(c->W<bf16>(p.embed_off), src, p.D, p.B, p.d.d_model, xdec,
+      HIP_TRY(launch_embed_tokens(c->W<bf16>(p.embed_off), src, p.D, p.B, p.d.d_model, p.V, xdec,
                                   c->W<float>(p.gains_off), c->K<bf16>(p.x_off), p.KBd, c->K<float>(p.ssq_a_off), s));
       const RowMap rows = c->dec_rows(j);
       const int pos = p.P + j - 1;

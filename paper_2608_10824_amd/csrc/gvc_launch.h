@@ -55,7 +55,7 @@ hipError_t launch_attn_prefill(const bf16* q, const bf16* kc, const bf16* vc, co
                                bool grouped, hipStream_t s);
 hipError_t launch_attn_decode(const float* qraw, const float* kraw, bf16* kc, const bf16* vc, const float2* rope,
                               int B, int H, int head_dim, int kv_pad, int pos, bf16* o, int KB, hipStream_t s);
-hipError_t launch_embed_tokens(const bf16* embed, const int* tokens, int tok_stride, int B, int d,
+hipError_t launch_embed_tokens(const bf16* embed, const int* tokens, int tok_stride, int B, int d, int V,
                                float* x, const float* gain, bf16* xn, int KB, float* ssq, hipStream_t s);
 hipError_t launch_logits_reduce(const float* logits, int rows, int V, int bin_lo, int full_vocab,
                                 int* tok_out, float* margin_out, int out_stride, int out_col,

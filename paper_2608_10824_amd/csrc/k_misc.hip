@@ -161,12 +161,12 @@ __global__ void k_im2row(const uint8_t* __restrict__ frame, int views, int img, 
 // Decode input row b: x = E[token], plus the folded-norm input bf16(x * gain)
 // (frag layout) and the row's sum of squares (one part).
 __global__ __launch_bounds__(256) void k_embed_tokens(const bf16* __restrict__ embed, const int* __restrict__ tokens,
-                                                      int tok_stride, int d, float* __restrict__ x,
+                                                      int tok_stride, int d, int V, float* __restrict__ x,
                                                       const float* __restrict__ gain, bf16* __restrict__ xn, int KB,
                                                       float* __restrict__ ssq) {
   __shared__ float red[4];
   const int b = blockIdx.x;
-  const bf16* e = embed + (size_t)tokens[b * tok_stride] * d;
+  const bf16* e = embed + (size_t)min(max(tokens[b * tok_stride], 0), V - 1) * d;   // ids clamped into [0, V)
   float ss = 0.f;
   for (int f = threadIdx.x * 4; f < d; f += 1024) {
     const float4 v = float4{bf2f(e[f]), bf2f(e[f + 1]), bf2f(e[f + 2]), bf2f(e[f + 3])};
@@ -554,9 +554,9 @@ hipError_t launch_gather_visual(const bf16* src, const int* idx, const int* pos,
   return hipGetLastError();
 }
 
-hipError_t launch_embed_tokens(const bf16* embed, const int* tokens, int tok_stride, int B, int d, float* x,
+hipError_t launch_embed_tokens(const bf16* embed, const int* tokens, int tok_stride, int B, int d, int V, float* x,
                                const float* gain, bf16* xn, int KB, float* ssq, hipStream_t s) {
-  hipLaunchKernelGGL(k_embed_tokens, dim3(B), dim3(256), 0, s, embed, tokens, tok_stride, d, x, gain, xn, KB, ssq);
+  hipLaunchKernelGGL(k_embed_tokens, dim3(B), dim3(256), 0, s, embed, tokens, tok_stride, d, V, x, gain, xn, KB, ssq);
   return hipGetLastError();
 }
 

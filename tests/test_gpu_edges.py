@@ -262,6 +262,32 @@ def test_decode_pass_matches_per_step_launches(cfg_fn, monkeypatch):
     assert rel_err(got["fused"][2], got["split"][2]) <= TOL
 
 
+@pytest.mark.parametrize("mode", ["single", "legacy"])
+def test_forced_tokens_outside_the_vocabulary_are_clamped(mode, monkeypatch):
+    """A fed-back id below 0 or at or above V reads the embedding row of 0 or
+    V - 1: the decode equals, bit for bit, the one fed those ids (single-launch
+    pass and per-step launches)."""
+    cfg = synth.config_c1()
+    w = synth.model_weights(cfg)
+    si = synth.step_inputs(cfg, 0)
+    if mode == "legacy":
+        monkeypatch.setenv("GVC_DECODE", "legacy")
+    V, D = cfg.vocab, cfg.n_decode
+    wild = [V + 7, -3, V, 5, -1, 2 * V, 0][:D]
+    tame = [min(max(t, 0), V - 1) for t in wild]
+    got = []
+    for ids in (wild, tame):
+        s = _session(cfg, w)
+        s.step_prefill(si["frame_prev"].to(DEV), si["text_ids"].to(DEV))
+        forced = torch.tensor([ids], dtype=torch.int32, device=DEV)
+        tok, mg, lg = s.decode_actions(logits=True, forced_tokens=forced)
+        s.margin_gate()
+        got.append((tok.cpu().numpy(), mg.cpu().numpy(), lg.cpu().numpy()))
+        s.close()
+    for a, b in zip(*got):
+        assert np.array_equal(a, b)
+
+
 @pytest.mark.parametrize("name", ["C1V-B2", "C4T-bidir-B2"])
 def test_batched_front_end_and_action_block(name):
     """Two episodes at once: the ViT front end (two views, so four view
