@@ -246,7 +246,7 @@ int32_t gvc_select_static_noalloc(const gvc_desc* desc, const uint8_t* frame_t, 
                                   uint8_t* reuse_mask, int32_t* n_static, void* stream);
 
 /* The prompt pass (Alg. 1, full or partial forward).  frame_t: dev uint8
- * [B][n_views][img][img][3]; text_ids: dev int32 [B][n_text] (ids < V);
+ * [B][n_views][img][img][3]; text_ids: dev int32 [B][n_text] (ids in [0, V); others are clamped into it);
  * extra_rows: dev fp32 [B][n_proprio + n_action_q][d] given embeddings, or
  * NULL when there are none; reuse_mask: dev uint8 [B][L][N] from
  * gvc_select_static, or NULL for a full pass.  Episodes whose cache is

@@ -1148,7 +1148,7 @@ int32_t gvc_step_prefill(gvc_ctx* c, const uint8_t* frame_t, const int32_t* text
       a.map = MAP_PLAIN; a.n_pairs = (p.patch.Nblk + 1) / 2; a.n_out = p.d.d_model; a.KB = p.KBp;
     }
     a.x = reinterpret_cast<const bf16x8*>(X);
-    a.e.rows = r0; a.e.h0 = c->H(0); a.e.embed = c->W<bf16>(p.embed_off); a.e.text_ids = text_ids;
+    a.e.rows = r0; a.e.h0 = c->H(0); a.e.embed = c->W<bf16>(p.embed_off); a.e.text_ids = text_ids; a.e.n_vocab = p.V;
     a.e.extra = extra_rows; a.e.n_patches = p.N; a.e.n_text = p.d.n_text; a.e.n_extra = p.n_extra;
     int32_t r = run_gemm(c, a, EPI_EMBED, c->counts[0], GVC_K_EMBED, c->big_gemm);
     if (r) return r;

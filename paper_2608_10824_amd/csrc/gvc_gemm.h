@@ -44,7 +44,7 @@ struct EpiArgs {
   float* store; int ld_store;
   // EPI_EMBED
   float* h0; const bf16* embed; const int* text_ids; const float* extra;
-  int n_patches, n_text, n_extra;
+  int n_patches, n_text, n_extra, n_vocab;   // text ids are clamped into [0, n_vocab)
   // Folded RMSNorm (decode): the GEMM input is bf16(x * gain) and the
   // accumulator is scaled by 1/sqrt(sum(x^2)/norm_dim + norm_eps), the sum
   // of squares of row m being the sum of ssq_in[m * ssq_parts + 0..parts-1].

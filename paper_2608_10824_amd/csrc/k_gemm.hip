@@ -230,7 +230,7 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, int pair, int lane, 
         }
       } else if (pos < e.n_patches + e.n_text) {
         const int t = pos == 0 ? 0 : pos - e.n_patches;
-        const bf16* er = e.embed + (size_t)e.text_ids[b * e.n_text + t] * d + f;
+        const bf16* er = e.embed + (size_t)min(max(e.text_ids[b * e.n_text + t], 0), e.n_vocab - 1) * d + f;
         o.x = bf2f(er[0]); o.y = bf2f(er[1]); o.z = bf2f(er[2]); o.w = bf2f(er[3]);
       } else {
         const float* xr = e.extra + ((size_t)b * e.n_extra + (pos - e.n_patches - e.n_text)) * d + f;

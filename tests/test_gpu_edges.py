@@ -288,6 +288,27 @@ def test_forced_tokens_outside_the_vocabulary_are_clamped(mode, monkeypatch):
         assert np.array_equal(a, b)
 
 
+def test_text_ids_outside_the_vocabulary_are_clamped():
+    """Prompt text ids below 0 or at or above V embed as 0 or V - 1: the
+    prompt pass gives the same state, bit for bit."""
+    cfg = synth.config_c1()
+    w = synth.model_weights(cfg)
+    si = synth.step_inputs(cfg, 0)
+    V = cfg.vocab
+    wild = si["text_ids"].clone()
+    wild[0, 1], wild[0, 2], wild[0, 3] = V + 3, -7, 2 * V
+    tame = wild.clamp(0, V - 1)
+    states = []
+    for ids in (wild, tame):
+        s = _session(cfg, w)
+        s.step_prefill(si["frame_prev"].to(DEV), ids.to(DEV))
+        states.append(_state(s, cfg))
+        s.close()
+    a, b = states
+    for x, y in zip(a[0] + a[1] + a[2] + [a[3]], b[0] + b[1] + b[2] + [b[3]]):
+        assert np.array_equal(x, y)
+
+
 @pytest.mark.parametrize("name", ["C1V-B2", "C4T-bidir-B2"])
 def test_batched_front_end_and_action_block(name):
     """Two episodes at once: the ViT front end (two views, so four view
