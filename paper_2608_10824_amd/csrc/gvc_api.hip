@@ -304,6 +304,9 @@ struct gvc_ctx {
   // split-k shapes of the decoupled core (GVC_SK_QKV=0, GVC_SK_DOWN=0 turn
   // them off)
   bool sk_qkv = true, sk_down = true;
+  // those shapes at 161-288 rows in one tile of 18 token blocks per k slice
+  // (GVC_SK_TALL=0: two tiles of 10, testing)
+  bool sk_tall = true;
   // persistent decode pass (k_decode.hip): eligible shape, its grid and LDS
   bool persist = false;
   int persist_wg = 0;
@@ -409,6 +412,7 @@ int32_t run_gemm_sk(gvc_ctx* c, GemmArgs& a, int epi, int M, int cls, int slices
   a.part = c->K<float>(p.part_off);
   a.sk_dx = c->sk_dx;
   a.sk_shape = shape;
+  a.sk_tall = c->sk_tall ? 1 : 0;
   a.part_ld = nblk * 16;
   a.part_rows = a.mblocks * 16;
   if ((size_t)a.sk_slices * a.part_rows * a.part_ld * 4 > p.part_bytes) return fail(GVC_EINVAL, "split-k buffer");
@@ -880,6 +884,7 @@ int32_t gvc_init_cache(const gvc_desc* desc, const gvc_weights* wt, void* weight
   if (const char* sc = getenv("GVC_SK_CORE")) c->sk_dx = atoi(sc) != 0;
   if (const char* e = getenv("GVC_SK_QKV")) c->sk_qkv = atoi(e) != 0;
   if (const char* e = getenv("GVC_SK_DOWN")) c->sk_down = atoi(e) != 0;
+  if (const char* e = getenv("GVC_SK_TALL")) c->sk_tall = atoi(e) != 0;
   if (const char* tw = getenv("GVC_BIG_TW")) c->big_tw = atoi(tw);
   if (const char* g = getenv("GVC_GEMM")) {
     if (!strcmp(g, "big")) c->big_gemm = true;

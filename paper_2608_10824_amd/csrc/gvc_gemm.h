@@ -76,6 +76,8 @@ struct GemmArgs {
   int sk_dx;            // split-k core: 0 = k_gemm_sk, 1 = k_gemm_dx (decoupled weight and token streams)
   int sk_shape;         // k_gemm_dx work split: SK_GU (8 waves x 2 blocks), SK_WIDE (12 x 1),
                         // SK_NARROW (8 x 1); see gemm_sk_group_blocks()
+  int sk_tall;          // SK_WIDE / SK_NARROW at 11-18 token blocks: one tile of 18 blocks per
+                        // k slice instead of two of 10 (0 = always tiles of 10)
   EpiArgs e;
 };
 

@@ -855,6 +855,13 @@ constexpr int kDxKC = 2, kDxD = 4, kDxNXW = 2, kDxRW = 8;
 // 8 blocks x 8 slices.  The wide core has 12 compute waves and 3 token stages
 // (156 KiB of LDS).
 constexpr int kDxWideW = 12, kDxWideD = 4, kDxWideR = 6, kDxNarrowW = 8;
+// Tall tiles: a launch of 11-18 token blocks (161-288 rows) as one tile of
+// 18 blocks per k slice, so each slice's weights leave HBM once instead of
+// once per 160-row tile (two rounds of workgroups, each streaming them
+// again); two token stages make room for the taller stages beside the rings
+// (wide 144 KiB, narrow 136 KiB of LDS).  A slice's partial sums are the same
+// MFMA sequence in either tiling, so they are bit-identical.
+constexpr int kSkTallT = 18, kDxTallD = 2;
 
 template <int T, int NCW, int PB, int KC, int DX, int NXW, int RW>
 static hipError_t launch_dx_core(const GemmArgs& a, hipStream_t s) {
@@ -880,11 +887,14 @@ int gemm_sk_group_blocks(int sk_shape) {
 hipError_t launch_gemm_sk(const GemmArgs& a, int epi, hipStream_t s) {
   if (a.map == MAP_SINGLE || a.map == MAP_QKV_SINGLE || a.e.ssq_in || !a.part) return hipErrorInvalidValue;
   if (a.sk_shape != SK_GU && !a.sk_dx) return hipErrorInvalidValue;   // one-block shapes exist for k_gemm_dx only
+  const bool tall = a.sk_tall && a.mblocks > kSkT && a.mblocks <= kSkTallT;
   hipError_t e;
   if (a.sk_shape == SK_WIDE)
-    e = launch_dx_core<kSkT, kDxWideW, 1, kDxKC, kDxWideD, kDxNXW, kDxWideR>(a, s);
+    e = tall ? launch_dx_core<kSkTallT, kDxWideW, 1, kDxKC, kDxTallD, kDxNXW, kDxWideR>(a, s)
+             : launch_dx_core<kSkT, kDxWideW, 1, kDxKC, kDxWideD, kDxNXW, kDxWideR>(a, s);
   else if (a.sk_shape == SK_NARROW)
-    e = launch_dx_core<kSkT, kDxNarrowW, 1, kDxKC, kDxD, kDxNXW, kDxRW>(a, s);
+    e = tall ? launch_dx_core<kSkTallT, kDxNarrowW, 1, kDxKC, kDxTallD, kDxNXW, kDxRW>(a, s)
+             : launch_dx_core<kSkT, kDxNarrowW, 1, kDxKC, kDxD, kDxNXW, kDxRW>(a, s);
   else
     e = a.sk_dx ? launch_dx_core<kSkT, 8, kSkNBW, kDxKC, kDxD, kDxNXW, kDxRW>(a, s)
                 : launch_sk_core<kSkT, kSkNBW, kSkKC, kSkD>(a, s);

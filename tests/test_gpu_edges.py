@@ -423,6 +423,33 @@ def test_many_row_tile_height_does_not_change_a_row():
             assert all(np.array_equal(a, b) for a, b in zip(flat, ref)), "tile height %s" % tw
 
 
+def test_tall_split_k_tiles_agree_bit_for_bit(monkeypatch):
+    """At 161-288 rows the split-k projections run one tile of 18 token
+    blocks per k slice instead of two tiles of 10 (GVC_SK_TALL=0); each
+    slice's partial sums are the same MFMA sequence either way, so a full
+    step over 264 rows (MID with four views: 17 token blocks) and a partial
+    step give the same state bit for bit."""
+    cfg = synth.config_mid().with_(n_views=4)
+    w = synth.model_weights(cfg)
+    si = synth.step_inputs(cfg, 96)
+    states = []
+    for tall in ("1", "0"):
+        monkeypatch.setenv("GVC_SK_TALL", tall)
+        s = _session(cfg, w)
+        monkeypatch.delenv("GVC_SK_TALL")
+        fp, ft, ids = si["frame_prev"].to(DEV), si["frame_t"].to(DEV), si["text_ids"].to(DEV)
+        s.step_prefill(fp, ids)
+        s.decode_actions()
+        s.margin_gate(force=[0])
+        mask, _ = s.select_static(ft, fp)
+        s.step_prefill(ft, ids, None, mask)
+        states.append(_state(s, cfg))
+        s.close()
+    a, b = states
+    for x, y in zip(a[0] + a[1] + a[2] + [a[3]], b[0] + b[1] + b[2] + [b[3]]):
+        assert np.array_equal(x, y)
+
+
 def test_split_k_cores_agree_bit_for_bit(monkeypatch):
     """The two split-k cores of the gate/up projection (decoupled weight and
     token streams in 12-block groups, the default, and the register-fed one
