@@ -307,6 +307,9 @@ struct gvc_ctx {
   // those shapes at 161-288 rows in one tile of 18 token blocks per k slice
   // (GVC_SK_TALL=0: two tiles of 10, testing)
   bool sk_tall = true;
+  // the output projection on the narrow split-k shape where tall tiles apply
+  // (GVC_SK_O=0: the per-pair kernel at every height)
+  bool sk_o = true;
   // persistent decode pass (k_decode.hip): eligible shape, its grid and LDS
   bool persist = false;
   int persist_wg = 0;
@@ -602,7 +605,10 @@ int32_t run_layer(gvc_ctx* c, int l, const RowMap& rows, int M, float* src, floa
     a.map = MAP_PLAIN; a.n_pairs = (p.wo[l].Nblk + 1) / 2; a.n_out = p.d.d_model; a.KB = p.KBd;
     a.x = reinterpret_cast<const bf16x8*>(O);
     a.e.rows = rows; a.e.resid = src; a.e.resid_mapped = mapped; a.e.out = R; a.e.out_mapped = 0;
-    int32_t r = run_gemm(c, a, EPI_RESID, M, k0 + 2, c->big_gemm);
+    // 8 k slices: the per-pair kernel's 8 k shares, summed in the same order
+    const bool o_sk = c->sk_o && c->sk_tall && c->sk_dx && !c->big_gemm && gemm_sk_tall_rows(M);
+    int32_t r = o_sk ? run_gemm_sk(c, a, EPI_RESID, M, k0 + 2, kSkDownSlices, SK_NARROW)
+                     : run_gemm(c, a, EPI_RESID, M, k0 + 2, c->big_gemm);
     if (r) return r;
   }
   {
@@ -885,6 +891,7 @@ int32_t gvc_init_cache(const gvc_desc* desc, const gvc_weights* wt, void* weight
   if (const char* e = getenv("GVC_SK_QKV")) c->sk_qkv = atoi(e) != 0;
   if (const char* e = getenv("GVC_SK_DOWN")) c->sk_down = atoi(e) != 0;
   if (const char* e = getenv("GVC_SK_TALL")) c->sk_tall = atoi(e) != 0;
+  if (const char* e = getenv("GVC_SK_O")) c->sk_o = atoi(e) != 0;
   if (const char* tw = getenv("GVC_BIG_TW")) c->big_tw = atoi(tw);
   if (const char* g = getenv("GVC_GEMM")) {
     if (!strcmp(g, "big")) c->big_gemm = true;

@@ -42,6 +42,9 @@ hipError_t launch_gemm_big(const GemmArgs& a, int epi, hipStream_t s);
 // weight blocks.
 hipError_t launch_gemm_sk(const GemmArgs& a, int epi, hipStream_t s);
 int gemm_sk_group_blocks(int sk_shape);
+// Whether a split-k launch of M rows takes one tall tile per k slice (the
+// wide and narrow shapes at 161-288 rows).
+bool gemm_sk_tall_rows(int M);
 hipError_t launch_gemm(const GemmArgs& a, int epi, int NT, hipStream_t s);
 // Stage 2 signal of one layer: tv[b * tv_bstride + h * N + n] = sum over the
 // T1 instruction rows after the image of their softmax probability on visual

@@ -858,10 +858,12 @@ constexpr int kDxWideW = 12, kDxWideD = 4, kDxWideR = 6, kDxNarrowW = 8;
 // Tall tiles: a launch of 11-18 token blocks (161-288 rows) as one tile of
 // 18 blocks per k slice, so each slice's weights leave HBM once instead of
 // once per 160-row tile (two rounds of workgroups, each streaming them
-// again); two token stages make room for the taller stages beside the rings
-// (wide 144 KiB, narrow 136 KiB of LDS).  A slice's partial sums are the same
-// MFMA sequence in either tiling, so they are bit-identical.
-constexpr int kSkTallT = 18, kDxTallD = 2;
+// again).  The taller token stages fit beside the rings with 3 stages and
+// 4-fragment rings in the wide shape (156 KiB of LDS), 2 stages in the narrow
+// one (136 KiB); 1-step chunks in 3-4 stages, 4 loader waves, 8-fragment
+// rings and a separate 14-block tile measured within 1%.  A slice's partial
+// sums are the same MFMA sequence in either tiling, so they are bit-identical.
+constexpr int kSkTallT = 18, kDxTallWideD = 3, kDxTallWideR = 4, kDxTallNarrowD = 2;
 
 template <int T, int NCW, int PB, int KC, int DX, int NXW, int RW>
 static hipError_t launch_dx_core(const GemmArgs& a, hipStream_t s) {
@@ -880,6 +882,11 @@ static hipError_t launch_dx_core(const GemmArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
+bool gemm_sk_tall_rows(int M) {
+  const int mblocks = (M + 15) / 16;
+  return mblocks > kSkT && mblocks <= kSkTallT;
+}
+
 int gemm_sk_group_blocks(int sk_shape) {
   return sk_shape == SK_WIDE ? kDxWideW : (sk_shape == SK_NARROW ? kDxNarrowW : 8 * kSkNBW);
 }
@@ -887,13 +894,13 @@ int gemm_sk_group_blocks(int sk_shape) {
 hipError_t launch_gemm_sk(const GemmArgs& a, int epi, hipStream_t s) {
   if (a.map == MAP_SINGLE || a.map == MAP_QKV_SINGLE || a.e.ssq_in || !a.part) return hipErrorInvalidValue;
   if (a.sk_shape != SK_GU && !a.sk_dx) return hipErrorInvalidValue;   // one-block shapes exist for k_gemm_dx only
-  const bool tall = a.sk_tall && a.mblocks > kSkT && a.mblocks <= kSkTallT;
+  const bool tall = a.sk_tall && gemm_sk_tall_rows(a.M);
   hipError_t e;
   if (a.sk_shape == SK_WIDE)
-    e = tall ? launch_dx_core<kSkTallT, kDxWideW, 1, kDxKC, kDxTallD, kDxNXW, kDxWideR>(a, s)
+    e = tall ? launch_dx_core<kSkTallT, kDxWideW, 1, kDxKC, kDxTallWideD, kDxNXW, kDxTallWideR>(a, s)
              : launch_dx_core<kSkT, kDxWideW, 1, kDxKC, kDxWideD, kDxNXW, kDxWideR>(a, s);
   else if (a.sk_shape == SK_NARROW)
-    e = tall ? launch_dx_core<kSkTallT, kDxNarrowW, 1, kDxKC, kDxTallD, kDxNXW, kDxRW>(a, s)
+    e = tall ? launch_dx_core<kSkTallT, kDxNarrowW, 1, kDxKC, kDxTallNarrowD, kDxNXW, kDxRW>(a, s)
              : launch_dx_core<kSkT, kDxNarrowW, 1, kDxKC, kDxD, kDxNXW, kDxRW>(a, s);
   else
     e = a.sk_dx ? launch_dx_core<kSkT, 8, kSkNBW, kDxKC, kDxD, kDxNXW, kDxRW>(a, s)

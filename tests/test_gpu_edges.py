@@ -425,10 +425,12 @@ def test_many_row_tile_height_does_not_change_a_row():
 
 def test_tall_split_k_tiles_agree_bit_for_bit(monkeypatch):
     """At 161-288 rows the split-k projections run one tile of 18 token
-    blocks per k slice instead of two tiles of 10 (GVC_SK_TALL=0); each
-    slice's partial sums are the same MFMA sequence either way, so a full
-    step over 264 rows (MID with four views: 17 token blocks) and a partial
-    step give the same state bit for bit."""
+    blocks per k slice instead of two tiles of 10, and the output projection
+    runs on the split-k core in 8 k slices instead of the per-pair kernel's
+    8 k shares (GVC_SK_TALL=0 turns both off).  Each slice's partial sums are
+    the same MFMA sequence either way and are added in the same order, so a
+    full step over 264 rows (MID with four views: 17 token blocks) and a
+    partial step give the same state bit for bit."""
     cfg = synth.config_mid().with_(n_views=4)
     w = synth.model_weights(cfg)
     si = synth.step_inputs(cfg, 96)
