@@ -29,10 +29,11 @@ int32_t fail(int32_t code, const std::string& msg) {
 
 constexpr size_t kAlign = 256;
 constexpr int kMaxNT = 5;   // token blocks per GEMM workgroup (best of 2..16 on the 7B prompt pass)
-// Vision front-end launches of up to 256 rows (one view; 2-8 MB of weights,
-// k ranges of 1024-4096): tiles of 2 token blocks, twice the workgroups of
-// 4-block tiles (ViT-L front end 2.07 -> 1.91 ms per step; 1 or 3 blocks
-// slower).  A row's result does not depend on the tile.
+// Vision front-end launches of up to 256 rows (one view) with at most 64
+// weight pairs (the 1024-wide output and fc2 projections): tiles of 2 token
+// blocks, twice the workgroups of 4-block tiles (ViT-L: 9.5 -> 6.8 and 16.5
+// -> 12.5 us per launch; QKV equal, fc1 slower, 1 or 3 blocks slower).  A
+// row's result does not depend on the tile.
 constexpr int kVitNT = 2;
 constexpr int kBigRows = 1024;  // sessions with at least this many prompt rows use k_gemm_big
 // Split-k prompt-pass GEMMs (k_gemm_dx, or k_gemm_sk with GVC_SK_CORE=0) of
@@ -440,7 +441,7 @@ int32_t run_gemm(gvc_ctx* c, GemmArgs& a, int epi, int M, int cls, bool big = fa
     return GVC_OK;
   }
   tile_gemm(a, M, c->force_splits);
-  if (cls == GVC_K_VIT && a.mblocks <= 16) a.mtiles = (a.mblocks + kVitNT - 1) / kVitNT;
+  if (cls == GVC_K_VIT && a.mblocks <= 16 && a.n_pairs <= 64) a.mtiles = (a.mblocks + kVitNT - 1) / kVitNT;
   // the folded RMSNorm reads at most 16 partial sums per lane, 4 lanes per wave per row
   if (a.e.ssq_in && (a.mblocks > 1 || a.e.ssq_parts > 16 * 4 * a.splits))
     return fail(GVC_EINVAL, "folded norm needs one token block and at most 32 parts per wave");
