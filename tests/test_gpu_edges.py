@@ -423,15 +423,18 @@ def test_many_row_tile_height_does_not_change_a_row():
             assert all(np.array_equal(a, b) for a, b in zip(flat, ref)), "tile height %s" % tw
 
 
-def test_tall_split_k_tiles_agree_bit_for_bit(monkeypatch):
+@pytest.mark.parametrize("views,text", [(2, 33), (4, 8), (4, 32)], ids=["161-rows", "264-rows", "288-rows"])
+def test_tall_split_k_tiles_agree_bit_for_bit(views, text, monkeypatch):
     """At 161-288 rows the split-k projections run one tile of 18 token
     blocks per k slice instead of two tiles of 10, and the output projection
     runs on the split-k core in 8 k slices instead of the per-pair kernel's
     8 k shares (GVC_SK_TALL=0 turns both off).  Each slice's partial sums are
     the same MFMA sequence either way and are added in the same order, so a
-    full step over 264 rows (MID with four views: 17 token blocks) and a
-    partial step give the same state bit for bit."""
-    cfg = synth.config_mid().with_(n_views=4)
+    full step and a partial step give the same state bit for bit.  MID
+    with 161, 264 and 288 prompt rows: 11, 17 and 18 token blocks, the
+    lowest and highest heights that take a tall tile."""
+    cfg = synth.config_mid().with_(n_views=views, n_text=text)
+    assert 160 < cfg.prompt_len <= 288
     w = synth.model_weights(cfg)
     si = synth.step_inputs(cfg, 96)
     states = []
