@@ -423,8 +423,9 @@ def test_many_row_tile_height_does_not_change_a_row():
             assert all(np.array_equal(a, b) for a, b in zip(flat, ref)), "tile height %s" % tw
 
 
-@pytest.mark.parametrize("views,text", [(2, 33), (4, 8), (4, 32)], ids=["161-rows", "264-rows", "288-rows"])
-def test_tall_split_k_tiles_agree_bit_for_bit(views, text, monkeypatch):
+@pytest.mark.parametrize("views,text,batch", [(2, 33, 1), (4, 8, 1), (4, 32, 1), (2, 8, 2)],
+                         ids=["161-rows", "264-rows", "288-rows", "2x136-rows"])
+def test_tall_split_k_tiles_agree_bit_for_bit(views, text, batch, monkeypatch):
     """At 161-288 rows the split-k projections run one tile of 18 token
     blocks per k slice instead of two tiles of 10, and the output projection
     runs on the split-k core in 8 k slices instead of the per-pair kernel's
@@ -432,9 +433,10 @@ def test_tall_split_k_tiles_agree_bit_for_bit(views, text, monkeypatch):
     the same MFMA sequence either way and are added in the same order, so a
     full step and a partial step give the same state bit for bit.  MID
     with 161, 264 and 288 prompt rows: 11, 17 and 18 token blocks, the
-    lowest and highest heights that take a tall tile."""
-    cfg = synth.config_mid().with_(n_views=views, n_text=text)
-    assert 160 < cfg.prompt_len <= 288
+    lowest and highest heights that take a tall tile; and two episodes of
+    136 rows in one launch."""
+    cfg = synth.config_mid().with_(n_views=views, n_text=text, batch=batch)
+    assert 160 < cfg.batch * cfg.prompt_len <= 288
     w = synth.model_weights(cfg)
     si = synth.step_inputs(cfg, 96)
     states = []
@@ -445,7 +447,7 @@ def test_tall_split_k_tiles_agree_bit_for_bit(views, text, monkeypatch):
         fp, ft, ids = si["frame_prev"].to(DEV), si["frame_t"].to(DEV), si["text_ids"].to(DEV)
         s.step_prefill(fp, ids)
         s.decode_actions()
-        s.margin_gate(force=[0])
+        s.margin_gate(force=[0] * cfg.batch)
         mask, _ = s.select_static(ft, fp)
         s.step_prefill(ft, ids, None, mask)
         states.append(_state(s, cfg))
