@@ -674,7 +674,7 @@ __global__ __launch_bounds__(8 * 64) void k_gemm_sk(const GemmArgs a) {
     for (int t = 0; t < T; ++t) {
       if (t >= nT) continue;
       const int m = (mb0 + t) * 16 + col;
-      *(floatx4*)(a.part + ((size_t)s * a.part_rows + m) * a.part_ld + vbs[j] * 16 + sub) = acc[j][t];
+      if (m < a.M) *(floatx4*)(a.part + ((size_t)s * a.part_rows + m) * a.part_ld + vbs[j] * 16 + sub) = acc[j][t];
     }
   }
 }
@@ -788,7 +788,8 @@ __global__ __launch_bounds__((NCW + NXW) * 64) void k_gemm_dx(const GemmArgs a) 
     for (int t = 0; t < T; ++t) {
       if (t >= nT) continue;
       const int m = (mb0 + t) * 16 + col;
-      *(floatx4*)(a.part + ((size_t)s * a.part_rows + m) * a.part_ld + vbs[p] * 16 + sub) = acc[p][t];
+      if (m < a.M)   // rows past the last one are never summed
+        *(floatx4*)(a.part + ((size_t)s * a.part_rows + m) * a.part_ld + vbs[p] * 16 + sub) = acc[p][t];
     }
   }
 }
@@ -809,11 +810,12 @@ __global__ __launch_bounds__(256) void k_gemm_sk_epi(const GemmArgs a) {
   const int m = mb * 16 + (lane & 15), sub = (lane >> 4) * 4;
   const int fa = (ma * a.wblk[0] + ba) * 16 + sub, fb = (mb2 * a.wblk[0] + bb) * 16 + sub;
   floatx4 va = {0, 0, 0, 0}, vb = {0, 0, 0, 0};
-  for (int s = 0; s < a.sk_slices; ++s) {
-    const float* row = a.part + ((size_t)s * a.part_rows + m) * a.part_ld;
-    va += *(const floatx4*)(row + fa);
-    if (b_ok) vb += *(const floatx4*)(row + fb);
-  }
+  if (m < a.M)   // the cores store no partial sums for rows past the last one
+    for (int s = 0; s < a.sk_slices; ++s) {
+      const float* row = a.part + ((size_t)s * a.part_rows + m) * a.part_ld;
+      va += *(const floatx4*)(row + fa);
+      if (b_ok) vb += *(const floatx4*)(row + fb);
+    }
   epilogue<EPI>(a, pair, lane, min(m, a.M - 1), va, vb, b_ok, m < a.M, 1.0f);
 }
 
